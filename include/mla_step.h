@@ -1,0 +1,131 @@
+/*
+ * mla_step.h -- C ABI of the MI355X (gfx950) mixed-step latent-attention
+ * library (libmlastep.so).
+ *
+ * One decode-node step of the serving scheme in the paper: in-flight decode
+ * rows (one new token per request) mixed with the chunked-prefill rows of
+ * deflected requests (section 2.3 "Chunked Prefill"; section 4.3.1, Eq. 4:
+ * a step carries B_n decode tokens plus chi - B_n prefill tokens over a node
+ * whose cache holds K_n tokens; section 4.3.2, Eq. 5: chunk i of a request
+ * starts after the sum of its earlier chunks).  The attention is the absorbed
+ * multi-head latent attention of the model the paper serves (DeepSeek-V2-Lite,
+ * section 6): 16 query heads share one cached 576-dim latent per token (512
+ * compressed dims + 64 rope dims); the value is the latent's first 512 dims.
+ *
+ * Per request r: p_r = prefix_lens[r] tokens are already cached, c_r =
+ * q_lens[r] >= 1 tokens are new this step (a decode row has c_r = 1).  The
+ * rows of all requests are concatenated in request order: request r owns rows
+ * cu_q[r] .. cu_q[r+1]-1, cu_q[0] = 0, T = cu_q[R].
+ *
+ *   append_latent_kv:  for t in [p_r, p_r + c_r):
+ *       kv_cache[bt[r][t / P]][t % P][:] = new_latents[cu_q[r] + t - p_r][:]
+ *   mixed_step_attn:   row i of request r (0 <= i < c_r) attends the keys
+ *       j = 0 .. p_r + i of its pages (bottom-right causal), for each head h:
+ *       s_j = scale * <q[row][h][0:576], k_j[0:576]>,
+ *       out[row][h][e] = sum_j softmax(s)_j * k_j[e]  (e < 512),
+ *       lse[row][h] = log sum_j exp(s_j)  (natural log).
+ *   Attention reads the appended latents from the cache: call append first,
+ *   on the same stream.
+ *
+ * Conventions
+ *   - bf16 values travel as uint16_t bit patterns.  All pointers are plain
+ *     device or host addresses as marked; device arrays are contiguous and
+ *     16-byte aligned.  The caller allocates and frees everything; the
+ *     library keeps no pointer after a call returns and allocates no device
+ *     memory.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Entry
+ *     points only enqueue work and never synchronise; a device fault shows up
+ *     at the caller's next synchronisation.
+ *   - Every entry point returns MLA_OK or a negative mla_status and, on error,
+ *     sets a thread-local message (mla_last_error).  All arguments are checked
+ *     on the host before anything is enqueued; nothing is launched on error.
+ *   - Device arrays must hold the same values as their host twins (q_lens /
+ *     prefix_lens).  Block-table entries are not read on the host; kernels
+ *     guard every page id (an id outside [0, num_pages) is never dereferenced:
+ *     append skips that slot, attention reads page 0 in its place) so a bad
+ *     table gives wrong numbers, not a memory fault.
+ *   - Two requests must not map the same written slot (undefined result).
+ *   - Reentrant; concurrent calls on different streams need distinct
+ *     workspaces.
+ */
+#ifndef MLA_STEP_H
+#define MLA_STEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MLA_ABI_VERSION 1
+#define MLA_NUM_HEADS 16
+#define MLA_D_QK 576 /* latent width: 512 compressed + 64 rope dims */
+#define MLA_D_V 512  /* value width: the first 512 latent dims */
+
+typedef enum {
+    MLA_OK = 0,
+    MLA_ERR_INVALID_ARG = -1, /* null pointer, negative or inconsistent size */
+    MLA_ERR_UNSUPPORTED = -2, /* page size not a power of two in [1, 1024] */
+    MLA_ERR_WORKSPACE = -3,   /* workspace pointer null or too small */
+    MLA_ERR_HIP = -4          /* a HIP runtime call failed (message has details) */
+} mla_status;
+
+typedef enum { MLA_OUT_F32 = 0, MLA_OUT_BF16 = 1 } mla_out_dtype;
+
+/* One step's batch; the same for every layer of the step. */
+typedef struct mla_batch {
+    int32_t num_reqs;          /* R >= 0; R == 0 makes every call a no-op */
+    int32_t page_size;         /* P: tokens per page, power of two in [1, 1024] */
+    int32_t num_pages;         /* pages in the pool (for guards) */
+    int32_t max_pages_per_req; /* block-table row stride, >= ceil((p_r + c_r) / P) */
+    const int32_t *q_lens;     /* HOST [R]: c_r >= 1; read during the call only */
+    const int32_t *prefix_lens;/* HOST [R]: p_r >= 0; read during the call only */
+    const int32_t *cu_q_dev;        /* DEVICE [R + 1]: row offsets (prefix sums of q_lens) */
+    const int32_t *prefix_lens_dev; /* DEVICE [R]: same values as prefix_lens */
+    const int32_t *block_table_dev; /* DEVICE [R][max_pages_per_req]: logical page -> pool page */
+} mla_batch;
+
+/* ABI version of the loaded library (MLA_ABI_VERSION it was built with). */
+int mla_abi_version(void);
+
+/* Message of the last non-OK return on this thread ("" if none). */
+const char *mla_last_error(void);
+
+/* Device workspace (bytes) that mixed_step_attn needs for this batch, or 0 on
+ * invalid arguments (then mla_last_error says why; a valid batch may also need
+ * 0 bytes).  Depends only on the host arrays and the device's CU count. */
+size_t mixed_step_workspace_bytes(const mla_batch *batch);
+
+/* Scatter the step's new latents into the paged cache (the append above).
+ *   new_latents  DEVICE bf16 [T][576], row order of the batch.
+ *   kv_cache     DEVICE bf16 [num_pages][P][576], updated in place; only the
+ *                T written slots change.
+ * Errors: MLA_ERR_INVALID_ARG (null pointer with T > 0, a negative length,
+ * p_r + c_r > max_pages_per_req * P), MLA_ERR_UNSUPPORTED, MLA_ERR_HIP. */
+int append_latent_kv(const mla_batch *batch, const uint16_t *new_latents, uint16_t *kv_cache,
+                     void *stream);
+
+/* Attention of every row of the step (the attend above).
+ *   q              DEVICE bf16 [T][16][576]: absorbed queries (after RoPE).
+ *   kv_cache       DEVICE bf16 [num_pages][P][576], already holding the
+ *                  step's new latents.
+ *   softmax_scale  finite, > 0 (1/sqrt(192) for the served model); applied to
+ *                  the fp32 dot product.
+ *   out            DEVICE [T][16][512], fp32 (MLA_OUT_F32) or bf16 rounded to
+ *                  nearest even (MLA_OUT_BF16).
+ *   lse            DEVICE fp32 [T][16] natural-log sum of exp(s), or NULL.
+ *   workspace      DEVICE scratch of at least mixed_step_workspace_bytes(batch)
+ *                  bytes (may be NULL if that is 0); contents on entry are
+ *                  ignored and on return undefined.
+ * Errors: MLA_ERR_INVALID_ARG, MLA_ERR_UNSUPPORTED, MLA_ERR_WORKSPACE,
+ * MLA_ERR_HIP. */
+int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *kv_cache,
+                    float softmax_scale, void *out, int32_t out_dtype, float *lse,
+                    void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLA_STEP_H */

@@ -1,0 +1,164 @@
+"""Python binding of libmlastep (include/mla_step.h): argument marshalling only.
+
+Every step of the computation runs in the library's HIP kernels; this module
+turns torch tensors into raw pointers and the caller's HIP stream.  There is
+no CPU fallback: if the library is not built, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmlastep.so")
+
+MLA_OK = 0
+MLA_ERR_INVALID_ARG = -1
+MLA_ERR_UNSUPPORTED = -2
+MLA_ERR_WORKSPACE = -3
+MLA_ERR_HIP = -4
+MLA_OUT_F32 = 0
+MLA_OUT_BF16 = 1
+NUM_HEADS, D_QK, D_V = 16, 576, 512
+
+EXPORTED = ("mla_abi_version", "mla_last_error", "mixed_step_workspace_bytes", "append_latent_kv",
+            "mixed_step_attn")
+
+
+class MlaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libmlastep error {code}: {msg}")
+        self.code = code
+
+
+class mla_batch(ctypes.Structure):
+    _fields_ = [
+        ("num_reqs", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+        ("max_pages_per_req", ctypes.c_int32),
+        ("q_lens", ctypes.POINTER(ctypes.c_int32)),
+        ("prefix_lens", ctypes.POINTER(ctypes.c_int32)),
+        ("cu_q_dev", ctypes.c_void_p),
+        ("prefix_lens_dev", ctypes.c_void_p),
+        ("block_table_dev", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmlastep.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_02043_amd/build.py "
+                              "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        L.mla_abi_version.restype = ctypes.c_int
+        L.mla_last_error.restype = ctypes.c_char_p
+        L.mixed_step_workspace_bytes.argtypes = [ctypes.POINTER(mla_batch)]
+        L.mixed_step_workspace_bytes.restype = ctypes.c_size_t
+        L.append_latent_kv.argtypes = [ctypes.POINTER(mla_batch), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        L.append_latent_kv.restype = ctypes.c_int
+        L.mixed_step_attn.argtypes = [ctypes.POINTER(mla_batch), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
+                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_size_t, ctypes.c_void_p]
+        L.mixed_step_attn.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int) -> None:
+    if rc != MLA_OK:
+        raise MlaError(rc, lib().mla_last_error().decode())
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+class DeviceBatch:
+    """Host and device copies of one step's lengths and block table.
+
+    q_lens / prefix_lens stay on the host (numpy int32, kept alive here);
+    cu_q, prefix_lens and the block table are torch int32 tensors on `device`.
+    """
+
+    def __init__(self, q_lens, prefix_lens, block_table, page_size: int, num_pages: int, device="cuda"):
+        import torch
+        self.q_lens = np.ascontiguousarray(q_lens, dtype=np.int32)
+        self.prefix_lens = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+        bt = np.ascontiguousarray(block_table, dtype=np.int32)
+        if bt.ndim != 2 or bt.shape[0] != self.q_lens.shape[0]:
+            raise ValueError("block_table must be [num_reqs][max_pages_per_req]")
+        cu = np.zeros(self.q_lens.shape[0] + 1, dtype=np.int32)
+        np.cumsum(self.q_lens, out=cu[1:])
+        self.num_rows = int(cu[-1])
+        self.cu_q_dev = torch.from_numpy(cu).to(device)
+        self.prefix_dev = torch.from_numpy(self.prefix_lens.copy()).to(device)
+        self.bt_dev = torch.from_numpy(bt.copy()).to(device)
+        self.page_size = int(page_size)
+        self.num_pages = int(num_pages)
+        self.max_pages = int(bt.shape[1])
+        self.c = mla_batch(
+            num_reqs=int(self.q_lens.shape[0]), page_size=self.page_size, num_pages=self.num_pages,
+            max_pages_per_req=self.max_pages,
+            q_lens=self.q_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            prefix_lens=self.prefix_lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            cu_q_dev=_ptr(self.cu_q_dev), prefix_lens_dev=_ptr(self.prefix_dev), block_table_dev=_ptr(self.bt_dev))
+
+    @classmethod
+    def from_batch(cls, batch, device="cuda") -> "DeviceBatch":
+        """From a paper_2607_02043_amd.workloads.Batch."""
+        return cls(batch.q_lens, batch.prefix_lens, batch.block_table, batch.page_size, batch.num_pages, device)
+
+
+def abi_version() -> int:
+    return int(lib().mla_abi_version())
+
+
+def mixed_step_workspace_bytes(batch: DeviceBatch) -> int:
+    n = int(lib().mixed_step_workspace_bytes(ctypes.byref(batch.c)))
+    err = lib().mla_last_error().decode()
+    if n == 0 and err:
+        raise MlaError(MLA_ERR_INVALID_ARG, err)
+    return n
+
+
+def append_latent_kv(batch: DeviceBatch, new_latents, kv_cache, stream=None) -> None:
+    """new_latents: uint16/bf16 [T][576] (device); kv_cache: [num_pages][P][576] updated in place."""
+    _check(lib().append_latent_kv(ctypes.byref(batch.c), _ptr(new_latents), _ptr(kv_cache), _stream(stream)))
+
+
+def mixed_step_attn(batch: DeviceBatch, q, kv_cache, softmax_scale: float, out, lse=None, workspace=None,
+                    stream=None) -> None:
+    """q: [T][16][576] bf16 bits; out: [T][16][512] float32 or bf16 (dtype picks the mode)."""
+    import torch
+    if out.dtype == torch.float32:
+        mode = MLA_OUT_F32
+    elif out.dtype in (torch.bfloat16, torch.uint16, torch.int16):
+        mode = MLA_OUT_BF16
+    else:
+        raise TypeError("out must be float32 or bfloat16")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().mixed_step_attn(ctypes.byref(batch.c), _ptr(q), _ptr(kv_cache), float(softmax_scale), _ptr(out),
+                                 mode, _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def workspace_for(batch: DeviceBatch, device="cuda"):
+    """A workspace tensor of the size mixed_step_attn needs for `batch` (None if 0)."""
+    import torch
+    n = mixed_step_workspace_bytes(batch)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device) if n > 0 else None

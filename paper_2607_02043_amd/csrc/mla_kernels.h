@@ -1,0 +1,64 @@
+// Launch-side description of the kernels of libmlastep (host <-> device).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mla {
+
+constexpr int kHeads = 16;
+constexpr int kDqk = 576;   // latent: 512 compressed + 64 rope dims
+constexpr int kDv = 512;    // value: first 512 latent dims
+constexpr int kRowBytes = kDqk * 2;
+constexpr int kKeysPerTile = 32;
+constexpr int kPageWindow = 256;   // page ids one work item may touch
+constexpr int kThreads = 256;      // 4 wavefronts of 64
+constexpr int kChunkTokensPerWave = 1;
+constexpr int kChunkBlockTokens = 4 * kChunkTokensPerWave;  // tokens per chunk work item
+constexpr int kPartialFloats = kHeads * kDv;                // one row's partial output
+constexpr int kPartialStats = kHeads * 2;                   // one row's (max, sum) per head
+
+struct AttnArgs {
+    const uint16_t *q;
+    const uint16_t *kv;
+    const int32_t *cu_q;
+    const int32_t *prefix;
+    const int32_t *bt;
+    void *out;
+    float *lse;
+    float *ws_chunk_o;    // [n_chunk_items][block tokens][16][512]
+    float *ws_chunk_ml;   // [n_chunk_items][block tokens][16][2]
+    float *ws_dec_o;      // [n_dec_items][16][512]
+    float *ws_dec_ml;     // [n_dec_items][16][2]
+    int32_t num_reqs;
+    int32_t num_rows;
+    int32_t page_size;
+    int32_t log2_page;
+    int32_t max_pages;
+    int32_t num_pages;
+    float scale_log2;     // softmax scale * log2(e)
+    int32_t ks_chunk;     // keys per chunk work item (a multiple of 64)
+    int32_t ks_dec;       // keys per decode work item (a multiple of 64)
+    int32_t n_chunk_items;
+    int32_t n_dec_items;
+    int32_t out_bf16;
+};
+
+struct AppendArgs {
+    const uint16_t *src;
+    uint16_t *kv;
+    const int32_t *cu_q;
+    const int32_t *prefix;
+    const int32_t *bt;
+    int32_t num_reqs;
+    int32_t num_rows;
+    int32_t page_size;
+    int32_t log2_page;
+    int32_t max_pages;
+    int32_t num_pages;
+};
+
+hipError_t launch_append(const AppendArgs &a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, hipStream_t s);
+hipError_t launch_combine(const AttnArgs &a, hipStream_t s);
+
+}  // namespace mla

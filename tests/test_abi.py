@@ -1,0 +1,121 @@
+"""The C ABI library without a GPU: it loads, exports every entry point the
+header declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2607_02043_amd as mla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mla_step.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s*([A-Za-z_][A-Za-z0-9_]*)\s*\(", text, re.M)
+    return sorted(set(n for n in names if n not in ("if", "while", "return")))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    L = mla.lib()
+    declared = _declared_functions()
+    assert set(declared) == set(mla.EXPORTED), declared
+    for name in declared:
+        assert hasattr(L, name), f"libmlastep.so does not export {name}"
+    assert L.mla_abi_version() == 1
+
+
+class _HostBatch:
+    """An mla_batch with host arrays and fake (never dereferenced) device pointers."""
+
+    def __init__(self, q_lens, prefix_lens, page=64, num_pages=100, max_pages=64):
+        self.ql = np.ascontiguousarray(q_lens, dtype=np.int32)
+        self.pl = np.ascontiguousarray(prefix_lens, dtype=np.int32)
+        self.c = mla.mla_batch(
+            num_reqs=len(self.ql), page_size=page, num_pages=num_pages, max_pages_per_req=max_pages,
+            q_lens=self.ql.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            prefix_lens=self.pl.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+            cu_q_dev=0x1000, prefix_lens_dev=0x2000, block_table_dev=0x3000)
+
+
+FAKE = 0x10000  # 16-byte aligned, never touched: every call below fails validation first
+
+
+def _append(b, new=FAKE, kv=FAKE):
+    return mla.lib().append_latent_kv(ctypes.byref(b.c) if b is not None else None, new, kv, None)
+
+
+def _attn(b, scale=0.07, dtype=0, q=FAKE, kv=FAKE, out=FAKE, lse=None):
+    return mla.lib().mixed_step_attn(ctypes.byref(b.c), q, kv, scale, out, dtype, lse, None, 0, None)
+
+
+def _err():
+    return mla.lib().mla_last_error().decode()
+
+
+def test_null_batch_is_rejected():
+    assert mla.lib().append_latent_kv(None, FAKE, FAKE, None) == mla.MLA_ERR_INVALID_ARG
+    assert "NULL" in _err()
+
+
+def test_empty_batch_is_a_no_op():
+    b = _HostBatch([], [])
+    assert _append(b) == mla.MLA_OK
+    assert _attn(b) == mla.MLA_OK
+
+
+@pytest.mark.parametrize("page,code", [(0, mla.MLA_ERR_UNSUPPORTED), (48, mla.MLA_ERR_UNSUPPORTED),
+                                       (2048, mla.MLA_ERR_UNSUPPORTED)])
+def test_page_size_must_be_a_power_of_two(page, code):
+    b = _HostBatch([1], [3], page=page)
+    assert _append(b) == code
+    assert "page_size" in _err()
+
+
+@pytest.mark.parametrize("ql,pl,frag", [([0], [3], "q_lens"), ([1], [-1], "prefix_lens"),
+                                        ([1, 5], [4095, 4092], "exceeds the block table")])
+def test_bad_lengths_are_rejected(ql, pl, frag):
+    b = _HostBatch(ql, pl, page=64, max_pages=64)
+    assert _append(b) == mla.MLA_ERR_INVALID_ARG
+    assert frag in _err()
+    assert _attn(b) == mla.MLA_ERR_INVALID_ARG
+
+
+def test_null_device_pointers_are_rejected():
+    b = _HostBatch([1], [3])
+    assert _append(b, new=None) == mla.MLA_ERR_INVALID_ARG
+    assert _attn(b, q=None) == mla.MLA_ERR_INVALID_ARG
+    assert _attn(b, out=None) == mla.MLA_ERR_INVALID_ARG
+    b.c.block_table_dev = None
+    assert _append(b) == mla.MLA_ERR_INVALID_ARG
+
+
+def test_misaligned_pointers_are_rejected():
+    b = _HostBatch([1], [3])
+    assert _append(b, new=FAKE + 2) == mla.MLA_ERR_INVALID_ARG
+    assert "aligned" in _err()
+    assert _attn(b, q=FAKE + 8) == mla.MLA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("scale", [0.0, -1.0, float("inf"), float("nan")])
+def test_bad_scale_is_rejected(scale):
+    b = _HostBatch([1], [3])
+    assert _attn(b, scale=scale) == mla.MLA_ERR_INVALID_ARG
+    assert "softmax_scale" in _err()
+
+
+def test_bad_out_dtype_is_rejected():
+    b = _HostBatch([1], [3])
+    assert _attn(b, dtype=7) == mla.MLA_ERR_INVALID_ARG
+
+
+def test_error_message_is_cleared_by_a_good_call():
+    b = _HostBatch([1], [3])
+    assert _attn(b, dtype=7) != mla.MLA_OK
+    assert _err() != ""
+    assert _attn(_HostBatch([], [])) == mla.MLA_OK
+    assert _err() == ""

@@ -1,0 +1,118 @@
+"""HIP path vs the fp64 oracle, through the C ABI (needs an MI355X).
+
+Small workloads are compared on every output row; the full-size workloads
+(256-request decode batches, 2048-token chunks over a 6144-token prefix, the
+27-layer step) on sampled rows that the oracle computes one by one.  Append is
+compared bit for bit on the whole pool (NaN canaries included).
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from harness import GpuLayer, assert_close, log, run_layer, sample_rows
+import paper_2607_02043_amd as mla
+from paper_2607_02043_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+EDGE_CASES = {
+    # name: (prefix_lens, q_lens, page_size)
+    "decode_single_key": ([0], [1], 64),
+    "decode_tile_edges": ([30, 31, 32, 63, 64, 65, 95, 127, 128, 255, 256, 257], [1] * 12, 64),
+    "page16_mixed": ([15, 0, 100, 3], [1, 37, 1, 70], 16),
+    "page1": ([5, 0, 40], [1, 9, 1], 1),
+    "page2_ragged_chunk": ([7, 0], [13, 2], 2),
+    "chunk_of_two": ([0], [2], 64),
+    "chunk_unaligned_prefix": ([70, 1], [45, 3], 64),
+    "chunk_long_prefix": ([5000], [37], 64),
+    "page256": ([600, 0, 1000], [1, 300, 1], 256),
+    "chunk_first": ([0, 9, 300], [33, 1, 1], 32),
+}
+
+
+def _compare_all_rows(wl, li, out_bf16=False):
+    b = wl.batch
+    g = run_layer(b, li, out_bf16=out_bf16)
+    pool_ref, out_ref, lse_ref = oracle.step(b, li, W.SOFTMAX_SCALE)
+    assert np.array_equal(g.pool_np(), pool_ref), "append: pool differs from the oracle"
+    if out_bf16:
+        assert_close(g.out_np(), out_ref, g.lse_np(), lse_ref, what=wl.name + " bf16", mean_rel=4e-3)
+    else:
+        assert_close(g.out_np(), out_ref, g.lse_np(), lse_ref, what=wl.name)
+
+
+@pytest.mark.parametrize("name", sorted(EDGE_CASES))
+def test_edge_cases_all_rows(name):
+    prefix, qlen, page = EDGE_CASES[name]
+    log(f"[gpu] edge case {name}: prefix={prefix} q_lens={qlen} page={page}")
+    wl = W.custom(prefix, qlen, page_size=page, seed=zlib.crc32(name.encode()) % 1000, name=name)
+    _compare_all_rows(wl, wl.layer(0))
+
+
+def test_many_requests():
+    rng = np.random.default_rng(5)
+    prefix = list(rng.integers(0, 3000, 300)) + [100, 0]
+    qlen = [1] * 300 + [64, 129]
+    log("[gpu] 302 requests (300 decode + 2 chunks), page 64")
+    wl = W.custom(prefix, qlen, page_size=64, seed=8, name="many_requests")
+    _compare_all_rows(wl, wl.layer(0))
+
+
+@pytest.mark.parametrize("idx", [1, 2])
+def test_config_all_rows(idx):
+    wl = W.config(idx)
+    log(f"[gpu] config {idx}: {wl.name}, all rows")
+    _compare_all_rows(wl, wl.layer(0))
+
+
+def test_config1_bf16_output():
+    wl = W.config(1)
+    log("[gpu] config 1, bf16 output")
+    _compare_all_rows(wl, wl.layer(0), out_bf16=True)
+
+
+def _compare_sampled(b, li, g, what, seed=0):
+    rows = sample_rows(b, seed=seed)
+    pool_ref = oracle.append(b, li.new_latents, li.pool)
+    assert np.array_equal(g.pool_np(), pool_ref), f"{what}: append pool differs"
+    out_ref, lse_ref = oracle.attend(b, li.q, pool_ref, W.SOFTMAX_SCALE, rows=rows)
+    assert_close(g.out_np()[rows], out_ref, g.lse_np()[rows], lse_ref, what=f"{what} ({len(rows)} sampled rows)")
+
+
+def test_config3_full_size_sampled():
+    wl = W.config(3)
+    log(f"[gpu] config 3 full size: {wl.name}")
+    li = wl.layer(0)
+    g = run_layer(wl.batch, li)
+    _compare_sampled(wl.batch, li, g, "config 3")
+
+
+@pytest.mark.parametrize("chunk", [0, 256, 4096])
+def test_config4_full_size_sampled(chunk):
+    wl = W.config(4, chunk=chunk)
+    log(f"[gpu] config 4 full size, chunk {chunk}")
+    li = wl.layer(0)
+    g = run_layer(wl.batch, li)
+    _compare_sampled(wl.batch, li, g, f"config 4 C={chunk}", seed=chunk)
+
+
+def test_config5_27_layers_sampled():
+    import torch
+    wl = W.config(5)
+    log(f"[gpu] config 5: {wl.name}")
+    db = mla.DeviceBatch.from_batch(wl.batch)
+    check = {0: None, 13: None, 26: None}
+    layers = []
+    for layer in range(wl.num_layers):
+        li = wl.layer(layer)
+        layers.append(GpuLayer(db, li))
+        if layer in check:
+            check[layer] = li
+    for g in layers:  # back to back on one stream, as the benchmark runs them
+        g.run()
+    torch.cuda.synchronize()
+    log("  27 layers done")
+    for layer, li in check.items():
+        _compare_sampled(wl.batch, li, layers[layer], f"config 5 layer {layer}", seed=layer)
