@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of one decode-node mixed step (latent append + mixed-step
+attention) on one MI355X, through the C ABI.
+
+Default workload: one layer, 32 decode requests with lognormal contexts
+(median 1024, sigma 1.0, clipped to [16, 8192]) plus one 512-token prefill
+chunk at prefix 0, page size 64 (the paper's scenario of section 3.2: a
+decode batch with a chunked prefill injected).  `--config N` picks another
+workload (1..5; `--chunk C` sets workload 4's chunk length).
+
+Timing: W untimed warm-up steps, then K timed steps bracketed by
+torch.cuda.synchronize().  All inputs are resident in HBM before timing
+starts.  Unless --no-rotate is given, the step cycles through enough
+independent copies of its buffers (pool, queries, new latents, outputs) that
+the rotating working set is >= 1 GiB, four times the 256 MB last-level
+(Infinity) cache, so bytes really come from HBM.
+
+Printed: one JSON line (metric, value = us/step, roofline of the dominant
+kernel from HIP events on its stream, CPU-oracle baseline on rank 0).
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16 MFMA
+ROTATE_TARGET_BYTES = 1 << 30
+METRIC = "mixed-step MLA attention µs/step; TB/s & TFLOP/s as % of combined roofline"
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- work model
+def algorithmic_work(batch, out_bytes_per_elem=4):
+    """Bytes and flops the method must move / compute for one layer.
+
+    attention: every row's keys are read once (1152 B per cached or new latent
+    of each request), queries read once (16 x 576 bf16 per row), outputs
+    written once (16 x 512 per row), lse written (16 fp32 per row), block-table
+    entries read once.  append: new latents read once and written once.
+    flops: 2 x 16 x (576 + 512) per (query token, visible key) pair.
+    """
+    p = batch.prefix_lens.astype(np.int64)
+    c = batch.q_lens.astype(np.int64)
+    T = int(c.sum())
+    keys = int((p + c).sum())
+    pages = int(np.ceil((p + c) / batch.page_size).sum())
+    attn_bytes = 1152 * keys + 18432 * T + 16 * 512 * out_bytes_per_elem * T + 64 * T + 4 * pages + 8 * batch.num_reqs
+    append_bytes = 2 * 1152 * T + 8 * batch.num_reqs
+    pairs = int((c * p + c * (c + 1) // 2).sum())
+    flops = 34816 * pairs
+    return {"attn_bytes": attn_bytes, "append_bytes": append_bytes, "step_bytes": attn_bytes + append_bytes,
+            "flops": flops, "pairs": pairs, "rows": T, "keys": keys}
+
+
+# -------------------------------------------------------------------- bench
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--chunk", type=int, default=2048, help="prefill chunk length of workload 4")
+    ap.add_argument("--out-dtype", choices=["f32", "bf16"], default="f32")
+    ap.add_argument("--no-rotate", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(each decode node is an independent one-GPU unit)"}))
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_02043_amd as mla
+    from paper_2607_02043_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    wl = W.config(args.config, chunk=args.chunk) if args.config == 4 else W.config(args.config)
+    b = wl.batch
+    out_bf16 = args.out_dtype == "bf16"
+    work = algorithmic_work(b, 2 if out_bf16 else 4)
+    L = wl.num_layers
+    log(f"[bench] workload {args.config}: {wl.name}; rows={work['rows']} keys={work['keys']} pairs={work['pairs']}")
+
+    db = mla.DeviceBatch.from_batch(b, device=dev)
+    ws = mla.workspace_for(db, device=dev)
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
+
+    # one buffer set per layer; rotation copies for small steps
+    layer_sets = []
+    t0 = time.time()
+    for layer in range(L):
+        li = wl.layer(layer)
+        layer_sets.append({"pool": up(li.pool), "new": up(li.new_latents), "q": up(li.q)})
+        del li
+    log(f"[bench] inputs generated and uploaded in {time.time() - t0:.1f}s")
+    odt = torch.bfloat16 if out_bf16 else torch.float32
+    set_bytes = sum(s["pool"].numel() * 2 + s["new"].numel() * 2 + s["q"].numel() * 2 for s in layer_sets)
+    set_bytes += L * work["rows"] * 16 * 512 * (2 if out_bf16 else 4)
+    n_rot = 1 if args.no_rotate else max(1, math.ceil(ROTATE_TARGET_BYTES / set_bytes))
+    rotations = []
+    for k in range(n_rot):
+        layers = []
+        for s in layer_sets:
+            d = {key: (v if k == 0 else v.clone()) for key, v in s.items()}
+            d["out"] = torch.empty((work["rows"], 16, 512), dtype=odt, device=dev)
+            d["lse"] = torch.empty((work["rows"], 16), dtype=torch.float32, device=dev)
+            layers.append(d)
+        rotations.append(layers)
+    log(f"[bench] {n_rot} rotating buffer set(s) of {set_bytes / 2**20:.1f} MiB")
+
+    stream = torch.cuda.current_stream()
+    scale = W.SOFTMAX_SCALE
+
+    def step(k, ev=None):
+        for j, d in enumerate(rotations[k % n_rot]):
+            mla.append_latent_kv(db, d["new"], d["pool"], stream)
+            if ev is not None:
+                ev[j][0].record(stream)
+            mla.mixed_step_attn(db, d["q"], d["pool"], scale, d["out"], d["lse"], ws, stream)
+            if ev is not None:
+                ev[j][1].record(stream)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+        del src, dst
+
+    # timed region: whole steps
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(k)
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    us_per_step = t_total / args.steps * 1e6
+
+    # same steps again with HIP events around the attention call (on its stream)
+    evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in range(L)]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        step(k, evs[k])
+    torch.cuda.synchronize()
+    attn_ms = [e0.elapsed_time(e1) for row in evs for e0, e1 in row]
+    attn_us = float(np.mean(attn_ms)) * 1e3
+    attn_us_p10, attn_us_p50, attn_us_p90 = (float(np.percentile(attn_ms, q)) * 1e3 for q in (10, 50, 90))
+    log(f"[bench] step {us_per_step:.2f} us; attention call mean {attn_us:.2f} us (p10 {attn_us_p10:.2f}, "
+        f"p50 {attn_us_p50:.2f}, p90 {attn_us_p90:.2f})")
+
+    attn_gbs = work["attn_bytes"] / (attn_us * 1e-6) / 1e9
+    attn_tflops = work["flops"] / (attn_us * 1e-6) / 1e12
+    step_bytes = work["step_bytes"] * L
+    step_flops = work["flops"] * L
+    ideal_us = max(step_bytes / (HBM_PEAK_GBS * 1e9), step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6
+    bound = "hbm" if step_bytes / HBM_PEAK_GBS >= step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e3) else "mfma"
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        roof = {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+    roof["kernel"] = "mixed_step_attn (attention_kernel + combine_kernel)"
+    roof["per_launch_us"] = round(attn_us, 3)
+    roof["algorithmic_bytes"] = work["attn_bytes"]
+    roof["algorithmic_flops"] = work["flops"]
+
+    result = {
+        "metric": METRIC,
+        "value": round(us_per_step, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_per_step / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": L, "page_size": b.page_size, "requests": b.num_reqs,
+                   "rows": work["rows"], "decode_rows": wl.num_decode, "chunks": [list(x) for x in wl.chunks],
+                   "out_dtype": args.out_dtype, "rotating_sets": n_rot, "parallelism": "single GPU"},
+        "step": {"ideal_us": round(ideal_us, 3), "roofline_frac": round(ideal_us / us_per_step, 4),
+                 "bound": bound, "TB_per_s": round(step_bytes / (us_per_step * 1e-6) / 1e12, 3),
+                 "TFLOP_per_s": round(step_flops / (us_per_step * 1e-6) / 1e12, 2),
+                 "algorithmic_bytes": step_bytes, "algorithmic_flops": step_flops},
+        "roofline": roof,
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.config)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wl, cfg):
+    """The fp64 oracle as it stands, timed on this host on a bounded sample."""
+    import oracle
+    from paper_2607_02043_amd import workloads as W
+
+    threads = len(os.sched_getaffinity(0))
+    b = wl.batch
+    li = wl.layer(0)
+    work = algorithmic_work(b)
+    total_pairs = work["pairs"]
+    if total_pairs <= 400_000:
+        rows = None
+        sample = "one full layer step (append + every row)"
+        frac = 1.0
+    else:
+        # a seeded sample of rows whose pairs add up to about 400k (a few seconds of fp64 work)
+        rng = np.random.default_rng(0)
+        order = rng.permutation(b.num_rows)
+        cu = b.cu_q
+        req_of = np.searchsorted(cu, np.arange(b.num_rows), side="right") - 1
+        pairs_of = b.prefix_lens[req_of].astype(np.int64) + (np.arange(b.num_rows) - cu[req_of]) + 1
+        csum = np.cumsum(pairs_of[order])
+        n = int(np.searchsorted(csum, 400_000)) + 1
+        rows = np.sort(order[:n])
+        frac = float(pairs_of[rows].sum()) / total_pairs
+        sample = f"{len(rows)} seeded random rows ({frac * 100:.2f}% of one layer's query-key pairs), scaled up"
+    times = []
+    for _ in range(3):
+        t = time.perf_counter()
+        oracle.step(b, li, W.SOFTMAX_SCALE, rows=rows, threads=threads)
+        times.append(time.perf_counter() - t)
+    per_layer_s = float(np.median(times)) / frac
+    value_us = per_layer_s * wl.num_layers * 1e6
+    return {"value": round(value_us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
+            "sample": sample + f"; median of 3; x{wl.num_layers} layer(s)",
+            "cpu": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+if __name__ == "__main__":
+    main()

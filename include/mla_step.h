@@ -94,7 +94,9 @@ const char *mla_last_error(void);
 
 /* Device workspace (bytes) that mixed_step_attn needs for this batch, or 0 on
  * invalid arguments (then mla_last_error says why; a valid batch may also need
- * 0 bytes).  Depends only on the host arrays and the device's CU count. */
+ * 0 bytes).  Depends only on the host arrays and the device's CU count.  The
+ * workspace holds fp32 partial results of rows whose keys are split across
+ * workgroups. */
 size_t mixed_step_workspace_bytes(const mla_batch *batch);
 
 /* Scatter the step's new latents into the paged cache (the append above).
@@ -117,7 +119,8 @@ int append_latent_kv(const mla_batch *batch, const uint16_t *new_latents, uint16
  *   lse            DEVICE fp32 [T][16] natural-log sum of exp(s), or NULL.
  *   workspace      DEVICE scratch of at least mixed_step_workspace_bytes(batch)
  *                  bytes (may be NULL if that is 0); contents on entry are
- *                  ignored and on return undefined.
+ *                  ignored and on return undefined; calls that overlap in
+ *                  time need distinct workspaces.
  * Errors: MLA_ERR_INVALID_ARG, MLA_ERR_UNSUPPORTED, MLA_ERR_WORKSPACE,
  * MLA_ERR_HIP. */
 int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *kv_cache,

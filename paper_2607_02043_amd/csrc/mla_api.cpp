@@ -8,7 +8,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <mutex>
+#include <vector>
 
 #include "mla_kernels.h"
 
@@ -101,71 +103,123 @@ int check_batch(const mla_batch *b, Shape *sh) {
 }
 
 struct Plan {
-    int ks_chunk = 0, ks_dec = 0;
-    int n_chunk_items = 0, n_dec_items = 0;
+    int ks_chunk = 0, n_chunk_items = 0;
+    int n_dec_wg = 0, dec_tiles_per_wg = 0, dec_total_tiles = 0;
     bool chunk_split = false, dec_split = false;
     size_t off_chunk_o = 0, off_chunk_ml = 0, off_dec_o = 0, off_dec_ml = 0, bytes = 0;
 };
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-// Work items: chunk requests -> (block of 4 tokens) x (key range of ks_chunk);
-// decode requests -> key ranges of ks_dec.  Ranges are sized so that the step
-// offers a few items per compute unit; every item's pages fit the kernel's
-// 256-entry page window.  The device recomputes the same counts from the
-// device copies of the lengths.
+// Rough per-CU costs used only to balance the two kinds of work (us).
+constexpr double kChunkTileUs = 3.2;      // 4 tokens x 32 keys on one CU
+constexpr double kCuStreamGBs = 50.0;     // one CU streaming alone
+constexpr double kChipStreamGBs = 6300.0; // all CUs streaming together
+
+struct DecReq {
+    long long first_tile, tiles, p;
+};
+
+// Does a decode share of S tiles per workgroup respect the kernel's limits
+// (segments and page-window entries per workgroup)?
+bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long S, int page_size) {
+    size_t k = 0;
+    for (long long R0 = 0; R0 < total; R0 += S) {
+        const long long R1 = std::min(R0 + S, total);
+        while (k < reqs.size() && reqs[k].first_tile + reqs[k].tiles <= R0) ++k;
+        long long segs = 0, pages = 0;
+        for (size_t j = k; j < reqs.size() && reqs[j].first_tile < R1; ++j) {
+            const long long t0 = std::max(R0 - reqs[j].first_tile, 0LL);
+            const long long t1 = std::min(R1 - reqs[j].first_tile, reqs[j].tiles);
+            const long long k0 = t0 * mla::kKeysPerTile;
+            const long long klast = std::min(t1 * mla::kKeysPerTile, reqs[j].p + 1) - 1;
+            pages += klast / page_size - k0 / page_size + 1;
+            ++segs;
+        }
+        if (segs > mla::kMaxDecSegments || pages > mla::kPageWindow) return false;
+    }
+    return true;
+}
+
+// Work layout of one call.
+//  * chunk requests -> items of (4 tokens) x (ks_chunk keys), longest rows
+//    first; key ranges are split only when the chunk is too small to give the
+//    chip enough items.
+//  * decode requests -> one list of 32-key tiles cut into equal shares for
+//    n_dec_wg persistent workgroups; n_dec_wg balances the decode stream
+//    against the chunk work that runs on the remaining compute units.
+// The device recomputes the same mapping from the device copies of the lengths.
 int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
     if (sh.R == 0) return MLA_OK;
     int st = MLA_OK;
     const int ncu = cu_count(&st);
     if (st != MLA_OK) return st;
     const long long P = b->page_size;
-    // keys one item may span: (window - 1) whole pages, in 64-key units
-    long long cap = ((long long)(mla::kPageWindow - 1) * P) / 64 * 64;
+    long long cap = ((long long)(mla::kPageWindow - 1) * P) / 64 * 64;  // keys per chunk item
     if (cap < 64) cap = 64;
-    const int BM = mla::kChunkBlockTokens;
+    const int BM = mla::kChunkBlockTokens, KT = mla::kKeysPerTile;
 
-    long long dec_keys = 0, n_dec = 0, chunk_blocks = 0, chunk_block_keys = 0, max_klim = 0;
+    std::vector<DecReq> dec;
+    long long chunk_blocks = 0, chunk_block_keys = 0, dec_total = 0;
     for (int r = 0; r < sh.R; ++r) {
         const long long c = b->q_lens[r], p = b->prefix_lens[r];
         if (c == 1) {
-            dec_keys += p + 1;
-            ++n_dec;
+            const long long nt = ceil_div_ll(p + 1, KT);
+            dec.push_back(DecReq{dec_total, nt, p});
+            dec_total += nt;
         } else {
             const long long nrb = ceil_div_ll(c, BM);
             chunk_blocks += nrb;
             for (long long rb = 0; rb < nrb; ++rb) chunk_block_keys += p + std::min(c, (rb + 1) * BM);
-            max_klim = std::max(max_klim, p + c);
         }
     }
+    if (dec_total > (1LL << 30)) return fail(MLA_ERR_INVALID_ARG, "too many decode keys in the step");
+    // chunk items
     const long long target = 2LL * ncu;
-    long long ks_dec = 256;
-    if (n_dec > 0) {
-        ks_dec = std::max<long long>(256, ceil_div_ll(ceil_div_ll(dec_keys, target), 64) * 64);
-        ks_dec = std::min(ks_dec, cap);
-    }
     long long ks_chunk = cap;
     if (chunk_blocks > 0 && chunk_blocks < target) {
         ks_chunk = std::max<long long>(128, ceil_div_ll(ceil_div_ll(chunk_block_keys, target), 64) * 64);
         ks_chunk = std::min(ks_chunk, cap);
     }
-    pl->ks_dec = (int)ks_dec;
-    pl->ks_chunk = (int)ks_chunk;
-    long long nci = 0, ndi = 0;
+    long long nci = 0;
     for (int r = 0; r < sh.R; ++r) {
         const long long c = b->q_lens[r], p = b->prefix_lens[r];
-        if (c == 1) {
-            const long long n = ceil_div_ll(p + 1, ks_dec);
-            ndi += n;
-            if (n > 1) pl->dec_split = true;
-        } else {
-            nci += ceil_div_ll(c, BM) * ceil_div_ll(p + c, ks_chunk);
-            if (p + c > ks_chunk) pl->chunk_split = true;
-        }
+        if (c == 1) continue;
+        nci += ceil_div_ll(c, BM) * ceil_div_ll(p + c, ks_chunk);
+        if (p + c > ks_chunk) pl->chunk_split = true;
     }
-    if (nci + ndi > (1LL << 30)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
+    if (nci > (1LL << 30)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
+    pl->ks_chunk = (int)ks_chunk;
     pl->n_chunk_items = (int)nci;
-    pl->n_dec_items = (int)ndi;
+    // decode shares
+    if (dec_total > 0) {
+        const double chunk_us = (double)ceil_div_ll(chunk_block_keys, KT) * kChunkTileUs;
+        long long best_g = std::min<long long>(ncu, dec_total);
+        if (chunk_us > 0.0 && ncu > 1) {
+            double best = 1e300;
+            for (long long g = 1; g < ncu && g <= dec_total; ++g) {
+                const double bw = std::min(kCuStreamGBs, kChipStreamGBs / g);  // GB/s per CU
+                const double t_dec = (double)ceil_div_ll(dec_total, g) * (KT * mla::kRowBytes) / (bw * 1e3);
+                const double t_chunk = chunk_us / (double)(ncu - g);
+                const double t = std::max(t_dec, t_chunk);
+                if (t < best) {
+                    best = t;
+                    best_g = g;
+                }
+            }
+        }
+        long long S = ceil_div_ll(dec_total, best_g);
+        while (S > 1 && !dec_share_fits(dec, dec_total, S, (int)P)) S = std::max(1LL, S * 3 / 4);
+        if (!dec_share_fits(dec, dec_total, S, (int)P))
+            return fail(MLA_ERR_UNSUPPORTED, "decode work does not fit the per-workgroup segment / page limits");
+        const long long G = ceil_div_ll(dec_total, S);
+        if (G > (1LL << 24)) return fail(MLA_ERR_INVALID_ARG, "too many decode workgroups");
+        pl->n_dec_wg = (int)G;
+        pl->dec_tiles_per_wg = (int)S;
+        pl->dec_total_tiles = (int)dec_total;
+        for (const DecReq &d : dec)
+            if (d.first_tile / S != (d.first_tile + d.tiles - 1) / S) pl->dec_split = true;
+    }
     size_t off = 0;
     if (pl->chunk_split) {
         pl->off_chunk_o = off;
@@ -175,12 +229,11 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
     }
     if (pl->dec_split) {
         pl->off_dec_o = off;
-        off = align256(off + (size_t)ndi * mla::kPartialFloats * sizeof(float));
+        off = align256(off + (size_t)2 * pl->n_dec_wg * mla::kPartialFloats * sizeof(float));
         pl->off_dec_ml = off;
-        off = align256(off + (size_t)ndi * mla::kPartialStats * sizeof(float));
+        off = align256(off + (size_t)2 * pl->n_dec_wg * mla::kPartialStats * sizeof(float));
     }
     pl->bytes = off;
-    (void)max_klim;
     return MLA_OK;
 }
 
@@ -266,16 +319,17 @@ int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *k
     a.num_pages = batch->num_pages;
     a.scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
     a.ks_chunk = pl.ks_chunk;
-    a.ks_dec = pl.ks_dec;
     a.n_chunk_items = pl.n_chunk_items;
-    a.n_dec_items = pl.n_dec_items;
+    a.n_dec_wg = pl.n_dec_wg;
+    a.dec_tiles_per_wg = pl.dec_tiles_per_wg;
+    a.dec_total_tiles = pl.dec_total_tiles;
     a.out_bf16 = out_dtype == MLA_OUT_BF16 ? 1 : 0;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = mla::launch_attention(a, s);
     if (e != hipSuccess) return hip_fail(e, "attention kernel launch");
     if (pl.chunk_split || pl.dec_split) {
         e = mla::launch_combine(a, s);
-        if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
+        if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
     }
     return MLA_OK;
 }

@@ -16,6 +16,7 @@ constexpr int kChunkTokensPerWave = 1;
 constexpr int kChunkBlockTokens = 4 * kChunkTokensPerWave;  // tokens per chunk work item
 constexpr int kPartialFloats = kHeads * kDv;                // one row's partial output
 constexpr int kPartialStats = kHeads * 2;                   // one row's (max, sum) per head
+constexpr int kMaxDecSegments = 64;                         // requests one decode workgroup may touch
 
 struct AttnArgs {
     const uint16_t *q;
@@ -27,8 +28,8 @@ struct AttnArgs {
     float *lse;
     float *ws_chunk_o;    // [n_chunk_items][block tokens][16][512]
     float *ws_chunk_ml;   // [n_chunk_items][block tokens][16][2]
-    float *ws_dec_o;      // [n_dec_items][16][512]
-    float *ws_dec_ml;     // [n_dec_items][16][2]
+    float *ws_dec_o;      // [2 n_dec_wg][16][512]: first / last segment of each decode workgroup
+    float *ws_dec_ml;     // [2 n_dec_wg][16][2]
     int32_t num_reqs;
     int32_t num_rows;
     int32_t page_size;
@@ -36,10 +37,11 @@ struct AttnArgs {
     int32_t max_pages;
     int32_t num_pages;
     float scale_log2;     // softmax scale * log2(e)
-    int32_t ks_chunk;     // keys per chunk work item (a multiple of 64)
-    int32_t ks_dec;       // keys per decode work item (a multiple of 64)
+    int32_t ks_chunk;          // keys per chunk work item (a multiple of 64)
     int32_t n_chunk_items;
-    int32_t n_dec_items;
+    int32_t n_dec_wg;          // persistent decode workgroups
+    int32_t dec_tiles_per_wg;  // 32-key decode tiles per workgroup share
+    int32_t dec_total_tiles;
     int32_t out_bf16;
 };
 

@@ -1,27 +1,26 @@
-// gfx950 kernels of libmlastep: latent append, mixed-step latent attention
-// (decode rows and chunked-prefill rows of one step), split merge.
+// gfx950 kernels of libmlastep: latent append and mixed-step latent attention
+// (decode rows and chunked-prefill rows of one step in one launch).
 //
 // The step is the one a decode node runs when it serves deflected prefill
 // chunks next to its in-flight decodes (section 2.3; section 4.3.1, Eq. 4 of
 // the paper); the head shapes are those of the served model's absorbed latent
 // attention (DeepSeek-V2-Lite, section 6).
 //
-// Work decomposition.  Every request is cut into work items:
-//   * decode request (c = 1): key ranges of ks_dec keys (split-KV).  A
-//     workgroup streams its range through a 4-deep ring of 32-key tiles that
-//     the wavefronts fill asynchronously (global -> LDS DMA); all four waves
-//     score the tile (16 heads = the MFMA's 16 columns) and each wave
-//     accumulates one 128-wide slice of the 512 value dims.
-//   * chunk request (c > 1): blocks of 4 query tokens (one per wave, 16 head
-//     rows each) times key ranges of ks_chunk keys.  Tiles go through a
-//     3-deep DMA ring; each tile's value part is converted once to fp16 and
-//     transposed in LDS so that P*V runs on fp16 MFMA.
-// Items of one request that split the key range write fp32 partials
-// (unnormalised sum, running max and sum in log2 units); the merge kernel
-// combines them in a fixed order, so results are run-to-run deterministic and
-// do not depend on the physical page order.
+// Work decomposition (one launch for all rows of a step):
+//   * decode rows (c = 1): persistent workgroups own equal shares of the list
+//     of all decode tiles (32 keys each); see the decode section below.
+//   * chunk rows (c > 1): one workgroup (4 wavefronts) per block of 4 query
+//     tokens (one per wave, 16 head rows each) times a key range of ks_chunk
+//     keys.  32-key tiles go through a 3-deep global -> LDS DMA ring; each
+//     tile's value part is converted once to fp16 and transposed in LDS so
+//     that P*V runs on fp16 MFMA.
+// Rows whose keys are split across workgroups leave fp32 partials (the
+// unnormalised sum, the running max and sum in log2 units); a second, small
+// merge kernel combines them in a fixed order.  Results are therefore
+// run-to-run deterministic and do not depend on the physical page order.
 #include "mla_kernels.h"
 
+#include <limits.h>
 #include <math.h>
 
 namespace mla {
@@ -33,24 +32,63 @@ typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kTileBytes = kKeysPerTile * kRowBytes;          // 36864
-constexpr int kChunksPerRow = kRowBytes / 16;                 // 72 16-byte chunks
-constexpr int kDmaPerTile = kTileBytes / (kThreads * 16);     // 9 per thread
+constexpr int kChunksPerRow = kRowBytes / 16;  // 72 16-byte chunks per latent
+// decode path
+constexpr int kDecKeys = kKeysPerTile;  // 32
+constexpr int kDecTileBytes = kDecKeys * kRowBytes;  // 36864
 constexpr int kDecRing = 4;
+constexpr int kDecLds = kDecRing * kDecTileBytes + 4 * kHeads * 20 * 4;  // ring + partial score blocks
+// chunk path
+constexpr int kChunkKeys = kKeysPerTile;  // 32
+constexpr int kChunkTileBytes = kChunkKeys * kRowBytes;  // 36864
 constexpr int kChunkRing = 3;
-constexpr int kVtStride = 80;                                 // bytes per dv row of V^T (32 fp16 + pad)
-constexpr int kVtBytes = kDv * kVtStride;                     // 40960
-constexpr int kDecLds = kDecRing * kTileBytes;                // 147456
-constexpr int kChunkLds = kChunkRing * kTileBytes + kVtBytes; // 151552
+constexpr int kVtStride = 80;  // bytes per dv row of V^T (32 fp16 + pad)
+constexpr int kVtBytes = kDv * kVtStride;
+constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kVtBytes;
 constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
 constexpr float kNegInf = -INFINITY;
+
+// Optional per-workgroup timeline for profiling builds (-DMLA_TRACE): slot k
+// of workgroup b records the 100 MHz real-time counter at point k.
+#ifdef MLA_TRACE
+__device__ unsigned long long g_trace[1 << 20];
+#define TRACE(k)                                                                        \
+    do {                                                                                \
+        if (threadIdx.x == 0 && blockIdx.x < (1 << 16))                                 \
+            g_trace[(size_t)blockIdx.x * 16 + (k)] = __builtin_amdgcn_s_memrealtime();  \
+    } while (0)
+#define TRACE_VAL(k, v)                                                                 \
+    do {                                                                                \
+        if (threadIdx.x == 0 && blockIdx.x < (1 << 16)) g_trace[(size_t)blockIdx.x * 16 + (k)] = (v); \
+    } while (0)
+// shader-clock stamps inside the third tile of an item (slots 10..15)
+#define TRACE_TILE(t, k)                                                                 \
+    do {                                                                                 \
+        if ((t) == 2 && threadIdx.x == 0 && blockIdx.x < (1 << 16))                      \
+            g_trace[(size_t)blockIdx.x * 16 + (k)] = __builtin_amdgcn_s_memtime();       \
+    } while (0)
+#else
+#define TRACE_TILE(t, k) \
+    do {                 \
+    } while (0)
+#define TRACE(k) \
+    do {         \
+    } while (0)
+#define TRACE_VAL(k, v) \
+    do {                \
+    } while (0)
+#endif
 constexpr float kLn2 = 0.69314718055994530942f;
 
-static_assert(kTileBytes % (kThreads * 16) == 0, "tile must split into whole DMA rounds");
-
 // ---------------------------------------------------------------- helpers
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t b) { return __uint_as_float(b << 16); }
+
+__device__ __forceinline__ uint32_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {
     return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
@@ -59,7 +97,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
 // One 16-byte global -> LDS DMA per lane: lane i writes LDS bytes
 // [base + 16 i, base + 16 i + 16).  `base` must be wave-uniform.  Issued with
 // inline assembly so that the compiler does not drain the whole ring before
-// every barrier; completion is tracked by hand with wait_vm below.
+// every barrier; completion is tracked by hand (vmcnt).
 __device__ __forceinline__ void lds_dma16(const void *gsrc, uint32_t lds_base) {
     asm volatile(
         "s_nop 0\n\t"
@@ -69,16 +107,13 @@ __device__ __forceinline__ void lds_dma16(const void *gsrc, uint32_t lds_base) {
         : "memory");
 }
 
-// Wait until at most `newer_tiles` tiles of DMA issued after the awaited one
-// are still in flight (9 DMA instructions per tile and wave).
-__device__ __forceinline__ void wait_dma_tiles(int newer_tiles) {
-    if (newer_tiles <= 0)
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    else if (newer_tiles == 1)
-        asm volatile("s_waitcnt vmcnt(9)" ::: "memory");
-    else
-        asm volatile("s_waitcnt vmcnt(18)" ::: "memory");
-}
+__device__ __forceinline__ void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void wait_dma_keep9() { asm volatile("s_waitcnt vmcnt(9)" ::: "memory"); }
+
+// vmcnt(0) with expcnt / lgkmcnt left alone (gfx9 s_waitcnt encoding),
+// issued through the builtin so the compiler's scoreboard accounts for it
+// and inserts no vmcnt wait of its own inside the pipelined loops.
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
@@ -105,6 +140,13 @@ __device__ __forceinline__ float wave_sum16(float v) {
 // read the same chunk of 8 consecutive keys hit 8 different bank groups.
 __device__ __forceinline__ int tile_off(int k, int c) { return (k * kChunksPerRow + (c ^ (k & 7))) * 16; }
 
+// Transposing LDS read (gfx950): inside each 16-lane group, lane i receives
+// element (i & 3) of the 8 bytes read by lane 4 j + (i >> 2), j = 0..3.
+__device__ __forceinline__ u32x2 lds_read_tr16(const char *p) {
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p));
+    return __builtin_bit_cast(u32x2, v);
+}
+
 // ------------------------------------------------------ work-item lookup
 // Items of one kind are numbered request by request; request r owns
 // count(r) consecutive items.  The workgroup scans the per-request counts
@@ -114,18 +156,24 @@ struct ReqLens {
     const int32_t *prefix;
 };
 
+struct Located {
+    int r, local, p, row0, c;
+};
+
 template <typename CountFn>
 __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn count, int *s_tmp,
-                            int &req, int &local) {
+                            Located &loc) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     if (tid == 0) s_tmp[4] = -1;
     int running = 0;
     for (int base = 0; base < num_reqs; base += kThreads) {
         const int r = base + tid;
-        int cnt = 0;
+        int cnt = 0, p = 0, row0 = 0, c = 0;
         if (r < num_reqs) {
-            const int c = rl.cu_q[r + 1] - rl.cu_q[r];
-            cnt = count(rl.prefix[r], c);
+            row0 = rl.cu_q[r];
+            c = rl.cu_q[r + 1] - row0;
+            p = rl.prefix[r];
+            cnt = count(p, c);
         }
         int inc = cnt;
 #pragma unroll
@@ -147,11 +195,13 @@ __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn
         if (cnt > 0 && target >= running + exc && target < running + inc) {
             s_tmp[4] = r;
             s_tmp[5] = target - running - exc;
+            s_tmp[6] = p;
+            s_tmp[7] = row0;
+            s_tmp[8] = c;
         }
         __syncthreads();
         if (s_tmp[4] >= 0) {
-            req = s_tmp[4];
-            local = s_tmp[5];
+            loc = Located{s_tmp[4], s_tmp[5], s_tmp[6], s_tmp[7], s_tmp[8]};
             return true;
         }
         running += total;
@@ -159,38 +209,32 @@ __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn
     return false;
 }
 
-__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
-
 struct ChunkCount {
     int ks;
     __device__ int operator()(int p, int c) const {
         return c > 1 ? ceil_div(c, kChunkBlockTokens) * ceil_div(p + c, ks) : 0;
     }
 };
-struct DecCount {
-    int ks;
-    __device__ int operator()(int p, int c) const { return c == 1 ? ceil_div(p + 1, ks) : 0; }
-};
 
 struct ChunkItem {
-    int r, p, c, row0, i0, i1, k0, k1, nks_eff;
+    int r, p, c, row0, i0, i1, k0, k1, ks, nks_eff;
 };
 
-__device__ __forceinline__ ChunkItem decode_chunk_item(const AttnArgs &a, int r, int local) {
+__device__ __forceinline__ ChunkItem decode_chunk_item(const AttnArgs &a, const Located &lc) {
     ChunkItem it;
-    it.r = r;
-    it.p = a.prefix[r];
-    it.row0 = a.cu_q[r];
-    it.c = a.cu_q[r + 1] - it.row0;
+    it.r = lc.r;
+    it.p = lc.p;
+    it.row0 = lc.row0;
+    it.c = lc.c;
     const int nrb = ceil_div(it.c, kChunkBlockTokens);
     const int nks = ceil_div(it.p + it.c, a.ks_chunk);
-    const int rb = nrb - 1 - local / nks;  // longest rows first
-    const int ks = local % nks;
+    const int rb = nrb - 1 - lc.local / nks;  // longest rows first
+    it.ks = lc.local % nks;
     it.i0 = rb * kChunkBlockTokens;
     it.i1 = min(it.i0 + kChunkBlockTokens, it.c);
     const int klim = it.p + it.i1;
     it.nks_eff = ceil_div(klim, a.ks_chunk);
-    it.k0 = ks * a.ks_chunk;
+    it.k0 = it.ks * a.ks_chunk;
     it.k1 = min(klim, it.k0 + a.ks_chunk);
     return it;
 }
@@ -207,13 +251,17 @@ __device__ __forceinline__ void load_page_window(const AttnArgs &a, int r, int l
     }
 }
 
-// Issue the DMA of one 32-key tile (keys kbase .. kbase+31, clamped to the
-// last valid key k1-1 so every byte read is a finite cached latent).
+// Issue the DMA of one tile of KEYS keys (kbase .. kbase + KEYS - 1, clamped
+// to the last valid key k1 - 1 so every byte read is a finite cached latent).
+// Instruction i of wave wv fills 1 KB segment i * 4 + wv of the tile.
+template <int KEYS>
 __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages, int lp0, int kbase, int k1,
                                            uint32_t lds_tile, int wv, int lane) {
+    constexpr int kDma = KEYS * kRowBytes / (kThreads * 16);
     const char *kv = reinterpret_cast<const char *>(a.kv);
+    const char *src[kDma];
 #pragma unroll
-    for (int i = 0; i < kDmaPerTile; ++i) {
+    for (int i = 0; i < kDma; ++i) {  // all page-id reads first, then the DMA burst
         const int seg = i * 4 + wv;
         const int u = seg * 64 + lane;
         const int kk = u / kChunksPerRow;
@@ -222,159 +270,474 @@ __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages
         key = key < k1 ? key : k1 - 1;
         const int page = s_pages[min((key >> a.log2_page) - lp0, kPageWindow - 1)];
         const size_t slot = (size_t)page * a.page_size + (key & (a.page_size - 1));
-        lds_dma16(kv + slot * kRowBytes + c * 16, __builtin_amdgcn_readfirstlane(lds_tile + seg * 1024));
+        src[i] = kv + slot * kRowBytes + c * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < kDma; ++i)
+        lds_dma16(src[i], __builtin_amdgcn_readfirstlane(lds_tile + (i * 4 + wv) * 1024));
+}
+
+// Scores of 16 keys (tile rows key_base .. key_base + 15) against one token's
+// query operand: lane l gets S[key_base + 4 (l/16) + i][head l%16], i = 0..3.
+// Reads are staged 6 steps at a time; two accumulation chains.
+__device__ __forceinline__ f32x4 score16(const char *tile, int key_base, const u32x4 *qreg, int lane) {
+    const int g = lane >> 4, key = key_base + (lane & 15);
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    constexpr int G = 6;
+#pragma unroll
+    for (int grp = 0; grp < 18 / G; ++grp) {
+        u32x4 av[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j)
+            av[j] = *reinterpret_cast<const u32x4 *>(tile + tile_off(key, (grp * G + j) * 4 + g));
+#pragma unroll
+        for (int j = 0; j < G; j += 2) {
+            acc0 = mfma_bf16(av[j], qreg[grp * G + j], acc0);
+            acc1 = mfma_bf16(av[j + 1], qreg[grp * G + j + 1], acc1);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, G, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, G, 0);
+    }
+    return acc0 + acc1;
+}
+
+// 32 keys (two 16-key halves), same layout per half.
+__device__ __forceinline__ void score32(const char *tile, const u32x4 *qreg, int lane, f32x4 s[2]) {
+    const int g = lane >> 4;
+    const int key0 = lane & 15, key1 = 16 + (lane & 15);
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    constexpr int G = 6;
+#pragma unroll
+    for (int grp = 0; grp < 18 / G; ++grp) {
+        u32x4 a0[G], a1[G];
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            const int st = grp * G + j;
+            a0[j] = *reinterpret_cast<const u32x4 *>(tile + tile_off(key0, st * 4 + g));
+            a1[j] = *reinterpret_cast<const u32x4 *>(tile + tile_off(key1, st * 4 + g));
+        }
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            acc0 = mfma_bf16(a0[j], qreg[grp * G + j], acc0);
+            acc1 = mfma_bf16(a1[j], qreg[grp * G + j], acc1);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * G, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * G, 0);
+    }
+    s[0] = acc0;
+    s[1] = acc1;
+}
+
+__device__ __forceinline__ void load_query(const AttnArgs &a, int row, int lane, u32x4 *qreg) {
+    const uint16_t *qp = a.q + ((size_t)row * kHeads + (lane & 15)) * kDqk + (lane >> 4) * 8;
+#pragma unroll
+    for (int st = 0; st < 18; ++st) qreg[st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
+}
+
+// Store 4 consecutive dims of one (row, head) output, fp32 or bf16.
+__device__ __forceinline__ void store_out4(const AttnArgs &a, int row, int head, int dv, f32x4 v) {
+    const size_t off = ((size_t)row * kHeads + head) * kDv + dv;
+    if (a.out_bf16) {
+        const uint32_t w0 = bf16_bits(v[0]) | (bf16_bits(v[1]) << 16);
+        const uint32_t w1 = bf16_bits(v[2]) | (bf16_bits(v[3]) << 16);
+        *reinterpret_cast<u32x2 *>(reinterpret_cast<uint16_t *>(a.out) + off) = u32x2{w0, w1};
+    } else {
+        *reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(a.out) + off) = v;
     }
 }
 
-// S^T (32 keys x 16 heads) of one tile against the query operand of one
-// token: lane l gets s[kt][i] = score of key 16 kt + 4 (l/16) + i, head l%16.
-__device__ __forceinline__ void score_tile(const char *tile, const u32x4 *qreg, int lane, f32x4 s[2]) {
-    const int g = lane >> 4;
+// ------------------------------------------------------------------ merge
+// Merge the key-split partials of nrows (<= 4) consecutive output rows (m_s,
+// l_s in log2 units, o_s unnormalised) in split order.  Partial row ii of
+// split s starts at po + s * stride_o + ii * kPartialFloats (stats likewise).
+// 256 threads: head = tid / 16, dims (tid % 16) * 32 .. +32, all rows at once.
+__device__ void merge_block(const AttnArgs &a, const float *po, const float *pml, size_t stride_o, size_t stride_ml,
+                            int nsplit, int row0, int nrows) {
+    const int tid = threadIdx.x;
+    const int hh = tid >> 4, d0 = (tid & 15) * 32;
+    float mmax[4], denom[4];
+    f32x4 o[4][8];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-        const int key = kt * 16 + (lane & 15);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int ii = 0; ii < 4; ++ii) {
+        mmax[ii] = kNegInf;
+        denom[ii] = 0.f;
 #pragma unroll
-        for (int st = 0; st < 18; ++st) {
-            const u32x4 av = *reinterpret_cast<const u32x4 *>(tile + tile_off(key, st * 4 + g));
-            acc = mfma_bf16(av, qreg[st], acc);
+        for (int k = 0; k < 8; ++k) o[ii][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int sp = 0; sp < nsplit; ++sp)
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii)
+            if (ii < nrows) mmax[ii] = fmaxf(mmax[ii], pml[sp * stride_ml + ii * kPartialStats + hh * 2]);
+    for (int sp = 0; sp < nsplit; ++sp) {
+#pragma unroll
+        for (int ii = 0; ii < 4; ++ii) {
+            if (ii >= nrows) continue;
+            const float *ml = pml + sp * stride_ml + ii * kPartialStats + hh * 2;
+            const float ms = ml[0];
+            const float wt = (ms == kNegInf) ? 0.f : exp2f(ms - mmax[ii]);
+            denom[ii] += wt * ml[1];
+            const f32x4 *src = reinterpret_cast<const f32x4 *>(po + sp * stride_o + ii * kPartialFloats + hh * kDv + d0);
+            f32x4 vv[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) vv[k] = src[k];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) o[ii][k] += wt * vv[k];
         }
-        s[kt] = acc;
+    }
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+        if (ii >= nrows) continue;
+        const float inv = 1.f / denom[ii];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) store_out4(a, row0 + ii, hh, d0 + 4 * k, o[ii][k] * inv);
+        if (a.lse && (tid & 15) == 0)
+            a.lse[(size_t)(row0 + ii) * kHeads + hh] = (mmax[ii] + log2f(denom[ii])) * kLn2;
     }
 }
 
 // ------------------------------------------------------------ decode path
-__device__ void decode_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages) {
-    int r, ks;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, DecCount{a.ks_dec}, s_tmp, r, ks)) return;
+// Decode rows run on persistent workgroups.  The 32-key tiles of all decode
+// requests, request after request, form one list; workgroup w owns tiles
+// [w S, (w + 1) S).  Its share splits into segments, one per request it
+// touches.  A segment streams its query block and then its tiles through a
+// 4-slot global -> LDS DMA ring, so prefetch runs on across request
+// boundaries and the start-up latency is paid once per workgroup.  Per tile,
+// wave w scores 16 keys over half of the 576 latent dims (the four partial
+// 16 x 16 score blocks meet in LDS), then accumulates its 128-wide slice of
+// the value dims over all 32 keys.  A request spread over several workgroups
+// leaves fp32 partials (slot 2 w for a workgroup's first segment, 2 w + 1 for
+// its last) that the merge kernel combines.
+constexpr int kMaxSeg = kMaxDecSegments;
+constexpr int kXStride = 20;  // floats per head row of a partial score block (16 + pad)
+
+struct DecSeg {
+    int r, p, row, t0, t1, pw, lp0;  // tiles t0 .. t1-1 of request r; page window offset / first page
+};
+
+__device__ __forceinline__ int dec_tiles(int p, int c) { return c == 1 ? ceil_div(p + 1, kDecKeys) : 0; }
+
+// Exclusive prefix sum over the 256 threads of the workgroup (uses s_w[0..3]).
+__device__ __forceinline__ int block_scan_excl(int v, int *s_w, int &total) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    int inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int t = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += t;
+    }
+    if (lane == 63) s_w[wv] = inc;
+    __syncthreads();
+    int off = 0;
+    total = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int t = s_w[k];
+        off += (k < wv) ? t : 0;
+        total += t;
+    }
+    __syncthreads();
+    return inc - v + off;
+}
+
+// Segments (request order) of the decode tile range [R0, R1); returns their count.
+__device__ int find_segments(const AttnArgs &a, int R0, int R1, DecSeg *s_seg, int *s_tmp) {
+    const int tid = threadIdx.x;
+    int running = 0, nseg = 0;
+    for (int base = 0; base < a.num_reqs && running < R1; base += kThreads) {
+        const int r = base + tid;
+        int nt = 0, p = 0, row0 = 0;
+        if (r < a.num_reqs) {
+            row0 = a.cu_q[r];
+            p = a.prefix[r];
+            // rows outside [0, T) only arise from device lengths that disagree with the host's
+            nt = (p >= 0 && row0 >= 0 && row0 < a.num_rows) ? dec_tiles(p, a.cu_q[r + 1] - row0) : 0;
+        }
+        int tot_t, tot_s;
+        const int T = running + block_scan_excl(nt, s_tmp, tot_t);
+        const bool ov = nt > 0 && T < R1 && T + nt > R0;
+        const int j = nseg + block_scan_excl(ov ? 1 : 0, s_tmp, tot_s);
+        if (ov && j < kMaxSeg) s_seg[j] = DecSeg{r, p, row0, max(R0 - T, 0), min(R1 - T, nt), 0, 0};
+        nseg += tot_s;
+        running += tot_t;
+    }
+    __syncthreads();
+    return min(nseg, kMaxSeg);
+}
+
+// Unit cursor of a workgroup's stream: segment j, tile t (t < 0: the query block).
+struct Cursor {
+    int j, t;
+};
+__device__ __forceinline__ void advance(Cursor &c, const DecSeg *s_seg) {
+    if (c.t < 0)
+        c.t = s_seg[c.j].t0;
+    else
+        ++c.t;
+    if (c.t >= s_seg[c.j].t1) {
+        ++c.j;
+        c.t = -1;
+    }
+}
+
+// DMA of one stream unit into a 36 KB ring slot.  A query block (16 heads x
+// 576 dims, 18 KB) is copied twice over so every unit takes 9 DMA rounds.
+__device__ __forceinline__ void issue_unit(const AttnArgs &a, const DecSeg &sg, int t, const int *s_pages,
+                                           uint32_t slot, int wv, int lane) {
+    constexpr int kDma = kDecTileBytes / (kThreads * 16);  // 9
+    const char *src[kDma];
+    if (t < 0) {
+        const char *qb = reinterpret_cast<const char *>(a.q + (size_t)sg.row * kHeads * kDqk);
+#pragma unroll
+        for (int i = 0; i < kDma; ++i) {
+            const int u = (i * 4 + wv) * 64 + lane;
+            src[i] = qb + (u % (kHeads * kChunksPerRow)) * 16;
+        }
+    } else {
+        const char *kv = reinterpret_cast<const char *>(a.kv);
+        const int kbase = t * kDecKeys, klast = sg.p;
+#pragma unroll
+        for (int i = 0; i < kDma; ++i) {
+            const int u = (i * 4 + wv) * 64 + lane;
+            const int kk = u / kChunksPerRow;
+            const int c = (u - kk * kChunksPerRow) ^ (kk & 7);
+            const int key = min(kbase + kk, klast);
+            const int page = s_pages[min(sg.pw + (key >> a.log2_page) - sg.lp0, kPageWindow - 1)];
+            src[i] = kv + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kRowBytes + c * 16;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) lds_dma16(src[i], __builtin_amdgcn_readfirstlane(slot + (i * 4 + wv) * 1024));
+}
+
+__device__ __forceinline__ void wait_units_newer(int n) {  // n of the later units may stay in flight
+    if (n <= 0)
+        wait_dma_all();
+    else if (n == 1)
+        wait_dma_keep9();
+    else
+        asm volatile("s_waitcnt vmcnt(18)" ::: "memory");
+}
+
+__device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int *s_pages, DecSeg *s_seg) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
-    const int p = a.prefix[r];
-    const int row = a.cu_q[r];
-    if (p < 0 || row < 0 || row >= a.num_rows) return;  // device lengths disagree with the host's
-    const int n_keys = p + 1;
-    const int nks = ceil_div(n_keys, a.ks_dec);
-    const int k0 = ks * a.ks_dec;
-    const int k1 = min(n_keys, k0 + a.ks_dec);
-    const int ntiles = ceil_div(k1 - k0, kKeysPerTile);
-    if (nks > 1 && a.ws_dec_o == nullptr) return;
-    const int lp0 = k0 >> a.log2_page;
-    load_page_window(a, r, lp0, ((k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
-    __syncthreads();
-
-    const uint32_t ring = lds_addr(smem);
-    for (int t = 0; t < kDecRing - 1 && t < ntiles; ++t)
-        issue_tile(a, s_pages, lp0, k0 + t * kKeysPerTile, k1, ring + t * kTileBytes, wv, lane);
-
-    u32x4 qreg[18];
-    {
-        const uint16_t *qp = a.q + ((size_t)row * kHeads + h) * kDqk + g * 8;
-#pragma unroll
-        for (int st = 0; st < 18; ++st) qreg[st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
+    const int R0 = w * a.dec_tiles_per_wg;
+    const int R1 = min(R0 + a.dec_tiles_per_wg, a.dec_total_tiles);
+    if (R0 >= R1) return;
+    const int nseg = find_segments(a, R0, R1, s_seg, s_tmp);
+    TRACE(1);
+    if (nseg == 0) return;
+    if (tid == 0) {  // page-window offsets of the segments
+        int pw = 0;
+        for (int j = 0; j < nseg; ++j) {
+            const DecSeg sg = s_seg[j];
+            const int lp0 = (sg.t0 * kDecKeys) >> a.log2_page;
+            const int klast = min(sg.t1 * kDecKeys, sg.p + 1) - 1;
+            s_seg[j].pw = pw;
+            s_seg[j].lp0 = lp0;
+            pw += (klast >> a.log2_page) - lp0 + 1;
+        }
     }
-    // Drain the query loads with the ring prologue: the compiler would otherwise
-    // wait for its own loads with vmcnt(0) inside the pipelined loop.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    for (int j = 0; j < nseg; ++j) {
+        const DecSeg sg = s_seg[j];
+        const int klast = min(sg.t1 * kDecKeys, sg.p + 1) - 1;
+        const int n = (klast >> a.log2_page) - sg.lp0 + 1;
+        const int32_t *btr = a.bt + (size_t)sg.r * a.max_pages;
+        for (int i = tid; i < n && sg.pw + i < kPageWindow; i += kThreads) {
+            const int lp = sg.lp0 + i;
+            const int pg = lp < a.max_pages ? btr[lp] : 0;
+            s_pages[sg.pw + i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
+        }
+    }
+    __syncthreads();
+    TRACE(2);
 
+    const int n_units = nseg + (R1 - R0);
+    TRACE_VAL(8, 1000000ull * 2 + n_units);
+    const uint32_t ring = lds_addr(smem);
+    float *s_X = reinterpret_cast<float *>(smem + kDecRing * kDecTileBytes);
+    Cursor prod{0, -1}, cons{0, -1};
+    for (int u = 0; u < kDecRing - 1 && u < n_units; ++u) {
+        issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + u * kDecTileBytes, wv, lane);
+        advance(prod, s_seg);
+    }
+
+    u32x4 qreg[9];  // this wave's half of the query operand: steps 9 (wv >> 1) .. + 9
     f32x4 acc[8];
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run = kNegInf, l_run = 0.f;
+    float m_ref = kNegInf, l_run = 0.f;
+    const int hf = wv >> 1;
+    const int kq = 16 * (wv & 1) + (lane & 15);             // key this lane scores
+    const int tr_key = 4 * g + ((lane & 15) >> 2);          // transposing-read source row
+    const int tr_dv = wv * 128 + 4 * (lane & 3);            // and its first value dim
 
-    for (int t = 0; t < ntiles; ++t) {
-        wait_dma_tiles(min(kDecRing - 2, ntiles - 1 - t));
+    TRACE(3);
+    for (int u = 0; u < n_units; ++u) {
+        wait_units_newer(min(kDecRing - 2, n_units - 1 - u));
         __syncthreads();
-        if (t + kDecRing - 1 < ntiles)
-            issue_tile(a, s_pages, lp0, k0 + (t + kDecRing - 1) * kKeysPerTile, k1,
-                       ring + ((t + kDecRing - 1) % kDecRing) * kTileBytes, wv, lane);
-        const char *tile = smem + (t % kDecRing) * kTileBytes;
-        const int kbase = k0 + t * kKeysPerTile;
-
-        f32x4 s[2];
-        score_tile(tile, qreg, lane, s);
-        float x[8];
+        if (prod.j < nseg) {
+            issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + ((u + kDecRing - 1) % kDecRing) * kDecTileBytes, wv,
+                       lane);
+            advance(prod, s_seg);
+        }
+        const char *slot = smem + (u % kDecRing) * kDecTileBytes;
+        const DecSeg sg = s_seg[cons.j];
+        if (cons.t < 0) {  // a new request: its query block
+#pragma unroll
+            for (int s2 = 0; s2 < 9; ++s2)
+                qreg[s2] = *reinterpret_cast<const u32x4 *>(slot + (h * kChunksPerRow + (9 * hf + s2) * 4 + g) * 16);
+            advance(cons, s_seg);
+            continue;
+        }
+        const int kbase = cons.t * kDecKeys;
+        // partial scores: keys 16 (wv & 1) .. + 16, dims of steps 9 hf .. 9 hf + 8
+        f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+        {
+            u32x4 av[9];
+#pragma unroll
+            for (int s2 = 0; s2 < 9; ++s2)
+                av[s2] = *reinterpret_cast<const u32x4 *>(slot + tile_off(kq, (9 * hf + s2) * 4 + g));
+#pragma unroll
+            for (int s2 = 0; s2 < 9; s2 += 2) {
+                sa = mfma_bf16(av[s2], qreg[s2], sa);
+                if (s2 + 1 < 9) sb = mfma_bf16(av[s2 + 1], qreg[s2 + 1], sb);
+            }
+        }
+        *reinterpret_cast<f32x4 *>(s_X + (wv * kHeads + h) * kXStride + 4 * g) = sa + sb;
+        __syncthreads();
+        // full scores of this lane's head: x[kt][i] = key 16 kt + 4 g + i (kt = 0, 1)
+        f32x4 x[2];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+            const f32x4 lo = *reinterpret_cast<const f32x4 *>(s_X + (kt * kHeads + h) * kXStride + 4 * g);
+            const f32x4 hi = *reinterpret_cast<const f32x4 *>(s_X + ((kt + 2) * kHeads + h) * kXStride + 4 * g);
+            x[kt] = lo + hi;
+        }
         float mt = kNegInf;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int key = kbase + 16 * (j >> 2) + 4 * g + (j & 3);
-            const float v = s[j >> 2][j & 3] * a.scale_log2;
-            x[j] = key < k1 ? v : kNegInf;
-            mt = fmaxf(mt, x[j]);
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                x[kt][i] = (kbase + 16 * kt + 4 * g + i <= sg.p) ? x[kt][i] * a.scale_log2 : kNegInf;
+                mt = fmaxf(mt, x[kt][i]);
+            }
         }
         mt = wave_max16(mt);
-        const float m_new = fmaxf(m_run, mt);
-        const float alpha = exp2f(m_run - m_new);
-        m_run = m_new;
+        // Lazy rescale (the same decision in every wave): keep the reference max
+        // unless the tile max exceeds it by more than 2^8.
+        if (__builtin_amdgcn_ballot_w64(mt > m_ref + 8.f) != 0) {
+            const float m_new = fmaxf(m_ref, mt);
+            const float alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
+#pragma unroll
+            for (int mt2 = 0; mt2 < 8; ++mt2) acc[mt2] = acc[mt2] * alpha;
+            l_run *= alpha;
+            m_ref = m_new;
+        }
+        // probabilities, split into bf16 hi + lo so that P*V keeps ~16 bits;
+        // slot 8 g + 4 kt + i of the B operand holds key 16 kt + 4 g + i
+        uint32_t bh[4], bl[4];
         float ps = 0.f;
-        uint32_t ph[4], pl[4];
 #pragma unroll
-        for (int j = 0; j < 8; j += 2) {
-            const float p0 = exp2f(x[j] - m_new), p1 = exp2f(x[j + 1] - m_new);
-            ps += p0 + p1;
-            const __bf16 h0 = (__bf16)p0, h1 = (__bf16)p1;
-            const __bf16 l0 = (__bf16)(p0 - (float)h0), l1 = (__bf16)(p1 - (float)h1);
-            ph[j >> 1] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
-            pl[j >> 1] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int i = 0; i < 4; i += 2) {
+                const float p0 = (x[kt][i] == kNegInf) ? 0.f : exp2f(x[kt][i] - m_ref);
+                const float p1 = (x[kt][i + 1] == kNegInf) ? 0.f : exp2f(x[kt][i + 1] - m_ref);
+                ps += p0 + p1;
+                const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
+                bh[kt * 2 + (i >> 1)] = h0 | (h1 << 16);
+                bl[kt * 2 + (i >> 1)] = bf16_bits(p0 - bf16_bits_to_float(h0)) |
+                                        (bf16_bits(p1 - bf16_bits_to_float(h1)) << 16);
+            }
         }
-        l_run = l_run * alpha + ps;
-        const u32x4 bh = {ph[0], ph[1], ph[2], ph[3]};
-        const u32x4 bl = {pl[0], pl[1], pl[2], pl[3]};
+        l_run += ps;
+        u32x4 vop[8];
 #pragma unroll
         for (int mt2 = 0; mt2 < 8; ++mt2) {
-            const int dv = wv * 128 + mt2 * 16 + (lane & 15);
-            const int c = dv >> 3, e = dv & 7;
-            uint32_t w[4];
-#pragma unroll
-            for (int j = 0; j < 8; j += 2) {
-                const int k0j = 16 * (j >> 2) + 4 * g + (j & 3);
-                const int k1j = k0j + 1;
-                const uint32_t v0 = *reinterpret_cast<const uint16_t *>(tile + tile_off(k0j, c) + e * 2);
-                const uint32_t v1 = *reinterpret_cast<const uint16_t *>(tile + tile_off(k1j, c) + e * 2);
-                w[j >> 1] = v0 | (v1 << 16);
-            }
-            const u32x4 av = {w[0], w[1], w[2], w[3]};
-            acc[mt2] = acc[mt2] * alpha;
-            acc[mt2] = mfma_bf16(av, bh, acc[mt2]);
-            acc[mt2] = mfma_bf16(av, bl, acc[mt2]);
+            const int dv = tr_dv + mt2 * 16;
+            const int byte = ((dv >> 2) & 1) * 8;
+            const u32x2 lo = lds_read_tr16(slot + tile_off(tr_key, dv >> 3) + byte);
+            const u32x2 hi = lds_read_tr16(slot + tile_off(tr_key + 16, dv >> 3) + byte);
+            vop[mt2] = u32x4{lo[0], lo[1], hi[0], hi[1]};
         }
-    }
+        const u32x4 opb_h = {bh[0], bh[1], bh[2], bh[3]};
+        const u32x4 opb_l = {bl[0], bl[1], bl[2], bl[3]};
+#pragma unroll
+        for (int mt2 = 0; mt2 < 8; ++mt2) acc[mt2] = mfma_bf16(vop[mt2], opb_h, acc[mt2]);
+#pragma unroll
+        for (int mt2 = 0; mt2 < 8; ++mt2) acc[mt2] = mfma_bf16(vop[mt2], opb_l, acc[mt2]);
 
-    const float l_tot = wave_sum16(l_run);
-    if (nks == 1) {
-        const float inv = 1.f / l_tot;
-        if (a.out_bf16) {
-            uint16_t *o = reinterpret_cast<uint16_t *>(a.out) + ((size_t)row * kHeads + h) * kDv;
+        const int jseg = cons.j;
+        advance(cons, s_seg);
+        if (cons.j != jseg) {  // the segment's last tile: finish it
+            const float l_tot = wave_sum16(l_run);
+            if (sg.t0 == 0 && sg.t1 == dec_tiles(sg.p, 1)) {
+                const float inv = 1.f / l_tot;
 #pragma unroll
-            for (int mt2 = 0; mt2 < 8; ++mt2) {
-                const int dv = wv * 128 + mt2 * 16 + 4 * g;
-                uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][0] * inv)) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][1] * inv)) << 16);
-                uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][2] * inv)) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][3] * inv)) << 16);
-                *reinterpret_cast<u32x2 *>(o + dv) = u32x2{w0, w1};
+                for (int mt2 = 0; mt2 < 8; ++mt2)
+                    store_out4(a, sg.row, h, wv * 128 + mt2 * 16 + 4 * g, acc[mt2] * inv);
+                if (a.lse && wv == 0 && g == 0) a.lse[(size_t)sg.row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
+            } else if (a.ws_dec_o != nullptr) {
+                const size_t slot_id = 2 * (size_t)w + (jseg == 0 ? 0 : 1);
+                float *po = a.ws_dec_o + (slot_id * kHeads + h) * kDv;
+#pragma unroll
+                for (int mt2 = 0; mt2 < 8; ++mt2)
+                    *reinterpret_cast<f32x4 *>(po + wv * 128 + mt2 * 16 + 4 * g) = acc[mt2];
+                if (wv == 0 && g == 0) {
+                    a.ws_dec_ml[(slot_id * kHeads + h) * 2 + 0] = m_ref;
+                    a.ws_dec_ml[(slot_id * kHeads + h) * 2 + 1] = l_tot;
+                }
             }
-        } else {
-            float *o = reinterpret_cast<float *>(a.out) + ((size_t)row * kHeads + h) * kDv;
 #pragma unroll
-            for (int mt2 = 0; mt2 < 8; ++mt2) {
-                const int dv = wv * 128 + mt2 * 16 + 4 * g;
-                *reinterpret_cast<f32x4 *>(o + dv) = acc[mt2] * inv;
-            }
-        }
-        if (a.lse && wv == 0 && g == 0) a.lse[(size_t)row * kHeads + h] = (m_run + log2f(l_tot)) * kLn2;
-    } else {
-        float *po = a.ws_dec_o + ((size_t)item * kHeads + h) * kDv;
-#pragma unroll
-        for (int mt2 = 0; mt2 < 8; ++mt2) {
-            const int dv = wv * 128 + mt2 * 16 + 4 * g;
-            *reinterpret_cast<f32x4 *>(po + dv) = acc[mt2];
-        }
-        if (wv == 0 && g == 0) {
-            a.ws_dec_ml[((size_t)item * kHeads + h) * 2 + 0] = m_run;
-            a.ws_dec_ml[((size_t)item * kHeads + h) * 2 + 1] = l_tot;
+            for (int mt2 = 0; mt2 < 8; ++mt2) acc[mt2] = f32x4{0.f, 0.f, 0.f, 0.f};
+            m_ref = kNegInf;
+            l_run = 0.f;
         }
     }
+    TRACE(4);
+}
+
+// Merge kernel side: workgroup w finishes the request (if any) that started in
+// an earlier workgroup's share and ends in its own.
+__device__ void decode_merge(const AttnArgs &a, int w, int *s_tmp, DecSeg *s_seg) {
+    const int S = a.dec_tiles_per_wg;
+    const int R0 = w * S, R1 = min(R0 + S, a.dec_total_tiles);
+    if (R0 >= R1 || a.ws_dec_o == nullptr) return;
+    if (find_segments(a, R0, R1, s_seg, s_tmp) == 0) return;
+    const DecSeg sg = s_seg[0];
+    const int nt = dec_tiles(sg.p, 1);
+    if (sg.t0 == 0 || sg.t1 != nt) return;  // starts here, or continues past this share
+    const int T = R0 - sg.t0;                // the request's first tile in the list
+    const int w0 = T / S;
+    const int tid = threadIdx.x, hh = tid >> 4, d0 = (tid & 15) * 32;
+    float mmax = kNegInf;
+    for (int v = w0; v <= w; ++v) {
+        const size_t sl = 2 * (size_t)v + ((v == w0 && T != w0 * S) ? 1 : 0);
+        mmax = fmaxf(mmax, a.ws_dec_ml[(sl * kHeads + hh) * 2]);
+    }
+    float denom = 0.f;
+    f32x4 o[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int v = w0; v <= w; ++v) {
+        const size_t sl = 2 * (size_t)v + ((v == w0 && T != w0 * S) ? 1 : 0);
+        const float ms = a.ws_dec_ml[(sl * kHeads + hh) * 2];
+        const float wt = (ms == kNegInf) ? 0.f : exp2f(ms - mmax);
+        denom += wt * a.ws_dec_ml[(sl * kHeads + hh) * 2 + 1];
+        const f32x4 *src = reinterpret_cast<const f32x4 *>(a.ws_dec_o + (sl * kHeads + hh) * kDv + d0);
+        f32x4 vv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) vv[k] = src[k];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) o[k] += wt * vv[k];
+    }
+    const float inv = 1.f / denom;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) store_out4(a, sg.row, hh, d0 + 4 * k, o[k] * inv);
+    if (a.lse && (tid & 15) == 0) a.lse[(size_t)sg.row * kHeads + hh] = (mmax + log2f(denom)) * kLn2;
 }
 
 // ------------------------------------------------------------- chunk path
@@ -389,15 +752,20 @@ __device__ __forceinline__ int vt_off(int dv, int slot) {
 }
 
 __device__ __forceinline__ void convert_values(const char *tile, char *vt, int tid) {
+    u32x4 kqs[2][4];
+#pragma unroll
+    for (int rep = 0; rep < 2; ++rep) {
+        const int pr = tid + rep * kThreads;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+            kqs[rep][kk] = *reinterpret_cast<const u32x4 *>(tile + tile_off((pr >> 6) * 4 + kk, pr & 63));
+    }
 #pragma unroll
     for (int rep = 0; rep < 2; ++rep) {
         const int pr = tid + rep * kThreads;
         const int c = pr & 63;   // value chunk: dims 8c .. 8c+7
         const int qd = pr >> 6;  // key quad: keys 4 qd .. 4 qd + 3
-        u32x4 kq[4];
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-            kq[kk] = *reinterpret_cast<const u32x4 *>(tile + tile_off(qd * 4 + kk, c));
+        const u32x4 *kq = kqs[rep];
         const int slot = 8 * (qd & 3) + 4 * (qd >> 2);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -414,54 +782,61 @@ __device__ __forceinline__ void convert_values(const char *tile, char *vt, int t
 }
 
 __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages) {
-    int r, local;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, r, local)) return;
-    const ChunkItem it = decode_chunk_item(a, r, local);
+    Located lc;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
+    const ChunkItem it = decode_chunk_item(a, lc);
+    TRACE(1);
+    const int r = it.r;
     if (it.k0 >= it.k1) return;  // key range past this block's causal limit
     if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;
     if (it.nks_eff > 1 && a.ws_chunk_o == nullptr) return;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
-    const int my_i = it.i0 + wv;            // this wave's token within the request
+    const int my_i = it.i0 + wv;     // this wave's token within the request
     const bool active = my_i < it.i1;
-    const int my_lim = it.p + my_i;         // last key this token may see
-    const int ntiles = ceil_div(it.k1 - it.k0, kKeysPerTile);
+    const int my_lim = it.p + my_i;  // last key this token may see
+    const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
     __syncthreads();
+    TRACE(2);
+    TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
     const uint32_t ring = lds_addr(smem);
-    char *vt = smem + kChunkRing * kTileBytes;
+    char *vt = smem + kChunkRing * kChunkTileBytes;
     for (int t = 0; t < kChunkRing - 1 && t < ntiles; ++t)
-        issue_tile(a, s_pages, lp0, it.k0 + t * kKeysPerTile, it.k1, ring + t * kTileBytes, wv, lane);
-
+        issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + t * kChunkKeys, it.k1, ring + t * kChunkTileBytes, wv, lane);
     u32x4 qreg[18];
-    const int qrow = it.row0 + (active ? my_i : it.i0);
-    {
-        const uint16_t *qp = a.q + ((size_t)qrow * kHeads + h) * kDqk + g * 8;
-#pragma unroll
-        for (int st = 0; st < 18; ++st) qreg[st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    load_query(a, it.row0 + (active ? my_i : it.i0), lane, qreg);
+    wait_vm_all();
+
     f32x4 acc[32];
 #pragma unroll
     for (int mt = 0; mt < 32; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_ref = kNegInf, l_run = 0.f;
 
+    TRACE(3);
     for (int t = 0; t < ntiles; ++t) {
-        wait_dma_tiles(min(kChunkRing - 2, ntiles - 1 - t));
+        TRACE_TILE(t, 10);
+        if (t + 1 < ntiles)
+            wait_dma_keep9();  // tile t + 1 may stay in flight
+        else
+            wait_dma_all();
         __syncthreads();
         if (t + kChunkRing - 1 < ntiles)
-            issue_tile(a, s_pages, lp0, it.k0 + (t + kChunkRing - 1) * kKeysPerTile, it.k1,
-                       ring + ((t + kChunkRing - 1) % kChunkRing) * kTileBytes, wv, lane);
-        const char *tile = smem + (t % kChunkRing) * kTileBytes;
+            issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + (t + kChunkRing - 1) * kChunkKeys, it.k1,
+                                   ring + ((t + kChunkRing - 1) % kChunkRing) * kChunkTileBytes, wv, lane);
+        const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
+        TRACE_TILE(t, 11);
         convert_values(tile, vt, tid);
         __syncthreads();
+        TRACE_TILE(t, 12);
         if (!active) continue;
-        const int kbase = it.k0 + t * kKeysPerTile;
+        const int kbase = it.k0 + t * kChunkKeys;
         f32x4 s[2];
-        score_tile(tile, qreg, lane, s);
+        score32(tile, qreg, lane, s);
+        TRACE_TILE(t, 13);
         float x[8];
         float mt = kNegInf;
 #pragma unroll
@@ -474,8 +849,7 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         mt = wave_max16(mt);
         // Lazy rescale: keep the reference max unless the tile max exceeds it
         // by more than 2^8 (probabilities then stay <= 256, exact range for fp16).
-        const bool grow = mt > m_ref + 8.f;
-        if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+        if (__builtin_amdgcn_ballot_w64(mt > m_ref + 8.f) != 0) {
             const float m_new = fmaxf(m_ref, mt);
             const float alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
 #pragma unroll
@@ -493,132 +867,88 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
             pv[j] = hj;
         }
         l_run += ps;
+        TRACE_TILE(t, 14);
         const u32x4 bop = __builtin_bit_cast(u32x4, pv);
 #pragma unroll
-        for (int mt2 = 0; mt2 < 32; ++mt2) {
-            const int dv = mt2 * 16 + (lane & 15);
-            const u32x4 av = *reinterpret_cast<const u32x4 *>(vt + vt_off(dv, 8 * g));
-            acc[mt2] = mfma_f16(av, bop, acc[mt2]);
+        for (int grp = 0; grp < 4; ++grp) {
+            u32x4 av[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                av[j] = *reinterpret_cast<const u32x4 *>(vt + vt_off((grp * 8 + j) * 16 + (lane & 15), 8 * g));
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[grp * 8 + j] = mfma_f16(av[j], bop, acc[grp * 8 + j]);
+            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
         }
+        TRACE_TILE(t, 15);
     }
-    if (!active) return;
 
+    TRACE(4);
     const float l_tot = wave_sum16(l_run);
     const int row = it.row0 + my_i;
     if (it.nks_eff == 1) {
+        if (!active) return;
         const float inv = 1.f / l_tot;
-        if (a.out_bf16) {
-            uint16_t *o = reinterpret_cast<uint16_t *>(a.out) + ((size_t)row * kHeads + h) * kDv;
 #pragma unroll
-            for (int mt2 = 0; mt2 < 32; ++mt2) {
-                const int dv = mt2 * 16 + 4 * g;
-                uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][0] * inv)) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][1] * inv)) << 16);
-                uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][2] * inv)) |
-                              ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)(acc[mt2][3] * inv)) << 16);
-                *reinterpret_cast<u32x2 *>(o + dv) = u32x2{w0, w1};
-            }
-        } else {
-            float *o = reinterpret_cast<float *>(a.out) + ((size_t)row * kHeads + h) * kDv;
-#pragma unroll
-            for (int mt2 = 0; mt2 < 32; ++mt2) {
-                const int dv = mt2 * 16 + 4 * g;
-                *reinterpret_cast<f32x4 *>(o + dv) = acc[mt2] * inv;
-            }
-        }
+        for (int mt2 = 0; mt2 < 32; ++mt2) store_out4(a, row, h, mt2 * 16 + 4 * g, acc[mt2] * inv);
         if (a.lse && g == 0) a.lse[(size_t)row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
-    } else {
+        return;
+    }
+    if (active) {
         const size_t prow = (size_t)item * kChunkBlockTokens + wv;
         float *po = a.ws_chunk_o + (prow * kHeads + h) * kDv;
 #pragma unroll
-        for (int mt2 = 0; mt2 < 32; ++mt2) {
-            const int dv = mt2 * 16 + 4 * g;
-            *reinterpret_cast<f32x4 *>(po + dv) = acc[mt2];
-        }
+        for (int mt2 = 0; mt2 < 32; ++mt2) *reinterpret_cast<f32x4 *>(po + mt2 * 16 + 4 * g) = acc[mt2];
         if (g == 0) {
             a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref;
             a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l_tot;
         }
     }
+    TRACE(5);
 }
 
 __global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) char smem[kMainLds];
-    __shared__ int s_tmp[8];
+    __shared__ int s_tmp[12];
     __shared__ int s_pages[kPageWindow];
+    __shared__ DecSeg s_seg[kMaxSeg];
     const int b = blockIdx.x;
-    if (b < a.n_chunk_items)
-        chunk_item(a, b, smem, s_tmp, s_pages);
+    TRACE(0);
+#ifdef MLA_TRACE
+    if (threadIdx.x == 0 && b < (1 << 16)) {
+        unsigned xcc, hw;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+        g_trace[(size_t)b * 16 + 9] = ((unsigned long long)xcc << 32) | hw;
+    }
+#endif
+    if (b < a.n_dec_wg)
+        decode_wg(a, b, smem, s_tmp, s_pages, s_seg);
     else
-        decode_item(a, b - a.n_chunk_items, smem, s_tmp, s_pages);
+        chunk_item(a, b - a.n_dec_wg, smem, s_tmp, s_pages);
+    TRACE(7);
 }
 
-// ------------------------------------------------------------------ merge
-// Combine the key-split partials of one row: m_s, l_s in log2 units, o_s
-// unnormalised.  256 threads: head = tid / 16, dims (tid % 16) * 32 .. +32.
-__device__ void merge_row(const float *po, const float *pml, size_t stride_o, size_t stride_ml, int nsplit,
-                          void *out, int out_bf16, float *lse, int row) {
-    const int tid = threadIdx.x;
-    const int hh = tid >> 4, d0 = (tid & 15) * 32;
-    float mmax = kNegInf;
-    for (int s = 0; s < nsplit; ++s) mmax = fmaxf(mmax, pml[s * stride_ml + hh * 2]);
-    float denom = 0.f;
-    f32x4 o[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < nsplit; ++s) {
-        const float ms = pml[s * stride_ml + hh * 2];
-        const float w = (ms == kNegInf) ? 0.f : exp2f(ms - mmax);
-        denom += w * pml[s * stride_ml + hh * 2 + 1];
-        const f32x4 *src = reinterpret_cast<const f32x4 *>(po + s * stride_o + hh * kDv + d0);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) o[k] += w * src[k];
-    }
-    const float inv = 1.f / denom;
-    if (out_bf16) {
-        uint16_t *dst = reinterpret_cast<uint16_t *>(out) + ((size_t)row * kHeads + hh) * kDv + d0;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const f32x4 v = o[k] * inv;
-            uint32_t w0 = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[0]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[1]) << 16);
-            uint32_t w1 = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[2]) |
-                          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)v[3]) << 16);
-            *reinterpret_cast<u32x2 *>(dst + 4 * k) = u32x2{w0, w1};
-        }
-    } else {
-        f32x4 *dst = reinterpret_cast<f32x4 *>(reinterpret_cast<float *>(out) + ((size_t)row * kHeads + hh) * kDv + d0);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) dst[k] = o[k] * inv;
-    }
-    if (lse && (tid & 15) == 0) lse[(size_t)row * kHeads + hh] = (mmax + log2f(denom)) * kLn2;
-}
-
+// Split merges, after the attention kernel (the kernel boundary makes every
+// partial visible): first one workgroup per decode workgroup, then one per
+// chunk item (the item with key split 0 merges its row block).
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
-    __shared__ int s_tmp[8];
+    __shared__ int s_tmp[12];
+    __shared__ DecSeg s_seg[kMaxSeg];
     const int b = blockIdx.x;
-    int r, local;
-    if (b < a.n_chunk_items) {
-        if (!locate_item(b, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, r, local)) return;
-        const ChunkItem it = decode_chunk_item(a, r, local);
-        if (it.k0 != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr) return;
-        if (it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;
-        const size_t so = (size_t)kChunkBlockTokens * kPartialFloats;
-        const size_t sm = (size_t)kChunkBlockTokens * kPartialStats;
-        for (int i = it.i0; i < it.i1; ++i) {
-            const size_t prow = (size_t)b * kChunkBlockTokens + (i - it.i0);
-            merge_row(a.ws_chunk_o + prow * kPartialFloats, a.ws_chunk_ml + prow * kPartialStats, so, sm, it.nks_eff,
-                      a.out, a.out_bf16, a.lse, it.row0 + i);
-        }
-    } else {
-        const int item = b - a.n_chunk_items;
-        if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, DecCount{a.ks_dec}, s_tmp, r, local)) return;
-        const int nks = ceil_div(a.prefix[r] + 1, a.ks_dec);
-        if (local != 0 || nks <= 1 || a.ws_dec_o == nullptr) return;
-        if (a.cu_q[r] < 0 || a.cu_q[r] >= a.num_rows) return;
-        merge_row(a.ws_dec_o + (size_t)item * kPartialFloats, a.ws_dec_ml + (size_t)item * kPartialStats,
-                  kPartialFloats, kPartialStats, nks, a.out, a.out_bf16, a.lse, a.cu_q[r]);
+    if (b < a.n_dec_wg) {
+        decode_merge(a, b, s_tmp, s_seg);
+        return;
     }
+    Located lc;
+    if (!locate_item(b - a.n_dec_wg, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
+    const ChunkItem it = decode_chunk_item(a, lc);
+    if (it.ks != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr) return;
+    if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;
+    const size_t first = (size_t)(b - a.n_dec_wg) * kChunkBlockTokens;
+    merge_block(a, a.ws_chunk_o + first * kPartialFloats, a.ws_chunk_ml + first * kPartialStats,
+                (size_t)kChunkBlockTokens * kPartialFloats, (size_t)kChunkBlockTokens * kPartialStats, it.nks_eff,
+                it.row0 + it.i0, it.i1 - it.i0);
 }
 
 // ----------------------------------------------------------------- append
@@ -638,29 +968,72 @@ __device__ __forceinline__ int find_request(const int32_t *cu_q, int num_reqs, i
     return lo;
 }
 
-constexpr int kAppendRowsPerWave = 4;
+constexpr int kAppendRowsPerWave = 8;
 
+// Each wave copies 8 consecutive rows.  Source rows are loaded first (they do
+// not depend on the lookup); the owning requests come from one window of 64
+// consecutive cu_q / prefix entries, so a wave needs one dependent round for
+// the lengths and one for the page ids.
 __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int row_base = (blockIdx.x * 4 + wv) * kAppendRowsPerWave;
+    const int row0 = (blockIdx.x * 4 + wv) * kAppendRowsPerWave;
+    if (row0 >= a.num_rows) return;
+    const int nrows = min(kAppendRowsPerWave, a.num_rows - row0);
+    u32x4 va[kAppendRowsPerWave], vb[kAppendRowsPerWave];
 #pragma unroll
     for (int k = 0; k < kAppendRowsPerWave; ++k) {
-        const int row = row_base + k;
-        if (row >= a.num_rows) return;
-        const int r = find_request(a.cu_q, a.num_reqs, row, lane);
-        const int t = a.prefix[r] + (row - a.cu_q[r]);
+        va[k] = u32x4{0u, 0u, 0u, 0u};
+        vb[k] = u32x4{0u, 0u, 0u, 0u};
+        if (k < nrows) {
+            const u32x4 *src = reinterpret_cast<const u32x4 *>(a.src + (size_t)(row0 + k) * kDqk);
+            va[k] = src[lane];
+            if (lane < kChunksPerRow - 64) vb[k] = src[64 + lane];
+        }
+    }
+    const int r0 = a.num_reqs <= 64 ? 0 : find_request(a.cu_q, a.num_reqs, row0, lane);
+    const int wi = r0 + lane;
+    const int cw = wi <= a.num_reqs ? a.cu_q[wi] : INT_MAX;
+    const int pw = wi < a.num_reqs ? a.prefix[wi] : 0;
+    int page[kAppendRowsPerWave], slot_in_page[kAppendRowsPerWave];
+#pragma unroll
+    for (int k = 0; k < kAppendRowsPerWave; ++k) {
+        page[k] = -1;
+        slot_in_page[k] = 0;
+        if (k >= nrows) continue;
+        const int row = row0 + k;
+        const uint64_t m = __builtin_amdgcn_ballot_w64(cw <= row);
+        const int cnt = __builtin_popcountll(m);
+        int r, start, pr;
+        if (cnt >= 1 && (cnt < 64 || r0 + 64 > a.num_reqs)) {
+            r = r0 + cnt - 1;
+            start = __shfl(cw, cnt - 1, 64);
+            pr = __shfl(pw, cnt - 1, 64);
+        } else {  // beyond the window (or inconsistent cu_q): search again
+            r = find_request(a.cu_q, a.num_reqs, row, lane);
+            start = a.cu_q[r];
+            pr = a.prefix[r];
+        }
+        const int t = pr + (row - start);
         const int lp = t >> a.log2_page;
-        const int page = (t >= 0 && lp < a.max_pages) ? a.bt[(size_t)r * a.max_pages + lp] : -1;
-        if ((unsigned)page >= (unsigned)a.num_pages) continue;
-        const size_t slot = (size_t)page * a.page_size + (t & (a.page_size - 1));
-        const u32x4 *src = reinterpret_cast<const u32x4 *>(a.src + (size_t)row * kDqk);
-        u32x4 *dst = reinterpret_cast<u32x4 *>(a.kv + slot * kDqk);
-        dst[lane] = src[lane];
-        if (lane < kChunksPerRow - 64) dst[64 + lane] = src[64 + lane];
+        if (t >= 0 && lp < a.max_pages && r < a.num_reqs) page[k] = a.bt[(size_t)r * a.max_pages + lp];
+        slot_in_page[k] = t & (a.page_size - 1);
+    }
+#pragma unroll
+    for (int k = 0; k < kAppendRowsPerWave; ++k) {
+        if (k >= nrows || (unsigned)page[k] >= (unsigned)a.num_pages) continue;
+        u32x4 *dst = reinterpret_cast<u32x4 *>(a.kv + ((size_t)page[k] * a.page_size + slot_in_page[k]) * kDqk);
+        dst[lane] = va[k];
+        if (lane < kChunksPerRow - 64) dst[64 + lane] = vb[k];
     }
 }
 
 }  // namespace
+
+#ifdef MLA_TRACE
+extern "C" int mla_trace_read(void *dst, size_t bytes) {
+    return (int)hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_trace), bytes, 0, hipMemcpyDeviceToHost);
+}
+#endif
 
 hipError_t launch_append(const AppendArgs &a, hipStream_t s) {
     const int rows_per_block = 4 * kAppendRowsPerWave;
@@ -671,14 +1044,14 @@ hipError_t launch_append(const AppendArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_attention(const AttnArgs &a, hipStream_t s) {
-    const int grid = a.n_chunk_items + a.n_dec_items;
+    const int grid = a.n_dec_wg + a.n_chunk_items;
     if (grid == 0) return hipSuccess;
     hipLaunchKernelGGL(attention_kernel, dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_combine(const AttnArgs &a, hipStream_t s) {
-    const int grid = a.n_chunk_items + a.n_dec_items;
+    const int grid = a.n_dec_wg + a.n_chunk_items;
     if (grid == 0) return hipSuccess;
     hipLaunchKernelGGL(combine_kernel, dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
