@@ -44,11 +44,7 @@ constexpr int kDecLds = kDecRing * kDecTileBytes + 4 * kHeads * 20 * 4;  // ring
 // chunk path
 constexpr int kChunkKeys = kKeysPerTile;  // 32
 constexpr int kChunkTileBytes = kChunkKeys * kRowBytes;  // 36864
-constexpr int kChunkRing = 3;
-constexpr int kVtStride = 80;  // bytes per dv row of V^T (32 fp16 + pad)
-constexpr int kVtBytes = kDv * kVtStride;
-constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kVtBytes;
-constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
+
 constexpr float kNegInf = -INFINITY;
 
 // Optional per-workgroup timeline for profiling builds (-DMLA_TRACE): slot k
@@ -124,15 +120,20 @@ __device__ __forceinline__ f32x4 mfma_f16(u32x4 a, u32x4 b, f32x4 c) {
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float wave_max16(float v) {  // reduce over lanes l, l^16, l^32, l^48
-    v = fmaxf(v, __shfl_xor(v, 16, 64));
-    v = fmaxf(v, __shfl_xor(v, 32, 64));
-    return v;
+// Reductions over lanes l, l^16, l^32, l^48 (the four row groups of a
+// 16-column MFMA tile) with the gfx950 cross-row swaps: permlane32_swap pairs
+// lane l with l +- 32, permlane16_swap pairs row groups 0-1 and 2-3.
+__device__ __forceinline__ float wave_max16(float v) {
+    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float wave_sum16(float v) {
-    v += __shfl_xor(v, 16, 64);
-    v += __shfl_xor(v, 32, 64);
-    return v;
+    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // LDS byte offset of 16-byte chunk c of key k inside a tile.  Chunk
@@ -299,33 +300,6 @@ __device__ __forceinline__ f32x4 score16(const char *tile, int key_base, const u
         __builtin_amdgcn_sched_group_barrier(0x008, G, 0);
     }
     return acc0 + acc1;
-}
-
-// 32 keys (two 16-key halves), same layout per half.
-__device__ __forceinline__ void score32(const char *tile, const u32x4 *qreg, int lane, f32x4 s[2]) {
-    const int g = lane >> 4;
-    const int key0 = lane & 15, key1 = 16 + (lane & 15);
-    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    constexpr int G = 6;
-#pragma unroll
-    for (int grp = 0; grp < 18 / G; ++grp) {
-        u32x4 a0[G], a1[G];
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            const int st = grp * G + j;
-            a0[j] = *reinterpret_cast<const u32x4 *>(tile + tile_off(key0, st * 4 + g));
-            a1[j] = *reinterpret_cast<const u32x4 *>(tile + tile_off(key1, st * 4 + g));
-        }
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            acc0 = mfma_bf16(a0[j], qreg[grp * G + j], acc0);
-            acc1 = mfma_bf16(a1[j], qreg[grp * G + j], acc1);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * G, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * G, 0);
-    }
-    s[0] = acc0;
-    s[1] = acc1;
 }
 
 __device__ __forceinline__ void load_query(const AttnArgs &a, int row, int lane, u32x4 *qreg) {
@@ -576,6 +550,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
 
     TRACE(3);
     for (int u = 0; u < n_units; ++u) {
+        TRACE_TILE(u, 10);
         wait_units_newer(min(kDecRing - 2, n_units - 1 - u));
         __syncthreads();
         if (prod.j < nseg) {
@@ -592,6 +567,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
             advance(cons, s_seg);
             continue;
         }
+        TRACE_TILE(u, 11);
         const int kbase = cons.t * kDecKeys;
         // partial scores: keys 16 (wv & 1) .. + 16, dims of steps 9 hf .. 9 hf + 8
         f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
@@ -608,6 +584,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
         }
         *reinterpret_cast<f32x4 *>(s_X + (wv * kHeads + h) * kXStride + 4 * g) = sa + sb;
         __syncthreads();
+        TRACE_TILE(u, 12);
         // full scores of this lane's head: x[kt][i] = key 16 kt + 4 g + i (kt = 0, 1)
         f32x4 x[2];
 #pragma unroll
@@ -654,6 +631,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
             }
         }
         l_run += ps;
+        TRACE_TILE(u, 13);
         u32x4 vop[8];
 #pragma unroll
         for (int mt2 = 0; mt2 < 8; ++mt2) {
@@ -670,6 +648,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
 #pragma unroll
         for (int mt2 = 0; mt2 < 8; ++mt2) acc[mt2] = mfma_bf16(vop[mt2], opb_l, acc[mt2]);
 
+        TRACE_TILE(u, 14);
         const int jseg = cons.j;
         advance(cons, s_seg);
         if (cons.j != jseg) {  // the segment's last tile: finish it
@@ -741,45 +720,53 @@ __device__ void decode_merge(const AttnArgs &a, int w, int *s_tmp, DecSeg *s_seg
 }
 
 // ------------------------------------------------------------- chunk path
-// Convert the value part of a tile (keys 0..31, dims 0..511, bf16) into a
-// transposed fp16 copy vt[dv][slot] (row stride 80 bytes, four 16-byte slot
-// groups per row, group q of row dv stored at position q ^ ((dv / 8) % 4) so
-// that lanes writing rows 8 apart spread over the banks).  Slot order matches
-// the score layout: slot 8 g + 4 kt + i holds key 16 kt + 4 g + i, so the
-// probabilities a lane already holds are the MFMA's B operand as they are.
-__device__ __forceinline__ int vt_off(int dv, int slot) {
-    return dv * kVtStride + ((((slot >> 3) ^ (dv >> 3)) & 3) << 4) + (slot & 7) * 2;
+// Chunk rows: one workgroup per block of 4 query tokens (wave w scores token
+// i0 + w: 16 head rows) and a key range of ks_chunk keys.  32-key tiles
+// stream through a 4-slot DMA ring.  Per tile, each wave scores its token
+// against all 576 latent dims, updates that token's running max and sum, and
+// publishes the token's probabilities (bf16 hi + lo, already in MFMA
+// B-operand order) and rescale factor in LDS.  Then every wave accumulates
+// its 128-wide slice of the value dims for all 4 tokens, so each transposed
+// V^T operand read feeds 8 MFMAs.  V stays bf16; hi + lo keeps P to ~16 bits.
+__device__ __forceinline__ void score_bases(int key, int g, int base[2]) {
+    // chunk 4 st + g of `key` sits at base[st & 1] + 128 (st >> 1): the xor
+    // swizzle only touches the chunk index's low 3 bits
+#pragma unroll
+    for (int e = 0; e < 2; ++e) base[e] = (key * kChunksPerRow + ((4 * e + g) ^ (key & 7))) * 16;
 }
 
-__device__ __forceinline__ void convert_values(const char *tile, char *vt, int tid) {
-    u32x4 kqs[2][4];
+// Scores of one 32-key tile for one token: s[kt][i] = key 16 kt + 4 g + i, head l%16.
+__device__ __forceinline__ void score32(const char *tile, const u32x4 *qreg, int lane, f32x4 s[2]) {
+    const int g = lane >> 4;
+    int b0[2], b1[2];
+    score_bases(lane & 15, g, b0);
+    score_bases(16 + (lane & 15), g, b1);
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    constexpr int G = 6;
 #pragma unroll
-    for (int rep = 0; rep < 2; ++rep) {
-        const int pr = tid + rep * kThreads;
+    for (int grp = 0; grp < 18 / G; ++grp) {
+        u32x4 a0[G], a1[G];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-            kqs[rep][kk] = *reinterpret_cast<const u32x4 *>(tile + tile_off((pr >> 6) * 4 + kk, pr & 63));
-    }
-#pragma unroll
-    for (int rep = 0; rep < 2; ++rep) {
-        const int pr = tid + rep * kThreads;
-        const int c = pr & 63;   // value chunk: dims 8c .. 8c+7
-        const int qd = pr >> 6;  // key quad: keys 4 qd .. 4 qd + 3
-        const u32x4 *kq = kqs[rep];
-        const int slot = 8 * (qd & 3) + 4 * (qd >> 2);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            f16x4 hv;
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const uint32_t word = kq[kk][e >> 1];
-                const uint32_t bits = (e & 1) ? (word >> 16) : (word & 0xffffu);
-                hv[kk] = (_Float16)bf16_bits_to_float(bits);
-            }
-            *reinterpret_cast<u32x2 *>(vt + vt_off(8 * c + e, slot)) = __builtin_bit_cast(u32x2, hv);
+        for (int j = 0; j < G; ++j) {
+            const int st = grp * G + j;
+            a0[j] = *reinterpret_cast<const u32x4 *>(tile + b0[st & 1] + 128 * (st >> 1));
+            a1[j] = *reinterpret_cast<const u32x4 *>(tile + b1[st & 1] + 128 * (st >> 1));
         }
+#pragma unroll
+        for (int j = 0; j < G; ++j) {
+            acc0 = mfma_bf16(a0[j], qreg[grp * G + j], acc0);
+            acc1 = mfma_bf16(a1[j], qreg[grp * G + j], acc1);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * G, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * G, 0);
     }
+    s[0] = acc0;
+    s[1] = acc1;
 }
+
+constexpr int kChunkRing = 4;
+constexpr int kPBytes = kChunkBlockTokens * 2 * 64 * 16;  // P hi / lo per token, per lane
+constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kPBytes + 2 * kChunkBlockTokens * kHeads * 4 + 16;
 
 __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages) {
     Located lc;
@@ -793,9 +780,9 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
-    const int my_i = it.i0 + wv;     // this wave's token within the request
-    const bool active = my_i < it.i1;
-    const int my_lim = it.p + my_i;  // last key this token may see
+    const int tok = it.i0 + wv;     // the token this wave scores
+    const bool active = tok < it.i1;
+    const int lim = it.p + tok;     // last key it may see
     const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
@@ -804,108 +791,146 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
     const uint32_t ring = lds_addr(smem);
-    char *vt = smem + kChunkRing * kChunkTileBytes;
+    u32x4 *s_P = reinterpret_cast<u32x4 *>(smem + kChunkRing * kChunkTileBytes);  // [token][hi, lo][lane]
+    float *s_alpha = reinterpret_cast<float *>(smem + kChunkRing * kChunkTileBytes + kPBytes);  // [token][head]
+    float *s_l = s_alpha + kChunkBlockTokens * kHeads;                                          // [token][head]
+    int *s_flag = reinterpret_cast<int *>(s_l + kChunkBlockTokens * kHeads);                    // [token]
     for (int t = 0; t < kChunkRing - 1 && t < ntiles; ++t)
         issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + t * kChunkKeys, it.k1, ring + t * kChunkTileBytes, wv, lane);
     u32x4 qreg[18];
-    load_query(a, it.row0 + (active ? my_i : it.i0), lane, qreg);
+    load_query(a, it.row0 + min(tok, it.i1 - 1), lane, qreg);  // an idle wave re-reads a valid row
     wait_vm_all();
 
-    f32x4 acc[32];
+    f32x4 acc[kChunkBlockTokens][8];  // [token][value-dim tile of this wave's 128-wide slice]
 #pragma unroll
-    for (int mt = 0; mt < 32; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_ref = kNegInf, l_run = 0.f;
+    for (int j = 0; j < kChunkBlockTokens; ++j)
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_ref = kNegInf, l_run = 0.f;  // this wave's token, head l%16
+    const int tr_key = 4 * g + ((lane & 15) >> 2);
+    const int tr_dv = wv * 128 + 4 * (lane & 3);
 
     TRACE(3);
     for (int t = 0; t < ntiles; ++t) {
         TRACE_TILE(t, 10);
-        if (t + 1 < ntiles)
-            wait_dma_keep9();  // tile t + 1 may stay in flight
-        else
-            wait_dma_all();
+        wait_units_newer(min(kChunkRing - 2, ntiles - 1 - t));
         __syncthreads();
         if (t + kChunkRing - 1 < ntiles)
             issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + (t + kChunkRing - 1) * kChunkKeys, it.k1,
                                    ring + ((t + kChunkRing - 1) % kChunkRing) * kChunkTileBytes, wv, lane);
         const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
-        TRACE_TILE(t, 11);
-        convert_values(tile, vt, tid);
-        __syncthreads();
-        TRACE_TILE(t, 12);
-        if (!active) continue;
         const int kbase = it.k0 + t * kChunkKeys;
-        f32x4 s[2];
-        score32(tile, qreg, lane, s);
+        TRACE_TILE(t, 11);
+        if (active) {
+            f32x4 s[2];
+            score32(tile, qreg, lane, s);
+            TRACE_TILE(t, 12);
+            float x[8];
+            float mt = kNegInf;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int key = kbase + 16 * (j >> 2) + 4 * g + (j & 3);
+                x[j] = (key < it.k1 && key <= lim) ? s[j >> 2][j & 3] * a.scale_log2 : kNegInf;
+                mt = fmaxf(mt, x[j]);
+            }
+            mt = wave_max16(mt);
+            // Lazy rescale: keep the reference max unless the tile max exceeds it
+            // by more than 2^8 (probabilities then stay <= 256).
+            const bool resc = __builtin_amdgcn_ballot_w64(mt > m_ref + 8.f) != 0;
+            float alpha = 1.f;
+            if (resc) {
+                const float m_new = fmaxf(m_ref, mt);
+                alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
+                m_ref = m_new;
+            }
+            uint32_t ph[4], pl[4];
+            float ps = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; j += 2) {
+                const float p0 = (x[j] == kNegInf) ? 0.f : exp2f(x[j] - m_ref);
+                const float p1 = (x[j + 1] == kNegInf) ? 0.f : exp2f(x[j + 1] - m_ref);
+                ps += p0 + p1;
+                const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
+                ph[j >> 1] = h0 | (h1 << 16);
+                pl[j >> 1] = bf16_bits(p0 - bf16_bits_to_float(h0)) | (bf16_bits(p1 - bf16_bits_to_float(h1)) << 16);
+            }
+            l_run = l_run * alpha + ps;
+            s_P[(wv * 2 + 0) * 64 + lane] = u32x4{ph[0], ph[1], ph[2], ph[3]};
+            s_P[(wv * 2 + 1) * 64 + lane] = u32x4{pl[0], pl[1], pl[2], pl[3]};
+            if (g == 0) s_alpha[wv * kHeads + h] = alpha;
+            if (lane == 0) s_flag[wv] = resc ? 1 : 0;
+        } else {  // idle wave: a zero token keeps the shared products finite
+            s_P[(wv * 2 + 0) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+            s_P[(wv * 2 + 1) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+            if (lane == 0) s_flag[wv] = 0;
+        }
+        __syncthreads();
         TRACE_TILE(t, 13);
-        float x[8];
-        float mt = kNegInf;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int key = kbase + 16 * (j >> 2) + 4 * g + (j & 3);
-            const float v = s[j >> 2][j & 3] * a.scale_log2;
-            x[j] = (key < it.k1 && key <= my_lim) ? v : kNegInf;
-            mt = fmaxf(mt, x[j]);
-        }
-        mt = wave_max16(mt);
-        // Lazy rescale: keep the reference max unless the tile max exceeds it
-        // by more than 2^8 (probabilities then stay <= 256, exact range for fp16).
-        if (__builtin_amdgcn_ballot_w64(mt > m_ref + 8.f) != 0) {
-            const float m_new = fmaxf(m_ref, mt);
-            const float alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
+        for (int j = 0; j < kChunkBlockTokens; ++j) {
+            if (s_flag[j] != 0) {
+                const float al = s_alpha[j * kHeads + h];
 #pragma unroll
-            for (int mt2 = 0; mt2 < 32; ++mt2) acc[mt2] = acc[mt2] * alpha;
-            l_run *= alpha;
-            m_ref = m_new;
+                for (int mt = 0; mt < 8; ++mt) acc[j][mt] = acc[j][mt] * al;
+            }
         }
-        float ps = 0.f;
-        f16x8 pv;
+        u32x4 bh[kChunkBlockTokens], bl[kChunkBlockTokens];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const float pj = (x[j] == kNegInf) ? 0.f : exp2f(x[j] - m_ref);
-            const _Float16 hj = (_Float16)pj;
-            ps += (float)hj;  // the normaliser sums exactly the weights the MFMA uses
-            pv[j] = hj;
+        for (int j = 0; j < kChunkBlockTokens; ++j) {
+            bh[j] = s_P[(j * 2 + 0) * 64 + lane];
+            bl[j] = s_P[(j * 2 + 1) * 64 + lane];
         }
-        l_run += ps;
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) {
+            const int dv = tr_dv + mt * 16;
+            const int byte = ((dv >> 2) & 1) * 8;
+            const u32x2 lo = lds_read_tr16(tile + tile_off(tr_key, dv >> 3) + byte);
+            const u32x2 hi = lds_read_tr16(tile + tile_off(tr_key + 16, dv >> 3) + byte);
+            const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
+#pragma unroll
+            for (int j = 0; j < kChunkBlockTokens; ++j) {
+                acc[j][mt] = mfma_bf16(av, bh[j], acc[j][mt]);
+                acc[j][mt] = mfma_bf16(av, bl[j], acc[j][mt]);
+            }
+        }
         TRACE_TILE(t, 14);
-        const u32x4 bop = __builtin_bit_cast(u32x4, pv);
-#pragma unroll
-        for (int grp = 0; grp < 4; ++grp) {
-            u32x4 av[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                av[j] = *reinterpret_cast<const u32x4 *>(vt + vt_off((grp * 8 + j) * 16 + (lane & 15), 8 * g));
-#pragma unroll
-            for (int j = 0; j < 8; ++j) acc[grp * 8 + j] = mfma_f16(av[j], bop, acc[grp * 8 + j]);
-            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-        }
-        TRACE_TILE(t, 15);
     }
 
     TRACE(4);
+    // running sums of all tokens, then each wave stores its value-dim slice
     const float l_tot = wave_sum16(l_run);
-    const int row = it.row0 + my_i;
-    if (it.nks_eff == 1) {
-        if (!active) return;
-        const float inv = 1.f / l_tot;
+    if (g == 0) s_l[wv * kHeads + h] = l_tot;
+    __syncthreads();
 #pragma unroll
-        for (int mt2 = 0; mt2 < 32; ++mt2) store_out4(a, row, h, mt2 * 16 + 4 * g, acc[mt2] * inv);
-        if (a.lse && g == 0) a.lse[(size_t)row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
-        return;
+    for (int j = 0; j < kChunkBlockTokens; ++j) {
+        const int tj = it.i0 + j;
+        if (tj >= it.i1) break;
+        const int row = it.row0 + tj;
+        if (it.nks_eff == 1) {
+            const float inv = 1.f / s_l[j * kHeads + h];
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) store_out4(a, row, h, wv * 128 + mt * 16 + 4 * g, acc[j][mt] * inv);
+        } else {
+            const size_t prow = (size_t)item * kChunkBlockTokens + j;
+            float *po = a.ws_chunk_o + (prow * kHeads + h) * kDv;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(po + wv * 128 + mt * 16 + 4 * g) = acc[j][mt];
+        }
     }
-    if (active) {
-        const size_t prow = (size_t)item * kChunkBlockTokens + wv;
-        float *po = a.ws_chunk_o + (prow * kHeads + h) * kDv;
-#pragma unroll
-        for (int mt2 = 0; mt2 < 32; ++mt2) *reinterpret_cast<f32x4 *>(po + mt2 * 16 + 4 * g) = acc[mt2];
-        if (g == 0) {
+    if (active && g == 0) {
+        const int row = it.row0 + tok;
+        if (it.nks_eff == 1) {
+            if (a.lse) a.lse[(size_t)row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
+        } else {
+            const size_t prow = (size_t)item * kChunkBlockTokens + wv;
             a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref;
             a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l_tot;
         }
     }
     TRACE(5);
 }
+
+constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
 
 __global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) char smem[kMainLds];
@@ -946,9 +971,10 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     if (it.ks != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr) return;
     if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;
     const size_t first = (size_t)(b - a.n_dec_wg) * kChunkBlockTokens;
-    merge_block(a, a.ws_chunk_o + first * kPartialFloats, a.ws_chunk_ml + first * kPartialStats,
-                (size_t)kChunkBlockTokens * kPartialFloats, (size_t)kChunkBlockTokens * kPartialStats, it.nks_eff,
-                it.row0 + it.i0, it.i1 - it.i0);
+    for (int i = 0; i < it.i1 - it.i0; i += 4)
+        merge_block(a, a.ws_chunk_o + (first + i) * kPartialFloats, a.ws_chunk_ml + (first + i) * kPartialStats,
+                    (size_t)kChunkBlockTokens * kPartialFloats, (size_t)kChunkBlockTokens * kPartialStats, it.nks_eff,
+                    it.row0 + it.i0 + i, min(4, it.i1 - it.i0 - i));
 }
 
 // ----------------------------------------------------------------- append
