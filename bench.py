@@ -41,6 +41,36 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("mla_kernels.hip", "mla_api.cpp", "mla_kernels.h"):
+        with open(os.path.join(ROOT, "paper_2607_02043_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(config_idx):
+    """HBM bytes per mixed_step_attn call from the committed rocprofv3 counter
+    summary, or None if there is none for this workload or the kernels changed
+    since it was taken."""
+    path = os.path.join(ROOT, "profiles", "mixed_step_attn_config%d.md" % config_idx)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and line.startswith("    "):
+                k, v = line.strip().split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return int(fields["traffic_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
 # ---------------------------------------------------------------- work model
 def algorithmic_work(batch, out_bytes_per_elem=4):
     """Bytes and flops the method must move / compute for one layer.
@@ -187,6 +217,7 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+    roof["traffic"] = profiled_traffic(args.config) if not out_bf16 else None
     roof["kernel"] = "mixed_step_attn (attention_kernel + combine_kernel)"
     roof["per_launch_us"] = round(attn_us, 3)
     roof["algorithmic_bytes"] = work["attn_bytes"]
