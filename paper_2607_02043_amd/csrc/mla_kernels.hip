@@ -720,14 +720,19 @@ __device__ void decode_merge(const AttnArgs &a, int w, int *s_tmp, DecSeg *s_seg
 }
 
 // ------------------------------------------------------------- chunk path
-// Chunk rows: one workgroup per block of 4 query tokens (wave w scores token
-// i0 + w: 16 head rows) and a key range of ks_chunk keys.  32-key tiles
-// stream through a 4-slot DMA ring.  Per tile, each wave scores its token
-// against all 576 latent dims, updates that token's running max and sum, and
-// publishes the token's probabilities (bf16 hi + lo, already in MFMA
-// B-operand order) and rescale factor in LDS.  Then every wave accumulates
-// its 128-wide slice of the value dims for all 4 tokens, so each transposed
-// V^T operand read feeds 8 MFMAs.  V stays bf16; hi + lo keeps P to ~16 bits.
+// Chunk rows: one workgroup per block of 6 query tokens and a key range of
+// ks_chunk keys; 32-key tiles stream through a 3-slot DMA ring.
+//  * Scores.  Waves 2p and 2p+1 hold the queries of tokens 3p .. 3p+2, wave 2p
+//    over latent dims 0..287 and wave 2p+1 over dims 288..575, so every K
+//    operand read from LDS feeds three MFMAs per key block.  The pair then
+//    swaps partial scores through LDS: wave 2p finishes tokens 3p and 3p+1,
+//    wave 2p+1 token 3p+2.
+//  * Softmax.  The owning wave turns a token's scores into probabilities
+//    against a fixed reference max (no rescaling; see the passes below) and
+//    publishes them in LDS (fp16, already in MFMA B-operand order).
+//  * P*V.  Every wave accumulates its 128-wide slice of the value dims for all
+//    6 tokens: each transposed V^T operand read is converted to fp16 once and
+//    feeds 6 MFMAs.  fp16 holds every bf16 value in [2^-14, 65504] exactly.
 __device__ __forceinline__ void score_bases(int key, int g, int base[2]) {
     // chunk 4 st + g of `key` sits at base[st & 1] + 128 (st >> 1): the xor
     // swizzle only touches the chunk index's low 3 bits
@@ -735,38 +740,81 @@ __device__ __forceinline__ void score_bases(int key, int g, int base[2]) {
     for (int e = 0; e < 2; ++e) base[e] = (key * kChunksPerRow + ((4 * e + g) ^ (key & 7))) * 16;
 }
 
-// Scores of one 32-key tile for one token: s[kt][i] = key 16 kt + 4 g + i, head l%16.
-__device__ __forceinline__ void score32(const char *tile, const u32x4 *qreg, int lane, f32x4 s[2]) {
+constexpr int kPairTokens = kChunkBlockTokens / 2;  // 3 tokens per wave pair
+
+// Partial scores of one 32-key tile over k-steps 9 HALF .. 9 HALF + 8 (288
+// latent dims) for the wave's 3 tokens: s[j][kt][i] = key 16 kt + 4 g + i,
+// head l%16, local token j.  K operands are read two steps ahead.
+template <int HALF>
+__device__ __forceinline__ void score_half(const char *tile, const u32x4 (&qreg)[kPairTokens][9], int lane,
+                                           f32x4 (&s)[kPairTokens][2]) {
     const int g = lane >> 4;
     int b0[2], b1[2];
     score_bases(lane & 15, g, b0);
     score_bases(16 + (lane & 15), g, b1);
-    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    constexpr int G = 6;
 #pragma unroll
-    for (int grp = 0; grp < 18 / G; ++grp) {
-        u32x4 a0[G], a1[G];
+    for (int j = 0; j < kPairTokens; ++j) s[j][0] = s[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    u32x4 a0[3], a1[3];
 #pragma unroll
-        for (int j = 0; j < G; ++j) {
-            const int st = grp * G + j;
-            a0[j] = *reinterpret_cast<const u32x4 *>(tile + b0[st & 1] + 128 * (st >> 1));
-            a1[j] = *reinterpret_cast<const u32x4 *>(tile + b1[st & 1] + 128 * (st >> 1));
-        }
-#pragma unroll
-        for (int j = 0; j < G; ++j) {
-            acc0 = mfma_bf16(a0[j], qreg[grp * G + j], acc0);
-            acc1 = mfma_bf16(a1[j], qreg[grp * G + j], acc1);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * G, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * G, 0);
+    for (int st = 0; st < 2; ++st) {
+        const int gs = 9 * HALF + st;
+        a0[st] = *reinterpret_cast<const u32x4 *>(tile + b0[gs & 1] + 128 * (gs >> 1));
+        a1[st] = *reinterpret_cast<const u32x4 *>(tile + b1[gs & 1] + 128 * (gs >> 1));
     }
-    s[0] = acc0;
-    s[1] = acc1;
+#pragma unroll
+    for (int st = 0; st < 9; ++st) {
+        if (st + 2 < 9) {  // operands two steps ahead
+            const int gs = 9 * HALF + st + 2;
+            a0[(st + 2) % 3] = *reinterpret_cast<const u32x4 *>(tile + b0[gs & 1] + 128 * (gs >> 1));
+            a1[(st + 2) % 3] = *reinterpret_cast<const u32x4 *>(tile + b1[gs & 1] + 128 * (gs >> 1));
+        }
+#pragma unroll
+        for (int j = 0; j < kPairTokens; ++j) {
+            s[j][0] = mfma_bf16(a0[st % 3], qreg[j][st], s[j][0]);
+            s[j][1] = mfma_bf16(a1[st % 3], qreg[j][st], s[j][1]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
-constexpr int kChunkRing = 4;
-constexpr int kPBytes = kChunkBlockTokens * 2 * 64 * 16;  // P hi / lo per token, per lane
-constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kPBytes + 2 * kChunkBlockTokens * kHeads * 4 + 16;
+// bf16 pairs -> fp16 pairs (exact for |v| in [2^-14, 65504]; larger values
+// clamp to +-65504, smaller ones round toward zero).
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+    const auto h = __builtin_amdgcn_cvt_pkrtz(__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u));
+    return __builtin_bit_cast(uint32_t, h);
+}
+
+__device__ __forceinline__ uint32_t f16x2_bits(float a, float b) {
+    typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+    const f16x2 v = {(_Float16)a, (_Float16)b};  // round to nearest even
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// V^T operand of 16 value dims x 32 keys (transposing reads of keys k and
+// k + 16, see tr_base) converted to fp16.
+__device__ __forceinline__ u32x4 load_vt_f16(const char *vb) {
+    const u32x2 lo = lds_read_tr16(vb);
+    const u32x2 hi = lds_read_tr16(vb + 16 * kRowBytes);
+    return u32x4{bf16x2_to_f16x2(lo[0]), bf16x2_to_f16x2(lo[1]), bf16x2_to_f16x2(hi[0]), bf16x2_to_f16x2(hi[1])};
+}
+
+constexpr int kChunkRing = 3;
+constexpr int kXBytes = 4 * 4 * 64 * 16;              // score swap: [wave][4][lane] f32x4
+constexpr int kPBytes = kChunkBlockTokens * 64 * 16;  // fp16 P: [token][lane] u32x4
+constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kXBytes + kPBytes + kChunkBlockTokens * kHeads * 4 + 16;
+// Largest exponent (log2 units) a probability may take against the reference
+// max: 2^15 stays inside fp16.
+constexpr float kMaxPExp = 15.f;
+
+// Passes of a chunk item.  The reference max of each (token, head) is fixed
+// for the whole key range, so the accumulators are never rescaled:
+//   kPassMain   reference = max of the first tile.  Each lane also tracks the
+//               max of every score it sees.  If a later score exceeds the
+//               reference by more than 2^15, the pass still runs to the end
+//               (an exit from the middle of the loop costs the accumulators
+//               their registers) and its products are discarded;
+//   kPassExact  then redoes the item against the exact max.
+enum { kPassMain = 0, kPassExact = 1 };
 
 __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages) {
     Located lc;
@@ -780,132 +828,180 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
-    const int tok = it.i0 + wv;     // the token this wave scores
-    const bool active = tok < it.i1;
-    const int lim = it.p + tok;     // last key it may see
+    const int pair = wv >> 1, half = wv & 1;
+    const int nt = it.i1 - it.i0;  // tokens of this block (1 .. 6)
     const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
-    __syncthreads();
     TRACE(2);
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
     const uint32_t ring = lds_addr(smem);
-    u32x4 *s_P = reinterpret_cast<u32x4 *>(smem + kChunkRing * kChunkTileBytes);  // [token][hi, lo][lane]
-    float *s_alpha = reinterpret_cast<float *>(smem + kChunkRing * kChunkTileBytes + kPBytes);  // [token][head]
-    float *s_l = s_alpha + kChunkBlockTokens * kHeads;                                          // [token][head]
-    int *s_flag = reinterpret_cast<int *>(s_l + kChunkBlockTokens * kHeads);                    // [token]
-    for (int t = 0; t < kChunkRing - 1 && t < ntiles; ++t)
-        issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + t * kChunkKeys, it.k1, ring + t * kChunkTileBytes, wv, lane);
-    u32x4 qreg[18];
-    load_query(a, it.row0 + min(tok, it.i1 - 1), lane, qreg);  // an idle wave re-reads a valid row
-    wait_vm_all();
+    f32x4 *s_X = reinterpret_cast<f32x4 *>(smem + kChunkRing * kChunkTileBytes);  // [wave][4][lane]
+    u32x4 *s_P = reinterpret_cast<u32x4 *>(smem + kChunkRing * kChunkTileBytes + kXBytes);  // [token][lane]
+    float *s_l = reinterpret_cast<float *>(smem + kChunkRing * kChunkTileBytes + kXBytes + kPBytes);  // [token][head]
+    int *s_abort = reinterpret_cast<int *>(s_l + kChunkBlockTokens * kHeads);
+
+    // Local token j of this wave is block token 3 pair + perm(j): wave 2p keeps
+    // local 0, 1 (tokens 3p, 3p+1) and hands over local 2; wave 2p+1 keeps
+    // local 0 (token 3p+2) and hands over local 1, 2 (tokens 3p, 3p+1).
+    const int n_own = 2 - half;
+    u32x4 qreg[kPairTokens][9];
+#pragma unroll
+    for (int j = 0; j < kPairTokens; ++j) {
+        const int tb = kPairTokens * pair + (half ? (j + 2) % 3 : j);
+        const int row = it.row0 + it.i0 + min(tb, nt - 1);  // an idle token re-reads a valid row
+        const uint16_t *qp = a.q + ((size_t)row * kHeads + h) * kDqk + 9 * half * 32 + g * 8;
+#pragma unroll
+        for (int st = 0; st < 9; ++st) qreg[j][st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
+    }
+
+    float m_ref[2], l_run[2];  // the tokens this wave owns, head l%16
+    int lim[2], own_tb[2];     // block token, last key it may see (-1: idle or not owned)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+        m_ref[jj] = kNegInf;
+        l_run[jj] = 0.f;
+        own_tb[jj] = kPairTokens * pair + (half ? 2 : jj);
+        lim[jj] = (jj < n_own && own_tb[jj] < nt) ? it.p + it.i0 + own_tb[jj] : -1;
+    }
+    // V^T reads: value dims wv*128 + 16 mt + 4 (l & 3) .. + 3 of keys tr_key and
+    // tr_key + 16.  Their 16-byte chunk is wv*16 + 8 (mt >> 2) + (2 (mt & 3) +
+    // ((l & 3) >> 1)); the xor swizzle touches only the low three bits, so four
+    // bases plus immediate offsets cover all mt.
+    const int tr_key = 4 * g + ((lane & 15) >> 2);
+    int tr_base[4];
+#pragma unroll
+    for (int m4 = 0; m4 < 4; ++m4)
+        tr_base[m4] = (tr_key * kChunksPerRow + wv * 16 + ((2 * m4 + ((lane & 3) >> 1)) ^ (tr_key & 7))) * 16 +
+                      (lane & 1) * 8;
+    const int partner = wv ^ 1;
 
     f32x4 acc[kChunkBlockTokens][8];  // [token][value-dim tile of this wave's 128-wide slice]
-#pragma unroll
-    for (int j = 0; j < kChunkBlockTokens; ++j)
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_ref = kNegInf, l_run = 0.f;  // this wave's token, head l%16
-    const int tr_key = 4 * g + ((lane & 15) >> 2);
-    const int tr_dv = wv * 128 + 4 * (lane & 3);
-
+    float m_lane[2] = {kNegInf, kNegInf};  // max of the scores this lane has seen
     TRACE(3);
-    for (int t = 0; t < ntiles; ++t) {
-        TRACE_TILE(t, 10);
-        wait_units_newer(min(kChunkRing - 2, ntiles - 1 - t));
-        __syncthreads();
-        if (t + kChunkRing - 1 < ntiles)
-            issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + (t + kChunkRing - 1) * kChunkKeys, it.k1,
-                                   ring + ((t + kChunkRing - 1) % kChunkRing) * kChunkTileBytes, wv, lane);
-        const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
-        const int kbase = it.k0 + t * kChunkKeys;
-        TRACE_TILE(t, 11);
-        if (active) {
-            f32x4 s[2];
-            score32(tile, qreg, lane, s);
+    for (int pass = kPassMain; pass <= kPassExact; ++pass) {
+        const bool main_pass = pass == kPassMain;
+        if (tid == 0) *s_abort = 0;
+        __syncthreads();  // page window and abort flag ready; the ring is idle
+        for (int t = 0; t < kChunkRing - 1 && t < ntiles; ++t)
+            issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + t * kChunkKeys, it.k1, ring + t * kChunkTileBytes, wv,
+                                   lane);
+        if (main_pass) wait_vm_all();  // queries (and the first tiles) landed
+#pragma unroll
+        for (int j = 0; j < kChunkBlockTokens; ++j)
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) l_run[jj] = 0.f;
+        for (int t = 0; t < ntiles; ++t) {
+            TRACE_TILE(t, 10);
+            wait_units_newer(min(kChunkRing - 2, ntiles - 1 - t));
+            __syncthreads();
+            if (t + kChunkRing - 1 < ntiles)
+                issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + (t + kChunkRing - 1) * kChunkKeys, it.k1,
+                                       ring + ((t + kChunkRing - 1) % kChunkRing) * kChunkTileBytes, wv, lane);
+            const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
+            const int kbase = it.k0 + t * kChunkKeys;
+            TRACE_TILE(t, 11);
+            f32x4 s[kPairTokens][2];
+            if (half)
+                score_half<1>(tile, qreg, lane, s);
+            else
+                score_half<0>(tile, qreg, lane, s);
+            // hand over the partner's tokens: wave 2p writes local 2, wave 2p+1 local 1, 2
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int j = half ? 1 + (q >> 1) : 2;
+                if (q < 2 || half) s_X[(wv * 4 + q) * 64 + lane] = s[j][q & 1];
+            }
+            __syncthreads();
             TRACE_TILE(t, 12);
-            float x[8];
-            float mt = kNegInf;
+            bool bad = false;
+            // keys of this tile every owned token may see in full (no mask needed)
+            const int lim_min = n_own == 2 ? min(lim[0], lim[1]) : lim[0];
+            const bool full_tile = kbase + kChunkKeys <= it.k1 && kbase + kChunkKeys - 1 <= lim_min;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int key = kbase + 16 * (j >> 2) + 4 * g + (j & 3);
-                x[j] = (key < it.k1 && key <= lim) ? s[j >> 2][j & 3] * a.scale_log2 : kNegInf;
-                mt = fmaxf(mt, x[j]);
-            }
-            mt = wave_max16(mt);
-            // Lazy rescale: keep the reference max unless the tile max exceeds it
-            // by more than 2^8 (probabilities then stay <= 256).
-            const bool resc = __builtin_amdgcn_ballot_w64(mt > m_ref + 8.f) != 0;
-            float alpha = 1.f;
-            if (resc) {
-                const float m_new = fmaxf(m_ref, mt);
-                alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
-                m_ref = m_new;
-            }
-            uint32_t ph[4], pl[4];
-            float ps = 0.f;
+            for (int jj = 0; jj < 2; ++jj) {
+                if (jj >= n_own) break;
+                float raw[8];  // dot products of keys 16 kt + 4 g + i, index 4 kt + i
 #pragma unroll
-            for (int j = 0; j < 8; j += 2) {
-                const float p0 = (x[j] == kNegInf) ? 0.f : exp2f(x[j] - m_ref);
-                const float p1 = (x[j + 1] == kNegInf) ? 0.f : exp2f(x[j + 1] - m_ref);
-                ps += p0 + p1;
-                const uint32_t h0 = bf16_bits(p0), h1 = bf16_bits(p1);
-                ph[j >> 1] = h0 | (h1 << 16);
-                pl[j >> 1] = bf16_bits(p0 - bf16_bits_to_float(h0)) | (bf16_bits(p1 - bf16_bits_to_float(h1)) << 16);
+                for (int kt = 0; kt < 2; ++kt) {
+                    const f32x4 full = s[jj][kt] + s_X[(partner * 4 + 2 * jj + kt) * 64 + lane];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) raw[4 * kt + i] = full[i];
+                }
+                if (!full_tile) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int key = kbase + 16 * (e >> 2) + 4 * g + (e & 3);
+                        raw[e] = (key < it.k1 && key <= lim[jj]) ? raw[e] : kNegInf;
+                    }
+                }
+                float mr = raw[0];
+#pragma unroll
+                for (int e = 1; e < 8; ++e) mr = fmaxf(mr, raw[e]);
+                const float xm = mr * a.scale_log2;  // this lane's max, log2 units
+                if (main_pass) {
+                    m_lane[jj] = fmaxf(m_lane[jj], xm);
+                    if (t == 0) m_ref[jj] = wave_max16(xm);
+                    bad |= xm - m_ref[jj] > kMaxPExp;  // also true for a first visible key after tile 0
+                }
+                // the scaled score is rounded before the max is subtracted, so the
+                // max key gets p = 1 exactly; masked scores give p = 0
+                const float mref = m_ref[jj] == kNegInf ? 0.f : m_ref[jj];
+                uint32_t pk[4];
+                float ps = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+#pragma clang fp contract(off)
+                    const float p0 = __builtin_amdgcn_exp2f(raw[e] * a.scale_log2 - mref);
+                    const float p1 = __builtin_amdgcn_exp2f(raw[e + 1] * a.scale_log2 - mref);
+                    ps += p0 + p1;
+                    pk[e >> 1] = f16x2_bits(p0, p1);
+                }
+                l_run[jj] += ps;
+                s_P[own_tb[jj] * 64 + lane] = u32x4{pk[0], pk[1], pk[2], pk[3]};
             }
-            l_run = l_run * alpha + ps;
-            s_P[(wv * 2 + 0) * 64 + lane] = u32x4{ph[0], ph[1], ph[2], ph[3]};
-            s_P[(wv * 2 + 1) * 64 + lane] = u32x4{pl[0], pl[1], pl[2], pl[3]};
-            if (g == 0) s_alpha[wv * kHeads + h] = alpha;
-            if (lane == 0) s_flag[wv] = resc ? 1 : 0;
-        } else {  // idle wave: a zero token keeps the shared products finite
-            s_P[(wv * 2 + 0) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-            s_P[(wv * 2 + 1) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-            if (lane == 0) s_flag[wv] = 0;
+            if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
+            __syncthreads();
+            TRACE_TILE(t, 13);
+            u32x4 bp[kChunkBlockTokens];
+#pragma unroll
+            for (int j = 0; j < kChunkBlockTokens; ++j) bp[j] = s_P[j * 64 + lane];
+            u32x4 av[2];
+            av[0] = load_vt_f16(tile + tr_base[0]);
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                if (mt + 1 < 8)  // next operand read and converted under this block's MFMAs
+                    av[(mt + 1) & 1] = load_vt_f16(tile + tr_base[(mt + 1) & 3] + 128 * ((mt + 1) >> 2));
+#pragma unroll
+                for (int j = 0; j < kChunkBlockTokens; ++j) acc[j][mt] = mfma_f16(av[mt & 1], bp[j], acc[j][mt]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            TRACE_TILE(t, 14);
         }
-        __syncthreads();
-        TRACE_TILE(t, 13);
+        // every wave has passed the last tile's barrier, so the flag is final
+        if (!main_pass || __builtin_amdgcn_readfirstlane(*s_abort) == 0) break;
+        wait_dma_all();
 #pragma unroll
-        for (int j = 0; j < kChunkBlockTokens; ++j) {
-            if (s_flag[j] != 0) {
-                const float al = s_alpha[j * kHeads + h];
-#pragma unroll
-                for (int mt = 0; mt < 8; ++mt) acc[j][mt] = acc[j][mt] * al;
-            }
-        }
-        u32x4 bh[kChunkBlockTokens], bl[kChunkBlockTokens];
-#pragma unroll
-        for (int j = 0; j < kChunkBlockTokens; ++j) {
-            bh[j] = s_P[(j * 2 + 0) * 64 + lane];
-            bl[j] = s_P[(j * 2 + 1) * 64 + lane];
-        }
-#pragma unroll
-        for (int mt = 0; mt < 8; ++mt) {
-            const int dv = tr_dv + mt * 16;
-            const int byte = ((dv >> 2) & 1) * 8;
-            const u32x2 lo = lds_read_tr16(tile + tile_off(tr_key, dv >> 3) + byte);
-            const u32x2 hi = lds_read_tr16(tile + tile_off(tr_key + 16, dv >> 3) + byte);
-            const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
-#pragma unroll
-            for (int j = 0; j < kChunkBlockTokens; ++j) {
-                acc[j][mt] = mfma_bf16(av, bh[j], acc[j][mt]);
-                acc[j][mt] = mfma_bf16(av, bl[j], acc[j][mt]);
-            }
-        }
-        TRACE_TILE(t, 14);
+        for (int jj = 0; jj < 2; ++jj) m_ref[jj] = wave_max16(m_lane[jj]);  // the exact max
+        __syncthreads();  // all waves read the flag before it is cleared
     }
 
     TRACE(4);
     // running sums of all tokens, then each wave stores its value-dim slice
-    const float l_tot = wave_sum16(l_run);
-    if (g == 0) s_l[wv * kHeads + h] = l_tot;
+    float l_tot[2];
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+        l_tot[jj] = wave_sum16(l_run[jj]);
+        if (jj < n_own && g == 0) s_l[own_tb[jj] * kHeads + h] = l_tot[jj];
+    }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kChunkBlockTokens; ++j) {
-        const int tj = it.i0 + j;
-        if (tj >= it.i1) break;
-        const int row = it.row0 + tj;
+        if (j >= nt) break;
+        const int row = it.row0 + it.i0 + j;
         if (it.nks_eff == 1) {
             const float inv = 1.f / s_l[j * kHeads + h];
 #pragma unroll
@@ -917,14 +1013,17 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
             for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(po + wv * 128 + mt * 16 + 4 * g) = acc[j][mt];
         }
     }
-    if (active && g == 0) {
-        const int row = it.row0 + tok;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+        const int tb = own_tb[jj];
+        if (jj >= n_own || tb >= nt || g != 0) continue;
+        const int row = it.row0 + it.i0 + tb;
         if (it.nks_eff == 1) {
-            if (a.lse) a.lse[(size_t)row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
+            if (a.lse) a.lse[(size_t)row * kHeads + h] = (m_ref[jj] + log2f(l_tot[jj])) * kLn2;
         } else {
-            const size_t prow = (size_t)item * kChunkBlockTokens + wv;
-            a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref;
-            a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l_tot;
+            const size_t prow = (size_t)item * kChunkBlockTokens + tb;
+            a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref[jj];
+            a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l_tot[jj];
         }
     }
     TRACE(5);

@@ -60,6 +60,33 @@ def test_many_requests():
     _compare_all_rows(wl, wl.layer(0))
 
 
+def _plant_spike(b, li, key_pos_req, req, token_row, scale=8.0):
+    """Overwrite the latent of key `key_pos_req` of request `req` with
+    scale * sign(q[token_row][head 0]): its score then exceeds every earlier
+    score of that row by far more than 2^15 in log2 units."""
+    q0 = W.bf16_bits_to_f32(li.q.reshape(-1, W.NUM_HEADS, W.D_QK)[token_row, 0])
+    spike = W.f32_to_bf16_bits(np.where(q0 >= 0, scale, -scale).astype(np.float32))
+    p, c = int(b.prefix_lens[req]), int(b.q_lens[req])
+    if key_pos_req < p:  # cached: write it into the pool through the block table
+        pg = int(b.block_table[req][key_pos_req // b.page_size])
+        li.pool[pg, key_pos_req % b.page_size] = spike
+    else:  # appended this step
+        row0 = int(np.concatenate([[0], np.cumsum(b.q_lens)])[req])
+        li.new_latents.reshape(-1, W.D_QK)[row0 + key_pos_req - p] = spike
+
+
+def test_chunk_late_score_spike():
+    """Chunk rows whose later keys outscore the first tile by more than the
+    fp16 probability range take the exact-max pass."""
+    wl = W.custom([100, 5, 0], [40, 1, 70], page_size=16, seed=11, name="score_spike")
+    b, li = wl.batch, wl.layer(0)
+    _plant_spike(b, li, 90, 0, token_row=30)   # cached key, request 0
+    _plant_spike(b, li, 125, 0, token_row=35)  # appended key, request 0
+    _plant_spike(b, li, 40, 2, token_row=41 + 60)  # appended key of the prefix-0 chunk
+    log("[gpu] chunk rows with late score spikes")
+    _compare_all_rows(wl, li)
+
+
 @pytest.mark.parametrize("idx", [1, 2])
 def test_config_all_rows(idx):
     wl = W.config(idx)
