@@ -278,6 +278,33 @@ __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages
         lds_dma16(src[i], __builtin_amdgcn_readfirstlane(lds_tile + (i * 4 + wv) * 1024));
 }
 
+// DMA of a 32-key tile that lies inside one page: a uniform source base (the
+// tile's first key) in SGPRs plus per-lane offsets fixed for all tiles.
+// Round i of wave wv fills LDS chunk u = 256 i + 64 wv + lane of the tile,
+// which holds source chunk (u % 72) ^ (key & 7) of key u / 72.
+constexpr int kTileDma = kKeysPerTile * kRowBytes / (kThreads * 16);  // 9 rounds per tile
+// Offsets (< 2^16) packed two per register: round i in the half i & 1 of word i / 2.
+__device__ __forceinline__ void tile_dma_offsets(int wv, int lane, uint32_t (&off)[(kTileDma + 1) / 2]) {
+#pragma unroll
+    for (int w = 0; w < (kTileDma + 1) / 2; ++w) off[w] = 0;
+#pragma unroll
+    for (int i = 0; i < kTileDma; ++i) {
+        const int u = (i * 4 + wv) * 64 + lane;
+        const int kk = u / kChunksPerRow;
+        const int c = (u - kk * kChunksPerRow) ^ (kk & 7);
+        off[i / 2] |= (uint32_t)(kk * kRowBytes + c * 16) << (16 * (i & 1));
+    }
+}
+
+__device__ __forceinline__ void lds_dma16_sbase(const void *sbase, uint32_t voff, uint32_t lds_base) {
+    asm volatile(
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, %1\n\t"
+        :
+        : "v"(voff), "s"(sbase), "{m0}"(lds_base)
+        : "memory");
+}
+
 // Scores of 16 keys (tile rows key_base .. key_base + 15) against one token's
 // query operand: lane l gets S[key_base + 4 (l/16) + i][head l%16], i = 0..3.
 // Reads are staged 6 steps at a time; two accumulation chains.
@@ -454,10 +481,24 @@ __device__ __forceinline__ void advance(Cursor &c, const DecSeg *s_seg) {
 }
 
 // DMA of one stream unit into a 36 KB ring slot.  A query block (16 heads x
-// 576 dims, 18 KB) is copied twice over so every unit takes 9 DMA rounds.
+// 576 dims, 18 KB) is copied twice over so every unit takes 9 DMA rounds.  A
+// full tile inside one page uses the uniform-base form (offsets `dma_off`).
 __device__ __forceinline__ void issue_unit(const AttnArgs &a, const DecSeg &sg, int t, const int *s_pages,
-                                           uint32_t slot, int wv, int lane) {
+                                           uint32_t slot, int wv, int lane,
+                                           const uint32_t (&dma_off)[(kTileDma + 1) / 2]) {
     constexpr int kDma = kDecTileBytes / (kThreads * 16);  // 9
+    const int kbase = t * kDecKeys;
+    if (t >= 0 && a.page_size >= kDecKeys && kbase + kDecKeys - 1 <= sg.p) {
+        const int page = s_pages[min(sg.pw + (kbase >> a.log2_page) - sg.lp0, kPageWindow - 1)];
+        const char *src = reinterpret_cast<const char *>(a.kv) +
+                          ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size + (kbase & (a.page_size - 1))) *
+                              kRowBytes;
+#pragma unroll
+        for (int i = 0; i < kDma; ++i)
+            lds_dma16_sbase(src, (dma_off[i / 2] >> (16 * (i & 1))) & 0xffffu,
+                            __builtin_amdgcn_readfirstlane(slot + (i * 4 + wv) * 1024));
+        return;
+    }
     const char *src[kDma];
     if (t < 0) {
         const char *qb = reinterpret_cast<const char *>(a.q + (size_t)sg.row * kHeads * kDqk);
@@ -468,7 +509,7 @@ __device__ __forceinline__ void issue_unit(const AttnArgs &a, const DecSeg &sg, 
         }
     } else {
         const char *kv = reinterpret_cast<const char *>(a.kv);
-        const int kbase = t * kDecKeys, klast = sg.p;
+        const int klast = sg.p;
 #pragma unroll
         for (int i = 0; i < kDma; ++i) {
             const int u = (i * 4 + wv) * 64 + lane;
@@ -530,11 +571,13 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
 
     const int n_units = nseg + (R1 - R0);
     TRACE_VAL(8, 1000000ull * 2 + n_units);
+    uint32_t dma_off[(kTileDma + 1) / 2];
+    tile_dma_offsets(wv, lane, dma_off);
     const uint32_t ring = lds_addr(smem);
     float *s_X = reinterpret_cast<float *>(smem + kDecRing * kDecTileBytes);
     Cursor prod{0, -1}, cons{0, -1};
     for (int u = 0; u < kDecRing - 1 && u < n_units; ++u) {
-        issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + u * kDecTileBytes, wv, lane);
+        issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + u * kDecTileBytes, wv, lane, dma_off);
         advance(prod, s_seg);
     }
 
@@ -555,7 +598,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
         __syncthreads();
         if (prod.j < nseg) {
             issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + ((u + kDecRing - 1) % kDecRing) * kDecTileBytes, wv,
-                       lane);
+                       lane, dma_off);
             advance(prod, s_seg);
         }
         const char *slot = smem + (u % kDecRing) * kDecTileBytes;
@@ -725,14 +768,16 @@ __device__ void decode_merge(const AttnArgs &a, int w, int *s_tmp, DecSeg *s_seg
 //  * Scores.  Waves 2p and 2p+1 hold the queries of tokens 3p .. 3p+2, wave 2p
 //    over latent dims 0..287 and wave 2p+1 over dims 288..575, so every K
 //    operand read from LDS feeds three MFMAs per key block.  The pair then
-//    swaps partial scores through LDS: wave 2p finishes tokens 3p and 3p+1,
-//    wave 2p+1 token 3p+2.
-//  * Softmax.  The owning wave turns a token's scores into probabilities
-//    against a fixed reference max (no rescaling; see the passes below) and
-//    publishes them in LDS (fp16, already in MFMA B-operand order).
+//    swaps partial scores through LDS so that wave 2p+h holds the full scores
+//    of keys 16h .. 16h+15 of the tile for its three tokens.
+//  * Softmax.  Probabilities against a fixed reference max (no rescaling; see
+//    the passes below), published in LDS as fp16 in MFMA B-operand order.
 //  * P*V.  Every wave accumulates its 128-wide slice of the value dims for all
 //    6 tokens: each transposed V^T operand read is converted to fp16 once and
 //    feeds 6 MFMAs.  fp16 holds every bf16 value in [2^-14, 65504] exactly.
+// The loop is software-pipelined: the softmax of tile t runs in the same
+// stretch of code as the P*V products of tile t - 1, so VALU work issues
+// while the matrix cores are busy; two barriers per tile.
 __device__ __forceinline__ void score_bases(int key, int g, int base[2]) {
     // chunk 4 st + g of `key` sits at base[st & 1] + 128 (st >> 1): the xor
     // swizzle only touches the chunk index's low 3 bits
@@ -743,11 +788,14 @@ __device__ __forceinline__ void score_bases(int key, int g, int base[2]) {
 constexpr int kPairTokens = kChunkBlockTokens / 2;  // 3 tokens per wave pair
 
 // Partial scores of one 32-key tile over k-steps 9 HALF .. 9 HALF + 8 (288
-// latent dims) for the wave's 3 tokens: s[j][kt][i] = key 16 kt + 4 g + i,
-// head l%16, local token j.  K operands are read two steps ahead.
+// latent dims) for the wave's 3 tokens, element i of key block kt = key
+// 16 kt + 4 g + i, head l%16.  keep[j] is key block HALF (this wave finishes
+// it), give[j] the other block (handed to the partner).  K operands are read
+// two steps ahead.
 template <int HALF>
 __device__ __forceinline__ void score_half(const char *tile, const u32x4 (&qreg)[kPairTokens][9], int lane,
-                                           f32x4 (&s)[kPairTokens][2]) {
+                                           f32x4 (&keep)[kPairTokens], f32x4 (&give)[kPairTokens]) {
+    f32x4 s[kPairTokens][2];
     const int g = lane >> 4;
     int b0[2], b1[2];
     score_bases(lane & 15, g, b0);
@@ -775,6 +823,11 @@ __device__ __forceinline__ void score_half(const char *tile, const u32x4 (&qreg)
         }
         __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int j = 0; j < kPairTokens; ++j) {
+        keep[j] = s[j][HALF];
+        give[j] = s[j][1 - HALF];
+    }
 }
 
 // bf16 pairs -> fp16 pairs (exact for |v| in [2^-14, 65504]; larger values
@@ -799,9 +852,10 @@ __device__ __forceinline__ u32x4 load_vt_f16(const char *vb) {
 }
 
 constexpr int kChunkRing = 3;
-constexpr int kXBytes = 4 * 4 * 64 * 16;              // score swap: [wave][4][lane] f32x4
-constexpr int kPBytes = kChunkBlockTokens * 64 * 16;  // fp16 P: [token][lane] u32x4
-constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kXBytes + kPBytes + kChunkBlockTokens * kHeads * 4 + 16;
+constexpr int kXBytes = 4 * kPairTokens * 64 * 16;         // score swap: [wave][token][lane] f32x4
+constexpr int kPBytes = 2 * kChunkBlockTokens * 64 * 16;  // fp16 P, two buffers: [buf][token][lane] u32x4
+constexpr int kHsBytes = 4 * kPairTokens * kHeads * 4;     // per-wave half maxima / sums: [wave][token][head]
+constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kXBytes + kPBytes + kHsBytes + 16;
 // Largest exponent (log2 units) a probability may take against the reference
 // max: 2^15 stays inside fp16.
 constexpr float kMaxPExp = 15.f;
@@ -828,7 +882,7 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
-    const int pair = wv >> 1, half = wv & 1;
+    const int pair = wv >> 1, half = wv & 1, partner = wv ^ 1;
     const int nt = it.i1 - it.i0;  // tokens of this block (1 .. 6)
     const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
@@ -837,33 +891,29 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
     const uint32_t ring = lds_addr(smem);
-    f32x4 *s_X = reinterpret_cast<f32x4 *>(smem + kChunkRing * kChunkTileBytes);  // [wave][4][lane]
-    u32x4 *s_P = reinterpret_cast<u32x4 *>(smem + kChunkRing * kChunkTileBytes + kXBytes);  // [token][lane]
-    float *s_l = reinterpret_cast<float *>(smem + kChunkRing * kChunkTileBytes + kXBytes + kPBytes);  // [token][head]
-    int *s_abort = reinterpret_cast<int *>(s_l + kChunkBlockTokens * kHeads);
+    char *const lds_x = smem + kChunkRing * kChunkTileBytes;
+    f32x4 *s_X = reinterpret_cast<f32x4 *>(lds_x);                                  // [wave][token][lane]
+    uint32_t *s_P = reinterpret_cast<uint32_t *>(lds_x + kXBytes);                  // [buf][token][lane][4]
+    float *s_hs = reinterpret_cast<float *>(lds_x + kXBytes + kPBytes);             // [wave][token][head]
+    int *s_abort = reinterpret_cast<int *>(lds_x + kXBytes + kPBytes + kHsBytes);
 
-    // Local token j of this wave is block token 3 pair + perm(j): wave 2p keeps
-    // local 0, 1 (tokens 3p, 3p+1) and hands over local 2; wave 2p+1 keeps
-    // local 0 (token 3p+2) and hands over local 1, 2 (tokens 3p, 3p+1).
-    const int n_own = 2 - half;
+    // queries of tokens 3 pair + j over this wave's half of the latent dims
     u32x4 qreg[kPairTokens][9];
 #pragma unroll
     for (int j = 0; j < kPairTokens; ++j) {
-        const int tb = kPairTokens * pair + (half ? (j + 2) % 3 : j);
-        const int row = it.row0 + it.i0 + min(tb, nt - 1);  // an idle token re-reads a valid row
+        const int row = it.row0 + it.i0 + min(kPairTokens * pair + j, nt - 1);  // an idle token re-reads a row
         const uint16_t *qp = a.q + ((size_t)row * kHeads + h) * kDqk + 9 * half * 32 + g * 8;
 #pragma unroll
         for (int st = 0; st < 9; ++st) qreg[j][st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
     }
-
-    float m_ref[2], l_run[2];  // the tokens this wave owns, head l%16
-    int lim[2], own_tb[2];     // block token, last key it may see (-1: idle or not owned)
+    // Key of score i (0..3) of this lane within a tile: 16 half + 4 g + i.
+    // A score counts if its key <= elim[j] (the token's causal limit, clipped
+    // to the item's key range; -1 for an idle token).
+    int elim[kPairTokens];
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-        m_ref[jj] = kNegInf;
-        l_run[jj] = 0.f;
-        own_tb[jj] = kPairTokens * pair + (half ? 2 : jj);
-        lim[jj] = (jj < n_own && own_tb[jj] < nt) ? it.p + it.i0 + own_tb[jj] : -1;
+    for (int j = 0; j < kPairTokens; ++j) {
+        const int tb = kPairTokens * pair + j;
+        elim[j] = tb < nt ? min(it.p + it.i0 + tb, it.k1 - 1) - (16 * half + 4 * g) : -1 - (it.k1 + 64);
     }
     // V^T reads: value dims wv*128 + 16 mt + 4 (l & 3) .. + 3 of keys tr_key and
     // tr_key + 16.  Their 16-byte chunk is wv*16 + 8 (mt >> 2) + (2 (mt & 3) +
@@ -875,135 +925,181 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     for (int m4 = 0; m4 < 4; ++m4)
         tr_base[m4] = (tr_key * kChunksPerRow + wv * 16 + ((2 * m4 + ((lane & 3) >> 1)) ^ (tr_key & 7))) * 16 +
                       (lane & 1) * 8;
-    const int partner = wv ^ 1;
 
+    uint32_t dma_off[(kTileDma + 1) / 2];
+    tile_dma_offsets(wv, lane, dma_off);
+    // DMA of tile t into its ring slot: a full tile inside one page takes the
+    // uniform-base form, any other tile (small pages, the last partial tile)
+    // the general one
+    auto issue = [&](int t) {
+        const int kbase = it.k0 + t * kChunkKeys;
+        const uint32_t dst = ring + (t % kChunkRing) * kChunkTileBytes;
+        if (a.page_size >= kChunkKeys && kbase + kChunkKeys <= it.k1) {
+            const int page = s_pages[min((kbase >> a.log2_page) - lp0, kPageWindow - 1)];
+            const char *src = reinterpret_cast<const char *>(a.kv) +
+                              ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size +
+                               (kbase & (a.page_size - 1))) * kRowBytes;
+#pragma unroll
+            for (int i = 0; i < kTileDma; ++i)
+                lds_dma16_sbase(src, (dma_off[i / 2] >> (16 * (i & 1))) & 0xffffu,
+                                __builtin_amdgcn_readfirstlane(dst + (i * 4 + wv) * 1024));
+        } else {
+            issue_tile<kChunkKeys>(a, s_pages, lp0, kbase, it.k1, dst, wv, lane);
+        }
+    };
+
+    float m_ref[kPairTokens], m_lane[kPairTokens], l_run[kPairTokens];
+#pragma unroll
+    for (int j = 0; j < kPairTokens; ++j) m_ref[j] = m_lane[j] = kNegInf;
     f32x4 acc[kChunkBlockTokens][8];  // [token][value-dim tile of this wave's 128-wide slice]
-    float m_lane[2] = {kNegInf, kNegInf};  // max of the scores this lane has seen
+    f32x4 keep[kPairTokens];
+    bool bad = false;
+
+    auto scores = [&](int t) {
+        const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
+        f32x4 give[kPairTokens];
+        if (half)
+            score_half<1>(tile, qreg, lane, keep, give);
+        else
+            score_half<0>(tile, qreg, lane, keep, give);
+        // hand the other key half over to the partner
+#pragma unroll
+        for (int j = 0; j < kPairTokens; ++j) s_X[(wv * kPairTokens + j) * 64 + lane] = give[j];
+    };
+    // full scores of this lane's 4 keys of token j (masked), raw dot products
+    auto tile_scores = [&](int t, int j, float raw[4]) {
+        const f32x4 f = keep[j] + s_X[(partner * kPairTokens + j) * 64 + lane];
+        const int rel = elim[j] - (it.k0 + t * kChunkKeys);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) raw[i] = i <= rel ? f[i] : kNegInf;
+    };
+    auto softmax = [&](int t, bool main_pass, int j) {
+        float raw[4];
+        tile_scores(t, j, raw);
+        const float xm = fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])) * a.scale_log2;
+        m_lane[j] = fmaxf(m_lane[j], xm);
+        // also true for a first visible key after the first tile
+        bad |= main_pass && xm - m_ref[j] > kMaxPExp;
+        // the scaled score is rounded before the max is subtracted, so the max
+        // key gets p = 1 exactly; masked scores give p = 0
+        const float mref = m_ref[j] == kNegInf ? 0.f : m_ref[j];
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma clang fp contract(off)
+            p[i] = __builtin_amdgcn_exp2f(raw[i] * a.scale_log2 - mref);
+        }
+        l_run[j] += (p[0] + p[1]) + (p[2] + p[3]);
+        const int tb = kPairTokens * pair + j;
+        *reinterpret_cast<u32x2 *>(s_P + (((t & 1) * kChunkBlockTokens + tb) * 64 + lane) * 4 + 2 * half) =
+            u32x2{f16x2_bits(p[0], p[1]), f16x2_bits(p[2], p[3])};
+    };
+    auto pv = [&](int t, bool with_softmax, bool main_pass) {  // P*V of tile t (and softmax of t + 1)
+        const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
+        u32x4 bp[kChunkBlockTokens];
+#pragma unroll
+        for (int j = 0; j < kChunkBlockTokens; ++j)
+            bp[j] = *reinterpret_cast<const u32x4 *>(s_P + (((t & 1) * kChunkBlockTokens + j) * 64 + lane) * 4);
+        u32x4 av[2];
+        av[0] = load_vt_f16(tile + tr_base[0]);
+#pragma unroll
+        for (int mt = 0; mt < 8; ++mt) {
+            if (mt + 1 < 8) av[(mt + 1) & 1] = load_vt_f16(tile + tr_base[(mt + 1) & 3] + 128 * ((mt + 1) >> 2));
+#pragma unroll
+            for (int j = 0; j < kChunkBlockTokens; ++j) acc[j][mt] = mfma_f16(av[mt & 1], bp[j], acc[j][mt]);
+            if (with_softmax && (mt & 1) && mt < 2 * kPairTokens) softmax(t + 1, main_pass, mt >> 1);
+        }
+    };
+
     TRACE(3);
     for (int pass = kPassMain; pass <= kPassExact; ++pass) {
         const bool main_pass = pass == kPassMain;
         if (tid == 0) *s_abort = 0;
         __syncthreads();  // page window and abort flag ready; the ring is idle
-        for (int t = 0; t < kChunkRing - 1 && t < ntiles; ++t)
-            issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + t * kChunkKeys, it.k1, ring + t * kChunkTileBytes, wv,
-                                   lane);
-        if (main_pass) wait_vm_all();  // queries (and the first tiles) landed
+        for (int t = 0; t < 2 && t < ntiles; ++t) issue(t);
+        wait_units_newer(min(1, ntiles - 1));  // queries and tile 0 landed
+        __syncthreads();
 #pragma unroll
         for (int j = 0; j < kChunkBlockTokens; ++j)
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) l_run[jj] = 0.f;
-        for (int t = 0; t < ntiles; ++t) {
-            TRACE_TILE(t, 10);
-            wait_units_newer(min(kChunkRing - 2, ntiles - 1 - t));
-            __syncthreads();
-            if (t + kChunkRing - 1 < ntiles)
-                issue_tile<kChunkKeys>(a, s_pages, lp0, it.k0 + (t + kChunkRing - 1) * kChunkKeys, it.k1,
-                                       ring + ((t + kChunkRing - 1) % kChunkRing) * kChunkTileBytes, wv, lane);
-            const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
-            const int kbase = it.k0 + t * kChunkKeys;
-            TRACE_TILE(t, 11);
-            f32x4 s[kPairTokens][2];
-            if (half)
-                score_half<1>(tile, qreg, lane, s);
-            else
-                score_half<0>(tile, qreg, lane, s);
-            // hand over the partner's tokens: wave 2p writes local 2, wave 2p+1 local 1, 2
+        for (int j = 0; j < kPairTokens; ++j) l_run[j] = 0.f;
+        bad = false;
+
+        // tile 0: scores, the reference max (both key halves), probabilities
+        TRACE_TILE(0, 11);
+        scores(0);
+        __syncthreads();
+        if (main_pass) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int j = half ? 1 + (q >> 1) : 2;
-                if (q < 2 || half) s_X[(wv * 4 + q) * 64 + lane] = s[j][q & 1];
+            for (int j = 0; j < kPairTokens; ++j) {
+                float raw[4];
+                tile_scores(0, j, raw);
+                const float hm = wave_max16(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])) * a.scale_log2);
+                if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = hm;
+                m_ref[j] = hm;
             }
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kPairTokens; ++j)
+                m_ref[j] = fmaxf(m_ref[j], s_hs[(partner * kPairTokens + j) * kHeads + h]);
+        }
+#pragma unroll
+        for (int j = 0; j < kPairTokens; ++j) softmax(0, main_pass, j);
+        if (ntiles > 1) wait_dma_all();  // tile 1
+        if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
+        __syncthreads();
+        if (2 < ntiles) issue(2);
+        // steady state: scores of tile t, then P*V of t - 1 with the softmax of t
+        for (int t = 1; t < ntiles; ++t) {
+            TRACE_TILE(t, 11);
+            scores(t);
             __syncthreads();
             TRACE_TILE(t, 12);
-            bool bad = false;
-            // keys of this tile every owned token may see in full (no mask needed)
-            const int lim_min = n_own == 2 ? min(lim[0], lim[1]) : lim[0];
-            const bool full_tile = kbase + kChunkKeys <= it.k1 && kbase + kChunkKeys - 1 <= lim_min;
-#pragma unroll
-            for (int jj = 0; jj < 2; ++jj) {
-                if (jj >= n_own) break;
-                float raw[8];  // dot products of keys 16 kt + 4 g + i, index 4 kt + i
-#pragma unroll
-                for (int kt = 0; kt < 2; ++kt) {
-                    const f32x4 full = s[jj][kt] + s_X[(partner * 4 + 2 * jj + kt) * 64 + lane];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) raw[4 * kt + i] = full[i];
-                }
-                if (!full_tile) {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int key = kbase + 16 * (e >> 2) + 4 * g + (e & 3);
-                        raw[e] = (key < it.k1 && key <= lim[jj]) ? raw[e] : kNegInf;
-                    }
-                }
-                float mr = raw[0];
-#pragma unroll
-                for (int e = 1; e < 8; ++e) mr = fmaxf(mr, raw[e]);
-                const float xm = mr * a.scale_log2;  // this lane's max, log2 units
-                if (main_pass) {
-                    m_lane[jj] = fmaxf(m_lane[jj], xm);
-                    if (t == 0) m_ref[jj] = wave_max16(xm);
-                    bad |= xm - m_ref[jj] > kMaxPExp;  // also true for a first visible key after tile 0
-                }
-                // the scaled score is rounded before the max is subtracted, so the
-                // max key gets p = 1 exactly; masked scores give p = 0
-                const float mref = m_ref[jj] == kNegInf ? 0.f : m_ref[jj];
-                uint32_t pk[4];
-                float ps = 0.f;
-#pragma unroll
-                for (int e = 0; e < 8; e += 2) {
-#pragma clang fp contract(off)
-                    const float p0 = __builtin_amdgcn_exp2f(raw[e] * a.scale_log2 - mref);
-                    const float p1 = __builtin_amdgcn_exp2f(raw[e + 1] * a.scale_log2 - mref);
-                    ps += p0 + p1;
-                    pk[e >> 1] = f16x2_bits(p0, p1);
-                }
-                l_run[jj] += ps;
-                s_P[own_tb[jj] * 64 + lane] = u32x4{pk[0], pk[1], pk[2], pk[3]};
-            }
+            pv(t - 1, true, main_pass);
+            TRACE_TILE(t, 15);
+            if (t + 1 < ntiles) wait_dma_all();  // tile t + 1
             if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
             __syncthreads();
             TRACE_TILE(t, 13);
-            u32x4 bp[kChunkBlockTokens];
-#pragma unroll
-            for (int j = 0; j < kChunkBlockTokens; ++j) bp[j] = s_P[j * 64 + lane];
-            u32x4 av[2];
-            av[0] = load_vt_f16(tile + tr_base[0]);
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                if (mt + 1 < 8)  // next operand read and converted under this block's MFMAs
-                    av[(mt + 1) & 1] = load_vt_f16(tile + tr_base[(mt + 1) & 3] + 128 * ((mt + 1) >> 2));
-#pragma unroll
-                for (int j = 0; j < kChunkBlockTokens; ++j) acc[j][mt] = mfma_f16(av[mt & 1], bp[j], acc[j][mt]);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            if (t + 2 < ntiles) issue(t + 2);
             TRACE_TILE(t, 14);
         }
-        // every wave has passed the last tile's barrier, so the flag is final
+        pv(ntiles - 1, false, main_pass);
+        // the last barrier passed after every wave's last flag write
         if (!main_pass || __builtin_amdgcn_readfirstlane(*s_abort) == 0) break;
-        wait_dma_all();
+        // abandoned: the exact max of both key halves, then the exact pass
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) m_ref[jj] = wave_max16(m_lane[jj]);  // the exact max
-        __syncthreads();  // all waves read the flag before it is cleared
+        for (int j = 0; j < kPairTokens; ++j) {
+            const float hm = wave_max16(m_lane[j]);
+            if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = hm;
+            m_ref[j] = hm;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kPairTokens; ++j) m_ref[j] = fmaxf(m_ref[j], s_hs[(partner * kPairTokens + j) * kHeads + h]);
+        __syncthreads();  // every wave read the flag and the maxima
     }
 
     TRACE(4);
-    // running sums of all tokens, then each wave stores its value-dim slice
-    float l_tot[2];
+    // per-head sums of each key half, then each wave stores its value-dim slice
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-        l_tot[jj] = wave_sum16(l_run[jj]);
-        if (jj < n_own && g == 0) s_l[own_tb[jj] * kHeads + h] = l_tot[jj];
+    for (int j = 0; j < kPairTokens; ++j) {
+        const float lh = wave_sum16(l_run[j]);
+        if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = lh;
     }
     __syncthreads();
+    auto row_sum = [&](int tb) {  // key half 0 + key half 1, in that order
+        const int w0 = 2 * (tb / kPairTokens), jj = tb % kPairTokens;
+        return s_hs[(w0 * kPairTokens + jj) * kHeads + h] + s_hs[((w0 + 1) * kPairTokens + jj) * kHeads + h];
+    };
 #pragma unroll
     for (int j = 0; j < kChunkBlockTokens; ++j) {
         if (j >= nt) break;
         const int row = it.row0 + it.i0 + j;
         if (it.nks_eff == 1) {
-            const float inv = 1.f / s_l[j * kHeads + h];
+            const float inv = 1.f / row_sum(j);
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) store_out4(a, row, h, wv * 128 + mt * 16 + 4 * g, acc[j][mt] * inv);
         } else {
@@ -1013,17 +1109,20 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
             for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(po + wv * 128 + mt * 16 + 4 * g) = acc[j][mt];
         }
     }
+    if (half == 0 && g == 0) {
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-        const int tb = own_tb[jj];
-        if (jj >= n_own || tb >= nt || g != 0) continue;
-        const int row = it.row0 + it.i0 + tb;
-        if (it.nks_eff == 1) {
-            if (a.lse) a.lse[(size_t)row * kHeads + h] = (m_ref[jj] + log2f(l_tot[jj])) * kLn2;
-        } else {
-            const size_t prow = (size_t)item * kChunkBlockTokens + tb;
-            a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref[jj];
-            a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l_tot[jj];
+        for (int j = 0; j < kPairTokens; ++j) {
+            const int tb = kPairTokens * pair + j;
+            if (tb >= nt) break;
+            const int row = it.row0 + it.i0 + tb;
+            const float l = row_sum(tb);
+            if (it.nks_eff == 1) {
+                if (a.lse) a.lse[(size_t)row * kHeads + h] = (m_ref[j] + log2f(l)) * kLn2;
+            } else {
+                const size_t prow = (size_t)item * kChunkBlockTokens + tb;
+                a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref[j];
+                a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l;
+            }
         }
     }
     TRACE(5);
