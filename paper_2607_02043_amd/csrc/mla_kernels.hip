@@ -930,12 +930,15 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     tile_dma_offsets(wv, lane, dma_off);
     // DMA of tile t into its ring slot: a full tile inside one page takes the
     // uniform-base form, any other tile (small pages, the last partial tile)
-    // the general one
-    auto issue = [&](int t) {
+    // the general one.  page_of(t) may be read well before the issue.
+    const bool in_page = a.page_size >= kChunkKeys;
+    auto page_of = [&](int t) {
+        return s_pages[min(((it.k0 + t * kChunkKeys) >> a.log2_page) - lp0, kPageWindow - 1)];
+    };
+    auto issue = [&](int t, int page) {
         const int kbase = it.k0 + t * kChunkKeys;
         const uint32_t dst = ring + (t % kChunkRing) * kChunkTileBytes;
-        if (a.page_size >= kChunkKeys && kbase + kChunkKeys <= it.k1) {
-            const int page = s_pages[min((kbase >> a.log2_page) - lp0, kPageWindow - 1)];
+        if (in_page && kbase + kChunkKeys <= it.k1) {
             const char *src = reinterpret_cast<const char *>(a.kv) +
                               ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size +
                                (kbase & (a.page_size - 1))) * kRowBytes;
@@ -1016,7 +1019,7 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         const bool main_pass = pass == kPassMain;
         if (tid == 0) *s_abort = 0;
         __syncthreads();  // page window and abort flag ready; the ring is idle
-        for (int t = 0; t < 2 && t < ntiles; ++t) issue(t);
+        for (int t = 0; t < 2 && t < ntiles; ++t) issue(t, page_of(t));
         wait_units_newer(min(1, ntiles - 1));  // queries and tile 0 landed
         __syncthreads();
 #pragma unroll
@@ -1050,10 +1053,11 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         if (ntiles > 1) wait_dma_all();  // tile 1
         if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
         __syncthreads();
-        if (2 < ntiles) issue(2);
+        if (2 < ntiles) issue(2, page_of(2));
         // steady state: scores of tile t, then P*V of t - 1 with the softmax of t
         for (int t = 1; t < ntiles; ++t) {
             TRACE_TILE(t, 11);
+            const int next_page = page_of(min(t + 2, ntiles - 1));  // consumed after the second barrier
             scores(t);
             __syncthreads();
             TRACE_TILE(t, 12);
@@ -1063,7 +1067,7 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
             if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
             __syncthreads();
             TRACE_TILE(t, 13);
-            if (t + 2 < ntiles) issue(t + 2);
+            if (t + 2 < ntiles) issue(t + 2, next_page);
             TRACE_TILE(t, 14);
         }
         pv(ntiles - 1, false, main_pass);
