@@ -188,7 +188,7 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
         nci += ceil_div_ll(c, BM) * ceil_div_ll(p + c, ks_chunk);
         if (p + c > ks_chunk) pl->chunk_split = true;
     }
-    if (nci > (1LL << 30)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
+    if (nci > (1LL << 27)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
     pl->ks_chunk = (int)ks_chunk;
     pl->n_chunk_items = (int)nci;
     // decode shares

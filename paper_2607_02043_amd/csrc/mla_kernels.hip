@@ -348,52 +348,58 @@ __device__ __forceinline__ void store_out4(const AttnArgs &a, int row, int head,
 }
 
 // ------------------------------------------------------------------ merge
-// Merge the key-split partials of nrows (<= 4) consecutive output rows (m_s,
-// l_s in log2 units, o_s unnormalised) in split order.  Partial row ii of
-// split s starts at po + s * stride_o + ii * kPartialFloats (stats likewise).
-// 256 threads: head = tid / 16, dims (tid % 16) * 32 .. +32, all rows at once.
-__device__ void merge_block(const AttnArgs &a, const float *po, const float *pml, size_t stride_o, size_t stride_ml,
-                            int nsplit, int row0, int nrows) {
+// Merge the key-split partials of one output row in split order.  Split s
+// holds an unnormalised output o_s (16 heads x 512 dims) with its max m_s
+// and sum l_s in log2 units; slot(s) gives pointers to both.  256 threads:
+// head tid / 16, dims (tid % 16) * 32 .. + 32.  The loads of up to four splits
+// go out together; the running result is rescaled whenever the max grows.
+struct SplitRef {
+    const float *o, *ml;
+};
+
+template <typename Slot>
+__device__ void merge_row(const AttnArgs &a, int row, int nsplit, Slot slot) {
     const int tid = threadIdx.x;
     const int hh = tid >> 4, d0 = (tid & 15) * 32;
-    float mmax[4], denom[4];
-    f32x4 o[4][8];
+    float M = kNegInf, den = 0.f;
+    f32x4 o[8];
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-        mmax[ii] = kNegInf;
-        denom[ii] = 0.f;
+    for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nsplit; s0 += 4) {
+        float ms[4], ls[4];
+        f32x4 v[4][8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) o[ii][k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    for (int sp = 0; sp < nsplit; ++sp)
+        for (int q = 0; q < 4; ++q) {
+            ms[q] = kNegInf;
+            ls[q] = 0.f;
+            if (s0 + q < nsplit) {
+                const SplitRef sr = slot(s0 + q);
+                ms[q] = sr.ml[hh * 2];
+                ls[q] = sr.ml[hh * 2 + 1];
+                const f32x4 *src = reinterpret_cast<const f32x4 *>(sr.o + hh * kDv + d0);
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii)
-            if (ii < nrows) mmax[ii] = fmaxf(mmax[ii], pml[sp * stride_ml + ii * kPartialStats + hh * 2]);
-    for (int sp = 0; sp < nsplit; ++sp) {
+                for (int k = 0; k < 8; ++k) v[q][k] = src[k];
+            } else {
 #pragma unroll
-        for (int ii = 0; ii < 4; ++ii) {
-            if (ii >= nrows) continue;
-            const float *ml = pml + sp * stride_ml + ii * kPartialStats + hh * 2;
-            const float ms = ml[0];
-            const float wt = (ms == kNegInf) ? 0.f : exp2f(ms - mmax[ii]);
-            denom[ii] += wt * ml[1];
-            const f32x4 *src = reinterpret_cast<const f32x4 *>(po + sp * stride_o + ii * kPartialFloats + hh * kDv + d0);
-            f32x4 vv[8];
+                for (int k = 0; k < 8; ++k) v[q][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+        }
 #pragma unroll
-            for (int k = 0; k < 8; ++k) vv[k] = src[k];
+        for (int q = 0; q < 4; ++q) {
+            if (ms[q] == kNegInf) continue;  // a split that saw no key of this row
+            const float m_new = fmaxf(M, ms[q]);
+            const float c_old = (M == kNegInf) ? 0.f : exp2f(M - m_new);
+            const float c_new = exp2f(ms[q] - m_new);
+            den = den * c_old + ls[q] * c_new;
 #pragma unroll
-            for (int k = 0; k < 8; ++k) o[ii][k] += wt * vv[k];
+            for (int k = 0; k < 8; ++k) o[k] = o[k] * c_old + v[q][k] * c_new;
+            M = m_new;
         }
     }
+    const float inv = 1.f / den;
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) {
-        if (ii >= nrows) continue;
-        const float inv = 1.f / denom[ii];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) store_out4(a, row0 + ii, hh, d0 + 4 * k, o[ii][k] * inv);
-        if (a.lse && (tid & 15) == 0)
-            a.lse[(size_t)(row0 + ii) * kHeads + hh] = (mmax[ii] + log2f(denom[ii])) * kLn2;
-    }
+    for (int k = 0; k < 8; ++k) store_out4(a, row, hh, d0 + 4 * k, o[k] * inv);
+    if (a.lse && (tid & 15) == 0) a.lse[(size_t)row * kHeads + hh] = (M + log2f(den)) * kLn2;
 }
 
 // ------------------------------------------------------------ decode path
@@ -734,32 +740,12 @@ __device__ void decode_merge(const AttnArgs &a, int w, int *s_tmp, DecSeg *s_seg
     if (sg.t0 == 0 || sg.t1 != nt) return;  // starts here, or continues past this share
     const int T = R0 - sg.t0;                // the request's first tile in the list
     const int w0 = T / S;
-    const int tid = threadIdx.x, hh = tid >> 4, d0 = (tid & 15) * 32;
-    float mmax = kNegInf;
-    for (int v = w0; v <= w; ++v) {
+    // slot 2 v holds workgroup v's first segment, 2 v + 1 its last one
+    merge_row(a, sg.row, w - w0 + 1, [&](int s) {
+        const int v = w0 + s;
         const size_t sl = 2 * (size_t)v + ((v == w0 && T != w0 * S) ? 1 : 0);
-        mmax = fmaxf(mmax, a.ws_dec_ml[(sl * kHeads + hh) * 2]);
-    }
-    float denom = 0.f;
-    f32x4 o[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int v = w0; v <= w; ++v) {
-        const size_t sl = 2 * (size_t)v + ((v == w0 && T != w0 * S) ? 1 : 0);
-        const float ms = a.ws_dec_ml[(sl * kHeads + hh) * 2];
-        const float wt = (ms == kNegInf) ? 0.f : exp2f(ms - mmax);
-        denom += wt * a.ws_dec_ml[(sl * kHeads + hh) * 2 + 1];
-        const f32x4 *src = reinterpret_cast<const f32x4 *>(a.ws_dec_o + (sl * kHeads + hh) * kDv + d0);
-        f32x4 vv[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) vv[k] = src[k];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) o[k] += wt * vv[k];
-    }
-    const float inv = 1.f / denom;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) store_out4(a, sg.row, hh, d0 + 4 * k, o[k] * inv);
-    if (a.lse && (tid & 15) == 0) a.lse[(size_t)sg.row * kHeads + hh] = (mmax + log2f(denom)) * kLn2;
+        return SplitRef{a.ws_dec_o + sl * kHeads * kDv, a.ws_dec_ml + sl * kHeads * 2};
+    });
 }
 
 // ------------------------------------------------------------- chunk path
@@ -1158,7 +1144,7 @@ __global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
 
 // Split merges, after the attention kernel (the kernel boundary makes every
 // partial visible): first one workgroup per decode workgroup, then one per
-// chunk item (the item with key split 0 merges its row block).
+// (chunk item, block row).
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     __shared__ int s_tmp[12];
     __shared__ DecSeg s_seg[kMaxSeg];
@@ -1167,16 +1153,19 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
         decode_merge(a, b, s_tmp, s_seg);
         return;
     }
+    // one workgroup per (chunk item, row of its block): the item with key split
+    // 0 merges that row over the block's splits
+    const int item = (b - a.n_dec_wg) / kChunkBlockTokens, j = (b - a.n_dec_wg) % kChunkBlockTokens;
     Located lc;
-    if (!locate_item(b - a.n_dec_wg, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
     const ChunkItem it = decode_chunk_item(a, lc);
-    if (it.ks != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr) return;
+    if (it.ks != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr || j >= it.i1 - it.i0) return;
     if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;
-    const size_t first = (size_t)(b - a.n_dec_wg) * kChunkBlockTokens;
-    for (int i = 0; i < it.i1 - it.i0; i += 4)
-        merge_block(a, a.ws_chunk_o + (first + i) * kPartialFloats, a.ws_chunk_ml + (first + i) * kPartialStats,
-                    (size_t)kChunkBlockTokens * kPartialFloats, (size_t)kChunkBlockTokens * kPartialStats, it.nks_eff,
-                    it.row0 + it.i0 + i, min(4, it.i1 - it.i0 - i));
+    // split ks of this block is item + ks
+    merge_row(a, it.row0 + it.i0 + j, it.nks_eff, [&](int ks) {
+        const size_t prow = (size_t)(item + ks) * kChunkBlockTokens + j;
+        return SplitRef{a.ws_chunk_o + prow * kPartialFloats, a.ws_chunk_ml + prow * kPartialStats};
+    });
 }
 
 // ----------------------------------------------------------------- append
@@ -1279,7 +1268,9 @@ hipError_t launch_attention(const AttnArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_combine(const AttnArgs &a, hipStream_t s) {
-    const int grid = a.n_dec_wg + a.n_chunk_items;
+    const long long grid_ll = (long long)a.n_dec_wg + (long long)a.n_chunk_items * kChunkBlockTokens;
+    if (grid_ll > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    const int grid = (int)grid_ll;
     if (grid == 0) return hipSuccess;
     hipLaunchKernelGGL(combine_kernel, dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
