@@ -51,10 +51,10 @@ def kernel_source_hash():
 
 
 def profiled_traffic(config_idx):
-    """HBM bytes per mixed_step_attn call from the committed rocprofv3 counter
+    """HBM bytes per mixed_step call from the committed rocprofv3 counter
     summary, or None if there is none for this workload or the kernels changed
     since it was taken."""
-    path = os.path.join(ROOT, "profiles", "mixed_step_attn_config%d.md" % config_idx)
+    path = os.path.join(ROOT, "profiles", "mixed_step_config%d.md" % config_idx)
     if not os.path.exists(path):
         return None
     fields = {}
@@ -105,6 +105,8 @@ def main():
     ap.add_argument("--out-dtype", choices=["f32", "bf16"], default="f32")
     ap.add_argument("--no-rotate", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--two-call", action="store_true",
+                    help="time append_latent_kv + mixed_step_attn instead of the fused mixed_step")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -162,10 +164,14 @@ def main():
 
     def step(k, ev=None):
         for j, d in enumerate(rotations[k % n_rot]):
-            mla.append_latent_kv(db, d["new"], d["pool"], stream)
+            if args.two_call:
+                mla.append_latent_kv(db, d["new"], d["pool"], stream)
             if ev is not None:
                 ev[j][0].record(stream)
-            mla.mixed_step_attn(db, d["q"], d["pool"], scale, d["out"], d["lse"], ws, stream)
+            if args.two_call:
+                mla.mixed_step_attn(db, d["q"], d["pool"], scale, d["out"], d["lse"], ws, stream)
+            else:
+                mla.mixed_step(db, d["q"], d["new"], d["pool"], scale, d["out"], d["lse"], ws, stream)
             if ev is not None:
                 ev[j][1].record(stream)
 
@@ -205,7 +211,9 @@ def main():
     log(f"[bench] step {us_per_step:.2f} us; attention call mean {attn_us:.2f} us (p10 {attn_us_p10:.2f}, "
         f"p50 {attn_us_p50:.2f}, p90 {attn_us_p90:.2f})")
 
-    attn_gbs = work["attn_bytes"] / (attn_us * 1e-6) / 1e9
+    # the timed call: the fused step (append + attention), or the attention call alone
+    call_bytes = work["attn_bytes"] if args.two_call else work["step_bytes"]
+    attn_gbs = call_bytes / (attn_us * 1e-6) / 1e9
     attn_tflops = work["flops"] / (attn_us * 1e-6) / 1e12
     step_bytes = work["step_bytes"] * L
     step_flops = work["flops"] * L
@@ -217,10 +225,11 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
-    roof["traffic"] = profiled_traffic(args.config) if not out_bf16 else None
-    roof["kernel"] = "mixed_step_attn (attention_kernel + combine_kernel)"
+    roof["traffic"] = profiled_traffic(args.config) if not (out_bf16 or args.two_call) else None
+    roof["kernel"] = ("mixed_step_attn (attention_kernel + combine_kernel)" if args.two_call
+                      else "mixed_step (attention_kernel with the fused append + combine_kernel)")
     roof["per_launch_us"] = round(attn_us, 3)
-    roof["algorithmic_bytes"] = work["attn_bytes"]
+    roof["algorithmic_bytes"] = call_bytes
     roof["algorithmic_flops"] = work["flops"]
 
     result = {
@@ -238,7 +247,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "layers": L, "page_size": b.page_size, "requests": b.num_reqs,
                    "rows": work["rows"], "decode_rows": wl.num_decode, "chunks": [list(x) for x in wl.chunks],
-                   "out_dtype": args.out_dtype, "rotating_sets": n_rot, "parallelism": "single GPU"},
+                   "out_dtype": args.out_dtype, "rotating_sets": n_rot, "parallelism": "single GPU",
+                   "entry": "append_latent_kv + mixed_step_attn" if args.two_call else "mixed_step"},
         "step": {"ideal_us": round(ideal_us, 3), "roofline_frac": round(ideal_us / us_per_step, 4),
                  "bound": bound, "TB_per_s": round(step_bytes / (us_per_step * 1e-6) / 1e12, 3),
                  "TFLOP_per_s": round(step_flops / (us_per_step * 1e-6) / 1e12, 2),

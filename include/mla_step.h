@@ -25,7 +25,7 @@
  *       out[row][h][e] = sum_j softmax(s)_j * k_j[e]  (e < 512),
  *       lse[row][h] = log sum_j exp(s_j)  (natural log).
  *   Attention reads the appended latents from the cache: call append first,
- *   on the same stream.
+ *   on the same stream, or call mixed_step, which does both in one launch.
  *
  * Conventions
  *   - bf16 values travel as uint16_t bit patterns.  All pointers are plain
@@ -58,7 +58,7 @@
 extern "C" {
 #endif
 
-#define MLA_ABI_VERSION 1
+#define MLA_ABI_VERSION 2
 #define MLA_NUM_HEADS 16
 #define MLA_D_QK 576 /* latent width: 512 compressed + 64 rope dims */
 #define MLA_D_V 512  /* value width: the first 512 latent dims */
@@ -126,6 +126,22 @@ int append_latent_kv(const mla_batch *batch, const uint16_t *new_latents, uint16
 int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *kv_cache,
                     float softmax_scale, void *out, int32_t out_dtype, float *lse,
                     void *workspace, size_t workspace_bytes, void *stream);
+
+/* The whole step: append_latent_kv followed by mixed_step_attn, in one
+ * launch (plus the split merge when the batch needs one).  Results (out, lse
+ * and the cache) are bit-identical to the two calls.  The step's new keys are
+ * read from new_latents while they are written into the cache, so no
+ * workgroup waits for the append.
+ *   new_latents  DEVICE bf16 [T][576], row order of the batch.
+ *   kv_cache     DEVICE bf16 [num_pages][P][576]: holds the cached prefixes on
+ *                entry; on return also the T new latents (only their slots
+ *                change).
+ *   other arguments as for mixed_step_attn.
+ * Errors: as mixed_step_attn, and MLA_ERR_INVALID_ARG for a NULL new_latents
+ * with T > 0. */
+int mixed_step(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
+               float softmax_scale, void *out, int32_t out_dtype, float *lse, void *workspace,
+               size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -25,7 +25,7 @@ MLA_OUT_BF16 = 1
 NUM_HEADS, D_QK, D_V = 16, 576, 512
 
 EXPORTED = ("mla_abi_version", "mla_last_error", "mixed_step_workspace_bytes", "append_latent_kv",
-            "mixed_step_attn")
+            "mixed_step_attn", "mixed_step")
 
 
 class MlaError(RuntimeError):
@@ -69,6 +69,10 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_size_t, ctypes.c_void_p]
         L.mixed_step_attn.restype = ctypes.c_int
+        L.mixed_step.argtypes = [ctypes.POINTER(mla_batch), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_float, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_size_t, ctypes.c_void_p]
+        L.mixed_step.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -142,19 +146,31 @@ def append_latent_kv(batch: DeviceBatch, new_latents, kv_cache, stream=None) -> 
     _check(lib().append_latent_kv(ctypes.byref(batch.c), _ptr(new_latents), _ptr(kv_cache), _stream(stream)))
 
 
+def _out_mode(out) -> int:
+    import torch
+    if out.dtype == torch.float32:
+        return MLA_OUT_F32
+    if out.dtype in (torch.bfloat16, torch.uint16, torch.int16):
+        return MLA_OUT_BF16
+    raise TypeError("out must be float32 or bfloat16")
+
+
 def mixed_step_attn(batch: DeviceBatch, q, kv_cache, softmax_scale: float, out, lse=None, workspace=None,
                     stream=None) -> None:
     """q: [T][16][576] bf16 bits; out: [T][16][512] float32 or bf16 (dtype picks the mode)."""
-    import torch
-    if out.dtype == torch.float32:
-        mode = MLA_OUT_F32
-    elif out.dtype in (torch.bfloat16, torch.uint16, torch.int16):
-        mode = MLA_OUT_BF16
-    else:
-        raise TypeError("out must be float32 or bfloat16")
+    mode = _out_mode(out)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().mixed_step_attn(ctypes.byref(batch.c), _ptr(q), _ptr(kv_cache), float(softmax_scale), _ptr(out),
                                  mode, _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def mixed_step(batch: DeviceBatch, q, new_latents, kv_cache, softmax_scale: float, out, lse=None, workspace=None,
+               stream=None) -> None:
+    """append_latent_kv + mixed_step_attn in one launch (bit-identical results)."""
+    mode = _out_mode(out)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().mixed_step(ctypes.byref(batch.c), _ptr(q), _ptr(new_latents), _ptr(kv_cache), float(softmax_scale),
+                            _ptr(out), mode, _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def workspace_for(batch: DeviceBatch, device="cuda"):

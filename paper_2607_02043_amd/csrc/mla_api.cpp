@@ -277,13 +277,20 @@ int append_latent_kv(const mla_batch *batch, const uint16_t *new_latents, uint16
     return MLA_OK;
 }
 
-int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *kv_cache, float softmax_scale,
-                    void *out, int32_t out_dtype, float *lse, void *workspace, size_t workspace_bytes,
-                    void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by mixed_step_attn (new_latents == NULL) and mixed_step (fused append).
+int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
+           float softmax_scale, void *out, int32_t out_dtype, float *lse, void *workspace, size_t workspace_bytes,
+           void *stream) {
     Shape sh;
     int st = check_batch(batch, &sh);
     if (st != MLA_OK || sh.R == 0) return st;
     if (!q || !kv_cache || !out) return fail(MLA_ERR_INVALID_ARG, "q / kv_cache / out is NULL");
+    if (reinterpret_cast<uintptr_t>(new_latents) & 15)
+        return fail(MLA_ERR_INVALID_ARG, "new_latents must be 16-byte aligned");
     if (out_dtype != MLA_OUT_F32 && out_dtype != MLA_OUT_BF16)
         return fail(MLA_ERR_INVALID_ARG, "out_dtype = %d is neither MLA_OUT_F32 nor MLA_OUT_BF16", out_dtype);
     if (!std::isfinite(softmax_scale) || softmax_scale <= 0.f)
@@ -301,6 +308,8 @@ int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *k
     mla::AttnArgs a;
     a.q = q;
     a.kv = kv_cache;
+    a.new_kv = new_latents;
+    a.kv_out = new_latents ? kv_cache : nullptr;
     a.cu_q = batch->cu_q_dev;
     a.prefix = batch->prefix_lens_dev;
     a.bt = batch->block_table_dev;
@@ -332,6 +341,28 @@ int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *k
         if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
     }
     return MLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *kv_cache, float softmax_scale,
+                    void *out, int32_t out_dtype, float *lse, void *workspace, size_t workspace_bytes,
+                    void *stream) {
+    return attend(batch, q, nullptr, const_cast<uint16_t *>(kv_cache), softmax_scale, out, out_dtype, lse, workspace,
+                  workspace_bytes, stream);
+}
+
+int mixed_step(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
+               float softmax_scale, void *out, int32_t out_dtype, float *lse, void *workspace,
+               size_t workspace_bytes, void *stream) {
+    if (batch && batch->num_reqs > 0 && !new_latents) {
+        g_err[0] = '\0';
+        return fail(MLA_ERR_INVALID_ARG, "new_latents is NULL");
+    }
+    return attend(batch, q, new_latents, kv_cache, softmax_scale, out, out_dtype, lse, workspace, workspace_bytes,
+                  stream);
 }
 
 }  // extern "C"

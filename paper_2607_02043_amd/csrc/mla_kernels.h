@@ -20,6 +20,10 @@ constexpr int kMaxDecSegments = 64;                         // requests one deco
 struct AttnArgs {
     const uint16_t *q;
     const uint16_t *kv;
+    // Fused append (both null otherwise): the step's new latents, read in place
+    // of their cache slots, and the cache they are written into.
+    const uint16_t *new_kv;
+    uint16_t *kv_out;
     const int32_t *cu_q;
     const int32_t *prefix;
     const int32_t *bt;

@@ -255,11 +255,14 @@ __device__ __forceinline__ void load_page_window(const AttnArgs &a, int r, int l
 // Issue the DMA of one tile of KEYS keys (kbase .. kbase + KEYS - 1, clamped
 // to the last valid key k1 - 1 so every byte read is a finite cached latent).
 // Instruction i of wave wv fills 1 KB segment i * 4 + wv of the tile.
+// With a fused append, keys p_new .. are the step's new latents: key k comes
+// from row new_row0 + k - p_new of a.new_kv instead of its cache slot.
 template <int KEYS>
 __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages, int lp0, int kbase, int k1,
-                                           uint32_t lds_tile, int wv, int lane) {
+                                           uint32_t lds_tile, int wv, int lane, int p_new, int new_row0) {
     constexpr int kDma = KEYS * kRowBytes / (kThreads * 16);
     const char *kv = reinterpret_cast<const char *>(a.kv);
+    const char *nkv = reinterpret_cast<const char *>(a.new_kv);
     const char *src[kDma];
 #pragma unroll
     for (int i = 0; i < kDma; ++i) {  // all page-id reads first, then the DMA burst
@@ -271,7 +274,8 @@ __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages
         key = key < k1 ? key : k1 - 1;
         const int page = s_pages[min((key >> a.log2_page) - lp0, kPageWindow - 1)];
         const size_t slot = (size_t)page * a.page_size + (key & (a.page_size - 1));
-        src[i] = kv + slot * kRowBytes + c * 16;
+        src[i] = (nkv != nullptr && key >= p_new) ? nkv + (size_t)(new_row0 + key - p_new) * kRowBytes + c * 16
+                                                  : kv + slot * kRowBytes + c * 16;
     }
 #pragma unroll
     for (int i = 0; i < kDma; ++i)
@@ -303,6 +307,23 @@ __device__ __forceinline__ void lds_dma16_sbase(const void *sbase, uint32_t voff
         :
         : "v"(voff), "s"(sbase), "{m0}"(lds_base)
         : "memory");
+}
+
+// Fused append: copy n new latents (rows row0 .. of a.new_kv, keys key0 .. of
+// request r) into their cache slots; the whole workgroup takes part.  Slots
+// with a page id outside the pool are skipped.
+__device__ __forceinline__ void append_rows(const AttnArgs &a, int r, int key0, int row0, int n) {
+    const int32_t *btr = a.bt + (size_t)r * a.max_pages;
+    for (int x = threadIdx.x; x < n * kChunksPerRow; x += kThreads) {
+        const int i = x / kChunksPerRow, c = x - i * kChunksPerRow;
+        const int key = key0 + i;
+        const int lp = key >> a.log2_page;
+        const int page = lp < a.max_pages ? btr[lp] : -1;
+        if ((unsigned)page >= (unsigned)a.num_pages) continue;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(a.new_kv + (size_t)(row0 + i) * kDqk + c * 8);
+        *reinterpret_cast<u32x4 *>(a.kv_out + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kDqk +
+                                   c * 8) = v;
+    }
 }
 
 // Scores of 16 keys (tile rows key_base .. key_base + 15) against one token's
@@ -494,7 +515,8 @@ __device__ __forceinline__ void issue_unit(const AttnArgs &a, const DecSeg &sg, 
                                            const uint32_t (&dma_off)[(kTileDma + 1) / 2]) {
     constexpr int kDma = kDecTileBytes / (kThreads * 16);  // 9
     const int kbase = t * kDecKeys;
-    if (t >= 0 && a.page_size >= kDecKeys && kbase + kDecKeys - 1 <= sg.p) {
+    const int last_cached = a.new_kv != nullptr ? sg.p - 1 : sg.p;  // key p is the new latent when fused
+    if (t >= 0 && a.page_size >= kDecKeys && kbase + kDecKeys - 1 <= last_cached) {
         const int page = s_pages[min(sg.pw + (kbase >> a.log2_page) - sg.lp0, kPageWindow - 1)];
         const char *src = reinterpret_cast<const char *>(a.kv) +
                           ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size + (kbase & (a.page_size - 1))) *
@@ -523,7 +545,9 @@ __device__ __forceinline__ void issue_unit(const AttnArgs &a, const DecSeg &sg, 
             const int c = (u - kk * kChunksPerRow) ^ (kk & 7);
             const int key = min(kbase + kk, klast);
             const int page = s_pages[min(sg.pw + (key >> a.log2_page) - sg.lp0, kPageWindow - 1)];
-            src[i] = kv + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kRowBytes + c * 16;
+            src[i] = (a.new_kv != nullptr && key == klast)
+                         ? reinterpret_cast<const char *>(a.new_kv) + (size_t)sg.row * kRowBytes + c * 16
+                         : kv + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kRowBytes + c * 16;
         }
     }
 #pragma unroll
@@ -570,6 +594,12 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
             const int lp = sg.lp0 + i;
             const int pg = lp < a.max_pages ? btr[lp] : 0;
             s_pages[sg.pw + i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
+        }
+    }
+    if (a.new_kv != nullptr) {  // fused append: the workgroup holding a request's last tile writes its latent
+        for (int j = 0; j < nseg; ++j) {
+            const DecSeg sg = s_seg[j];
+            if (sg.t1 == dec_tiles(sg.p, 1)) append_rows(a, sg.r, sg.p, sg.row, 1);
         }
     }
     __syncthreads();
@@ -873,6 +903,8 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
+    // fused append: split 0 of a block writes the block's own new latents
+    if (a.new_kv != nullptr && it.ks == 0) append_rows(a, r, it.p + it.i0, it.row0 + it.i0, it.i1 - it.i0);
     TRACE(2);
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
@@ -918,13 +950,15 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     // uniform-base form, any other tile (small pages, the last partial tile)
     // the general one.  page_of(t) may be read well before the issue.
     const bool in_page = a.page_size >= kChunkKeys;
+    // with a fused append, keys p .. come from the new latents (general path)
+    const int cached_end = a.new_kv != nullptr ? min(it.k1, it.p) : it.k1;
     auto page_of = [&](int t) {
         return s_pages[min(((it.k0 + t * kChunkKeys) >> a.log2_page) - lp0, kPageWindow - 1)];
     };
     auto issue = [&](int t, int page) {
         const int kbase = it.k0 + t * kChunkKeys;
         const uint32_t dst = ring + (t % kChunkRing) * kChunkTileBytes;
-        if (in_page && kbase + kChunkKeys <= it.k1) {
+        if (in_page && kbase + kChunkKeys <= cached_end) {
             const char *src = reinterpret_cast<const char *>(a.kv) +
                               ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size +
                                (kbase & (a.page_size - 1))) * kRowBytes;
@@ -933,7 +967,7 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
                 lds_dma16_sbase(src, (dma_off[i / 2] >> (16 * (i & 1))) & 0xffffu,
                                 __builtin_amdgcn_readfirstlane(dst + (i * 4 + wv) * 1024));
         } else {
-            issue_tile<kChunkKeys>(a, s_pages, lp0, kbase, it.k1, dst, wv, lane);
+            issue_tile<kChunkKeys>(a, s_pages, lp0, kbase, it.k1, dst, wv, lane, it.p, it.row0);
         }
     };
 

@@ -43,7 +43,10 @@ class GpuLayer:
         self.lse = torch.full((T, W.NUM_HEADS), float("nan"), dtype=torch.float32, device=device) if want_lse else None
         self.ws = mla.workspace_for(dbatch, device)
 
-    def run(self, scale=W.SOFTMAX_SCALE, append=True):
+    def run(self, scale=W.SOFTMAX_SCALE, append=True, fused=False):
+        if fused:  # append + attention in one launch
+            mla.mixed_step(self.dbatch, self.q, self.new, self.pool, scale, self.out, self.lse, self.ws)
+            return
         if append:
             mla.append_latent_kv(self.dbatch, self.new, self.pool)
         mla.mixed_step_attn(self.dbatch, self.q, self.pool, scale, self.out, self.lse, self.ws)
@@ -59,11 +62,11 @@ class GpuLayer:
         return from_dev_u16(self.pool)
 
 
-def run_layer(batch, li, out_bf16=False, scale=W.SOFTMAX_SCALE):
+def run_layer(batch, li, out_bf16=False, scale=W.SOFTMAX_SCALE, fused=False):
     import torch
     db = mla.DeviceBatch.from_batch(batch)
     g = GpuLayer(db, li, out_bf16=out_bf16)
-    g.run(scale)
+    g.run(scale, fused=fused)
     torch.cuda.synchronize()
     return g
 

@@ -26,7 +26,8 @@ def test_library_loads_and_exports_every_declared_symbol():
     assert set(declared) == set(mla.EXPORTED), declared
     for name in declared:
         assert hasattr(L, name), f"libmlastep.so does not export {name}"
-    assert L.mla_abi_version() == 1
+    version = int(re.search(r"#define\s+MLA_ABI_VERSION\s+(\d+)", open(HEADER).read()).group(1))
+    assert L.mla_abi_version() == version
 
 
 class _HostBatch:
@@ -51,6 +52,10 @@ def _append(b, new=FAKE, kv=FAKE):
 
 def _attn(b, scale=0.07, dtype=0, q=FAKE, kv=FAKE, out=FAKE, lse=None):
     return mla.lib().mixed_step_attn(ctypes.byref(b.c), q, kv, scale, out, dtype, lse, None, 0, None)
+
+
+def _step(b, scale=0.07, dtype=0, q=FAKE, new=FAKE, kv=FAKE, out=FAKE, lse=None):
+    return mla.lib().mixed_step(ctypes.byref(b.c), q, new, kv, scale, out, dtype, lse, None, 0, None)
 
 
 def _err():
@@ -99,6 +104,18 @@ def test_misaligned_pointers_are_rejected():
     assert _append(b, new=FAKE + 2) == mla.MLA_ERR_INVALID_ARG
     assert "aligned" in _err()
     assert _attn(b, q=FAKE + 8) == mla.MLA_ERR_INVALID_ARG
+    assert _step(b, new=FAKE + 4) == mla.MLA_ERR_INVALID_ARG
+    assert "aligned" in _err()
+
+
+def test_fused_step_checks_its_arguments():
+    b = _HostBatch([1], [3])
+    assert _step(b, new=None) == mla.MLA_ERR_INVALID_ARG
+    assert "new_latents" in _err()
+    assert _step(b, scale=0.0) == mla.MLA_ERR_INVALID_ARG
+    assert _step(b, dtype=3) == mla.MLA_ERR_INVALID_ARG
+    assert _step(_HostBatch([0], [3])) == mla.MLA_ERR_INVALID_ARG
+    assert _step(_HostBatch([], []), new=None) == mla.MLA_OK
 
 
 @pytest.mark.parametrize("scale", [0.0, -1.0, float("inf"), float("nan")])

@@ -87,6 +87,45 @@ def test_chunk_late_score_spike():
     _compare_all_rows(wl, li)
 
 
+def _fused_vs_two_calls(wl, li, what):
+    """mixed_step (fused append) against append + mixed_step_attn: identical
+    bits for out, lse and the whole pool; and the oracle's tolerance."""
+    b = wl.batch
+    g2 = run_layer(b, li)
+    g1 = run_layer(b, li, fused=True)
+    assert np.array_equal(g1.pool_np(), g2.pool_np()), f"{what}: fused append pool differs"
+    assert np.array_equal(g1.out.cpu().numpy(), g2.out.cpu().numpy()), f"{what}: fused output bits differ"
+    assert np.array_equal(g1.lse.cpu().numpy(), g2.lse.cpu().numpy()), f"{what}: fused lse bits differ"
+    pool_ref, out_ref, lse_ref = oracle.step(b, li, W.SOFTMAX_SCALE)
+    assert np.array_equal(g1.pool_np(), pool_ref), f"{what}: fused append differs from the oracle"
+    assert_close(g1.out_np(), out_ref, g1.lse_np(), lse_ref, what=what + " fused")
+
+
+@pytest.mark.parametrize("name", sorted(EDGE_CASES))
+def test_fused_step_edge_cases(name):
+    prefix, qlen, page = EDGE_CASES[name]
+    log(f"[gpu] fused step, edge case {name}")
+    wl = W.custom(prefix, qlen, page_size=page, seed=zlib.crc32(name.encode()) % 1000, name=name)
+    _fused_vs_two_calls(wl, wl.layer(0), name)
+
+
+@pytest.mark.parametrize("idx", [1, 2])
+def test_fused_step_configs(idx):
+    wl = W.config(idx)
+    log(f"[gpu] fused step, config {idx}")
+    _fused_vs_two_calls(wl, wl.layer(0), wl.name)
+
+
+def test_fused_step_score_spike():
+    wl = W.custom([100, 5, 0], [40, 1, 70], page_size=16, seed=11, name="score_spike")
+    b, li = wl.batch, wl.layer(0)
+    _plant_spike(b, li, 90, 0, token_row=30)
+    _plant_spike(b, li, 125, 0, token_row=35)
+    _plant_spike(b, li, 40, 2, token_row=41 + 60)
+    log("[gpu] fused step with late score spikes")
+    _fused_vs_two_calls(wl, li, "score_spike")
+
+
 @pytest.mark.parametrize("idx", [1, 2])
 def test_config_all_rows(idx):
     wl = W.config(idx)
