@@ -92,11 +92,14 @@ int mla_abi_version(void);
 /* Message of the last non-OK return on this thread ("" if none). */
 const char *mla_last_error(void);
 
-/* Device workspace (bytes) that mixed_step_attn needs for this batch, or 0 on
- * invalid arguments (then mla_last_error says why; a valid batch may also need
- * 0 bytes).  Depends only on the host arrays and the device's CU count.  The
- * workspace holds fp32 partial results of rows whose keys are split across
- * workgroups. */
+/* Device workspace (bytes) that mixed_step_attn / mixed_step need for this
+ * batch, or 0 on invalid arguments (then mla_last_error says why; an empty
+ * batch also needs 0 bytes).  Depends only on the host arrays and the
+ * device's CU count.  The first 256 bytes hold the work-queue counters of the
+ * attention launch: they must be zero when a workspace is first used (e.g.
+ * hipMemset once after allocating it), and every completed call leaves them
+ * zero again.  The rest holds fp32 partial results of rows whose keys are
+ * split across work items; its contents on entry are ignored. */
 size_t mixed_step_workspace_bytes(const mla_batch *batch);
 
 /* Scatter the step's new latents into the paged cache (the append above).
@@ -118,9 +121,9 @@ int append_latent_kv(const mla_batch *batch, const uint16_t *new_latents, uint16
  *                  nearest even (MLA_OUT_BF16).
  *   lse            DEVICE fp32 [T][16] natural-log sum of exp(s), or NULL.
  *   workspace      DEVICE scratch of at least mixed_step_workspace_bytes(batch)
- *                  bytes (may be NULL if that is 0); contents on entry are
- *                  ignored and on return undefined; calls that overlap in
- *                  time need distinct workspaces.
+ *                  bytes (may be NULL if that is 0), zeroed once before its
+ *                  first use (see mixed_step_workspace_bytes); calls that
+ *                  overlap in time need distinct workspaces.
  * Errors: MLA_ERR_INVALID_ARG, MLA_ERR_UNSUPPORTED, MLA_ERR_WORKSPACE,
  * MLA_ERR_HIP. */
 int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *kv_cache,

@@ -174,7 +174,9 @@ def mixed_step(batch: DeviceBatch, q, new_latents, kv_cache, softmax_scale: floa
 
 
 def workspace_for(batch: DeviceBatch, device="cuda"):
-    """A workspace tensor of the size mixed_step_attn needs for `batch` (None if 0)."""
+    """A zeroed workspace tensor of the size mixed_step_attn / mixed_step need
+    for `batch` (None if 0).  It may be reused for any batch that needs no more
+    bytes: every completed call leaves its counters zero."""
     import torch
     n = mixed_step_workspace_bytes(batch)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device) if n > 0 else None
+    return torch.zeros(n, dtype=torch.uint8, device=device) if n > 0 else None

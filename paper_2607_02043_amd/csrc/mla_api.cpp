@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <algorithm>
 #include <mutex>
@@ -104,24 +105,28 @@ int check_batch(const mla_batch *b, Shape *sh) {
 
 struct Plan {
     int ks_chunk = 0, n_chunk_items = 0;
-    int n_dec_wg = 0, dec_tiles_per_wg = 0, dec_total_tiles = 0;
+    int n_dec_units = 0, dec_unit_tiles = 0, dec_total_tiles = 0, grid = 0, merge_hsplit = 1;
     bool chunk_split = false, dec_split = false;
     size_t off_chunk_o = 0, off_chunk_ml = 0, off_dec_o = 0, off_dec_ml = 0, bytes = 0;
 };
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-// Rough per-CU costs used only to balance the two kinds of work (us).
-constexpr double kChunkTileUs = 3.2;      // 4 tokens x 32 keys on one CU
-constexpr double kCuStreamGBs = 50.0;     // one CU streaming alone
-constexpr double kChipStreamGBs = 6300.0; // all CUs streaming together
+// Per-CU costs (us, measured on MI355X) used only to size the work items.
+constexpr double kChunkTileUs = 2.55;  // one chunk tile: 6 tokens x 32 keys
+constexpr double kChunkItemUs = 13.0;  // chunk item: lookup, queries, ring fill; epilogue stores
+constexpr double kEmptyItemUs = 1.5;   // a chunk item past its block's causal limit
+constexpr double kDecTileUs = 2.1;     // one decode tile: 1 token x 32 keys
+constexpr double kDecUnitUs = 5.5;     // decode unit start-up
+constexpr double kMergeGBs = 4000.0;   // partial rows written and merged, whole chip
+constexpr int kCounterBytes = 256;     // work-queue counters at the start of the workspace
 
 struct DecReq {
     long long first_tile, tiles, p;
 };
 
-// Does a decode share of S tiles per workgroup respect the kernel's limits
-// (segments and page-window entries per workgroup)?
+// Does a decode unit of S tiles respect the kernel's limits (segments and
+// page-window entries per unit)?
 bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long S, int page_size) {
     size_t k = 0;
     for (long long R0 = 0; R0 < total; R0 += S) {
@@ -141,26 +146,60 @@ bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long 
     return true;
 }
 
+// Loads of the G workgroups after the chunk items, each item taken in queue
+// order by the first free workgroup.
+std::vector<double> simulate_chunks(const std::vector<double> &items, int G) {
+    std::vector<double> heap(G, 0.0);  // min-heap of workgroup finish times
+    auto cmp = [](double x, double y) { return x > y; };
+    for (double c : items) {
+        std::pop_heap(heap.begin(), heap.end(), cmp);
+        heap.back() += c;
+        std::push_heap(heap.begin(), heap.end(), cmp);
+    }
+    return heap;
+}
+
+// Finishing time when n equal units of cost u follow, each taken by the first
+// free workgroup: the last unit starts at the smallest t by which n units
+// have started, i.e. sum_i ceil((t - L_i) / u) >= n over loads L_i < t.
+double fill_units(const std::vector<double> &loads, long long n, double u) {
+    double mx = 0.0;
+    for (double L : loads) mx = std::max(mx, L);
+    if (n <= 0) return mx;
+    auto started = [&](double t) {
+        long long k = 0;
+        for (double L : loads)
+            if (L < t) k += (long long)std::ceil((t - L) / u - 1e-9);
+        return k;
+    };
+    double lo = 0.0, hi = mx + (double)n * u + u;
+    for (int it = 0; it < 24 && hi - lo > 0.01 * u; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        if (started(mid) >= n)
+            hi = mid;
+        else
+            lo = mid;
+    }
+    return std::max(mx, hi + u);
+}
+
 // Work layout of one call.
-//  * chunk requests -> items of (4 tokens) x (ks_chunk keys), longest rows
-//    first; key ranges are split only when the chunk is too small to give the
-//    chip enough items.
-//  * decode requests -> one list of 32-key tiles cut into equal shares for
-//    n_dec_wg persistent workgroups; n_dec_wg balances the decode stream
-//    against the chunk work that runs on the remaining compute units.
+//  * chunk requests -> items of (6 tokens) x (ks_chunk keys), largest blocks
+//    first; ks_chunk is picked by simulating the work queue for a few
+//    candidate splits, counting the cost of the partials a split leaves.
+//  * decode requests -> one list of 32-key tiles cut into units of
+//    dec_unit_tiles; with chunk work present the units are small so that
+//    they fill the tail of the queue.
 // The device recomputes the same mapping from the device copies of the lengths.
-int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
-    if (sh.R == 0) return MLA_OK;
-    int st = MLA_OK;
-    const int ncu = cu_count(&st);
-    if (st != MLA_OK) return st;
+int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
     const long long P = b->page_size;
     long long cap = ((long long)(mla::kPageWindow - 1) * P) / 64 * 64;  // keys per chunk item
     if (cap < 64) cap = 64;
     const int BM = mla::kChunkBlockTokens, KT = mla::kKeysPerTile;
 
     std::vector<DecReq> dec;
-    long long chunk_blocks = 0, chunk_block_keys = 0, dec_total = 0;
+    std::vector<std::pair<long long, long long>> chunks;  // (p, c) of each chunk request, queue order
+    long long dec_total = 0;
     for (int r = 0; r < sh.R; ++r) {
         const long long c = b->q_lens[r], p = b->prefix_lens[r];
         if (c == 1) {
@@ -168,59 +207,144 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
             dec.push_back(DecReq{dec_total, nt, p});
             dec_total += nt;
         } else {
-            const long long nrb = ceil_div_ll(c, BM);
-            chunk_blocks += nrb;
-            for (long long rb = 0; rb < nrb; ++rb) chunk_block_keys += p + std::min(c, (rb + 1) * BM);
+            chunks.emplace_back(p, c);
         }
     }
     if (dec_total > (1LL << 30)) return fail(MLA_ERR_INVALID_ARG, "too many decode keys in the step");
-    // chunk items
-    const long long target = 2LL * ncu;
-    long long ks_chunk = cap;
-    if (chunk_blocks > 0 && chunk_blocks < target) {
-        ks_chunk = std::max<long long>(128, ceil_div_ll(ceil_div_ll(chunk_block_keys, target), 64) * 64);
-        ks_chunk = std::min(ks_chunk, cap);
-    }
-    long long nci = 0;
-    for (int r = 0; r < sh.R; ++r) {
-        const long long c = b->q_lens[r], p = b->prefix_lens[r];
-        if (c == 1) continue;
-        nci += ceil_div_ll(c, BM) * ceil_div_ll(p + c, ks_chunk);
-        if (p + c > ks_chunk) pl->chunk_split = true;
-    }
-    if (nci > (1LL << 27)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
-    pl->ks_chunk = (int)ks_chunk;
-    pl->n_chunk_items = (int)nci;
-    // decode shares
+    const int G = std::max(1, ncu);
+    const double row_bytes = (double)mla::kPartialFloats * 4.0;
+
+    // Candidate decode unit sizes (tiles); each must respect the kernel's
+    // per-unit segment and page-window limits.
+    std::vector<long long> units;
     if (dec_total > 0) {
-        const double chunk_us = (double)ceil_div_ll(chunk_block_keys, KT) * kChunkTileUs;
-        long long best_g = std::min<long long>(ncu, dec_total);
-        if (chunk_us > 0.0 && ncu > 1) {
-            double best = 1e300;
-            for (long long g = 1; g < ncu && g <= dec_total; ++g) {
-                const double bw = std::min(kCuStreamGBs, kChipStreamGBs / g);  // GB/s per CU
-                const double t_dec = (double)ceil_div_ll(dec_total, g) * (KT * mla::kRowBytes) / (bw * 1e3);
-                const double t_chunk = chunk_us / (double)(ncu - g);
-                const double t = std::max(t_dec, t_chunk);
+        const long long cands[] = {8, 16, 32, 64, ceil_div_ll(dec_total, 3LL * G), ceil_div_ll(dec_total, 2LL * G),
+                                   ceil_div_ll(dec_total, G)};
+        for (long long U : cands) {
+            U = std::max(1LL, std::min(U, dec_total));
+            while (U > 1 && !dec_share_fits(dec, dec_total, U, (int)P)) U = std::max(1LL, U * 3 / 4);
+            if (!dec_share_fits(dec, dec_total, U, (int)P)) continue;
+            if (std::find(units.begin(), units.end(), U) == units.end()) units.push_back(U);
+        }
+        if (units.empty())
+            return fail(MLA_ERR_UNSUPPORTED, "decode work does not fit the per-unit segment / page limits");
+    }
+    // Finishing time of the decode units (equal cost u) poured onto the loads
+    // left by the chunk items, plus the merge of the requests they split.
+    auto with_decode = [&](const std::vector<double> &loads, long long U) {
+        const long long n = ceil_div_ll(dec_total, U);
+        const double u = kDecUnitUs + kDecTileUs * (double)U;
+        long long split_parts = 0;
+        for (const DecReq &d : dec) {
+            const long long parts = (d.first_tile + d.tiles - 1) / U - d.first_tile / U + 1;
+            if (parts > 1) split_parts += parts + 1;
+        }
+        return fill_units(loads, n, u) + (double)split_parts * row_bytes / (kMergeGBs * 1e3);
+    };
+
+    // Chunk key split (keys per item).  Items in device queue order: request
+    // by request, blocks largest first, ceil((p + c) / ks) key splits per
+    // block (a split past a block's causal limit is an empty item, still taken
+    // off the queue).
+    long long ks_best = cap, U_best = units.empty() ? 1 : units.back();
+    {
+        // first pass: each key split with a cheap estimate of the decode fill;
+        // second pass: the exact fill for the two best splits
+        struct Cand {
+            long long ks;
+            double merge_us, est;
+            std::vector<double> loads;
+        };
+        std::vector<Cand> cands;
+        std::vector<double> items;
+        for (long long ks = 64;; ks *= 2) {
+            const long long k = std::min(ks, cap);
+            items.clear();
+            long long split_rows = 0;
+            bool too_many = false;
+            for (const auto &pc : chunks) {
+                const long long p = pc.first, c = pc.second;
+                const long long nrb = ceil_div_ll(c, BM), nks = ceil_div_ll(p + c, k);
+                if ((long long)items.size() + nrb * nks > 16LL * G) {
+                    too_many = true;
+                    break;
+                }
+                for (long long rb = nrb - 1; rb >= 0; --rb) {
+                    const long long keys = p + std::min(c, (rb + 1) * BM);
+                    const long long ns = ceil_div_ll(keys, k);
+                    for (long long j = 0; j < nks; ++j)
+                        items.push_back(j < ns ? kChunkItemUs + kChunkTileUs * (double)ceil_div_ll(
+                                                                                 std::min(k, keys - j * k), KT)
+                                               : kEmptyItemUs);
+                    // partial rows are written, read back and the final row written by the merge
+                    if (ns > 1) split_rows += (ns + 1) * std::min<long long>(BM, c - rb * BM);
+                }
+            }
+            if (!too_many) {
+                Cand cd{k, (double)split_rows * row_bytes / (kMergeGBs * 1e3), 0.0, simulate_chunks(items, G)};
+                double mx = 0.0, sum = 0.0;
+                for (double L : cd.loads) {
+                    mx = std::max(mx, L);
+                    sum += L;
+                }
+                double est = mx;
+                if (dec_total > 0) {
+                    est = 1e300;
+                    for (long long U : units) {
+                        const double u = kDecUnitUs + kDecTileUs * (double)U;
+                        est = std::min(est, std::max(mx, (sum + (double)ceil_div_ll(dec_total, U) * u) / G));
+                    }
+                }
+                cd.est = est + cd.merge_us;
+                cands.push_back(std::move(cd));
+            }
+            if (k >= cap || chunks.empty()) break;
+        }
+        std::sort(cands.begin(), cands.end(), [](const Cand &x, const Cand &y) { return x.est < y.est; });
+        double best = 1e300;
+        for (size_t i = 0; i < cands.size() && i < 2; ++i) {
+            const Cand &cd = cands[i];
+            if (dec_total == 0) {
+                if (cd.est < best) {
+                    best = cd.est;
+                    ks_best = cd.ks;
+                }
+                continue;
+            }
+            for (long long U : units) {
+                const double t = with_decode(cd.loads, U) + cd.merge_us;
                 if (t < best) {
                     best = t;
-                    best_g = g;
+                    ks_best = cd.ks;
+                    U_best = U;
                 }
             }
         }
-        long long S = ceil_div_ll(dec_total, best_g);
-        while (S > 1 && !dec_share_fits(dec, dec_total, S, (int)P)) S = std::max(1LL, S * 3 / 4);
-        if (!dec_share_fits(dec, dec_total, S, (int)P))
-            return fail(MLA_ERR_UNSUPPORTED, "decode work does not fit the per-workgroup segment / page limits");
-        const long long G = ceil_div_ll(dec_total, S);
-        if (G > (1LL << 24)) return fail(MLA_ERR_INVALID_ARG, "too many decode workgroups");
-        pl->n_dec_wg = (int)G;
-        pl->dec_tiles_per_wg = (int)S;
-        pl->dec_total_tiles = (int)dec_total;
-        for (const DecReq &d : dec)
-            if (d.first_tile / S != (d.first_tile + d.tiles - 1) / S) pl->dec_split = true;
     }
-    size_t off = 0;
+    const long long U = dec_total > 0 ? U_best : 0;
+    const long long n_units = dec_total > 0 ? ceil_div_ll(dec_total, U) : 0;
+    long long nci = 0;
+    for (const auto &pc : chunks) {
+        const long long p = pc.first, c = pc.second;
+        nci += ceil_div_ll(c, BM) * ceil_div_ll(p + c, ks_best);
+        if (p + c > ks_best) pl->chunk_split = true;
+    }
+    if (nci > (1LL << 27)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
+    pl->ks_chunk = (int)ks_best;
+    pl->n_chunk_items = (int)nci;
+    pl->n_dec_units = (int)n_units;
+    pl->dec_unit_tiles = (int)U;
+    pl->dec_total_tiles = (int)dec_total;
+    pl->grid = (int)std::min<long long>(G, nci + n_units);
+    long long max_parts = 1;
+    for (const DecReq &d : dec) {
+        const long long parts = (d.first_tile + d.tiles - 1) / U - d.first_tile / U + 1;
+        if (parts > 1) pl->dec_split = true;
+        max_parts = std::max(max_parts, parts);
+    }
+    // a row merged from many parts is spread over several workgroups
+    pl->merge_hsplit = max_parts > 16 ? 8 : max_parts > 4 ? 4 : 1;
+    size_t off = kCounterBytes;
     if (pl->chunk_split) {
         pl->off_chunk_o = off;
         off = align256(off + (size_t)nci * BM * mla::kPartialFloats * sizeof(float));
@@ -229,11 +353,55 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
     }
     if (pl->dec_split) {
         pl->off_dec_o = off;
-        off = align256(off + (size_t)2 * pl->n_dec_wg * mla::kPartialFloats * sizeof(float));
+        off = align256(off + (size_t)2 * n_units * mla::kPartialFloats * sizeof(float));
         pl->off_dec_ml = off;
-        off = align256(off + (size_t)2 * pl->n_dec_wg * mla::kPartialStats * sizeof(float));
+        off = align256(off + (size_t)2 * n_units * mla::kPartialStats * sizeof(float));
     }
     pl->bytes = off;
+    static const bool log_plan = std::getenv("MLA_PLAN_LOG") != nullptr;
+    if (log_plan)
+        std::fprintf(stderr,
+                     "[mla plan] R=%d CUs=%d chunk items=%d (ks=%d keys, split=%d) decode units=%d x %d tiles "
+                     "(total %lld, split=%d, merge x%d) grid=%d workspace=%zu B\n",
+                     sh.R, ncu, pl->n_chunk_items, pl->ks_chunk, (int)pl->chunk_split, pl->n_dec_units,
+                     pl->dec_unit_tiles, dec_total, (int)pl->dec_split, pl->merge_hsplit, pl->grid, pl->bytes);
+    return MLA_OK;
+}
+
+// The plan depends only on the host lengths, the page size and the CU count;
+// the last one is kept per thread so a steady stream of identical steps
+// plans once.
+int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
+    *pl = Plan{};
+    if (sh.R == 0) return MLA_OK;
+    int st = MLA_OK;
+    const int ncu = cu_count(&st);
+    if (st != MLA_OK) return st;
+    thread_local std::vector<int32_t> key;
+    thread_local Plan cached;
+    thread_local bool have = false;
+    const size_t n = 4 + 2 * (size_t)sh.R;
+    bool same = have && key.size() == n && key[0] == b->page_size && key[1] == ncu && key[2] == sh.R &&
+                key[3] == b->max_pages_per_req;
+    if (same) {
+        same = std::memcmp(key.data() + 4, b->q_lens, sh.R * sizeof(int32_t)) == 0 &&
+               std::memcmp(key.data() + 4 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t)) == 0;
+    }
+    if (same) {
+        *pl = cached;
+        return MLA_OK;
+    }
+    st = make_plan_uncached(b, sh, ncu, pl);
+    if (st != MLA_OK) return st;
+    key.resize(n);
+    key[0] = b->page_size;
+    key[1] = ncu;
+    key[2] = sh.R;
+    key[3] = b->max_pages_per_req;
+    std::memcpy(key.data() + 4, b->q_lens, sh.R * sizeof(int32_t));
+    std::memcpy(key.data() + 4 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t));
+    cached = *pl;
+    have = true;
     return MLA_OK;
 }
 
@@ -320,6 +488,7 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
     a.ws_chunk_ml = pl.chunk_split ? reinterpret_cast<float *>(ws + pl.off_chunk_ml) : nullptr;
     a.ws_dec_o = pl.dec_split ? reinterpret_cast<float *>(ws + pl.off_dec_o) : nullptr;
     a.ws_dec_ml = pl.dec_split ? reinterpret_cast<float *>(ws + pl.off_dec_ml) : nullptr;
+    a.work = reinterpret_cast<int32_t *>(ws);
     a.num_reqs = sh.R;
     a.num_rows = sh.T;
     a.page_size = batch->page_size;
@@ -329,8 +498,10 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
     a.scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
     a.ks_chunk = pl.ks_chunk;
     a.n_chunk_items = pl.n_chunk_items;
-    a.n_dec_wg = pl.n_dec_wg;
-    a.dec_tiles_per_wg = pl.dec_tiles_per_wg;
+    a.n_dec_units = pl.n_dec_units;
+    a.dec_unit_tiles = pl.dec_unit_tiles;
+    a.grid = pl.grid;
+    a.merge_hsplit = pl.merge_hsplit;
     a.dec_total_tiles = pl.dec_total_tiles;
     a.out_bf16 = out_dtype == MLA_OUT_BF16 ? 1 : 0;
     const hipStream_t s = static_cast<hipStream_t>(stream);

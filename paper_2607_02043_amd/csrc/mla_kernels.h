@@ -31,8 +31,9 @@ struct AttnArgs {
     float *lse;
     float *ws_chunk_o;    // [n_chunk_items][block tokens][16][512]
     float *ws_chunk_ml;   // [n_chunk_items][block tokens][16][2]
-    float *ws_dec_o;      // [2 n_dec_wg][16][512]: first / last segment of each decode workgroup
-    float *ws_dec_ml;     // [2 n_dec_wg][16][2]
+    float *ws_dec_o;      // [2 n_dec_units][16][512]: first / last segment of each decode unit
+    float *ws_dec_ml;     // [2 n_dec_units][16][2]
+    int32_t *work;        // [2]: next work item, workgroups done; zero between calls
     int32_t num_reqs;
     int32_t num_rows;
     int32_t page_size;
@@ -41,10 +42,12 @@ struct AttnArgs {
     int32_t num_pages;
     float scale_log2;     // softmax scale * log2(e)
     int32_t ks_chunk;          // keys per chunk work item (a multiple of 64)
-    int32_t n_chunk_items;
-    int32_t n_dec_wg;          // persistent decode workgroups
-    int32_t dec_tiles_per_wg;  // 32-key decode tiles per workgroup share
+    int32_t n_chunk_items;     // work items 0 .. n_chunk_items - 1
+    int32_t n_dec_units;       // then the decode units: slices of the flattened decode tile list
+    int32_t dec_unit_tiles;    // 32-key decode tiles per unit
     int32_t dec_total_tiles;
+    int32_t grid;              // persistent workgroups of the attention launch
+    int32_t merge_hsplit;      // merge workgroups per split decode row (1, 4 or 8: heads split among them)
     int32_t out_bf16;
 };
 

@@ -50,23 +50,41 @@ constexpr float kNegInf = -INFINITY;
 // Optional per-workgroup timeline for profiling builds (-DMLA_TRACE): slot k
 // of workgroup b records the 100 MHz real-time counter at point k.
 #ifdef MLA_TRACE
+// Trace builds only: per work item, 16 stamps (slot = the item's queue index).
 __device__ unsigned long long g_trace[1 << 20];
-#define TRACE(k)                                                                        \
-    do {                                                                                \
-        if (threadIdx.x == 0 && blockIdx.x < (1 << 16))                                 \
-            g_trace[(size_t)blockIdx.x * 16 + (k)] = __builtin_amdgcn_s_memrealtime();  \
+__shared__ int s_trace_item;
+#define TRACE_ITEM(item)                                                                  \
+    do {                                                                                  \
+        if (threadIdx.x == 0) {                                                           \
+            s_trace_item = (item);                                                        \
+            unsigned xcc, hw;                                                             \
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));           \
+            asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));             \
+            if ((item) < (1 << 16)) {                                                     \
+                g_trace[(size_t)(item) * 16 + 0] = __builtin_amdgcn_s_memrealtime();      \
+                g_trace[(size_t)(item) * 16 + 9] = ((unsigned long long)xcc << 32) | hw;  \
+            }                                                                             \
+        }                                                                                 \
     } while (0)
-#define TRACE_VAL(k, v)                                                                 \
-    do {                                                                                \
-        if (threadIdx.x == 0 && blockIdx.x < (1 << 16)) g_trace[(size_t)blockIdx.x * 16 + (k)] = (v); \
+#define TRACE(k)                                                                          \
+    do {                                                                                  \
+        if (threadIdx.x == 0 && s_trace_item < (1 << 16))                                 \
+            g_trace[(size_t)s_trace_item * 16 + (k)] = __builtin_amdgcn_s_memrealtime();  \
+    } while (0)
+#define TRACE_VAL(k, v)                                                                   \
+    do {                                                                                  \
+        if (threadIdx.x == 0 && s_trace_item < (1 << 16)) g_trace[(size_t)s_trace_item * 16 + (k)] = (v); \
     } while (0)
 // shader-clock stamps inside the third tile of an item (slots 10..15)
-#define TRACE_TILE(t, k)                                                                 \
-    do {                                                                                 \
-        if ((t) == 2 && threadIdx.x == 0 && blockIdx.x < (1 << 16))                      \
-            g_trace[(size_t)blockIdx.x * 16 + (k)] = __builtin_amdgcn_s_memtime();       \
+#define TRACE_TILE(t, k)                                                                  \
+    do {                                                                                  \
+        if ((t) == 2 && threadIdx.x == 0 && s_trace_item < (1 << 16))                     \
+            g_trace[(size_t)s_trace_item * 16 + (k)] = __builtin_amdgcn_s_memtime();      \
     } while (0)
 #else
+#define TRACE_ITEM(item) \
+    do {                 \
+    } while (0)
 #define TRACE_TILE(t, k) \
     do {                 \
     } while (0)
@@ -77,6 +95,7 @@ __device__ unsigned long long g_trace[1 << 20];
     do {                \
     } while (0)
 #endif
+
 constexpr float kLn2 = 0.69314718055994530942f;
 
 // ---------------------------------------------------------------- helpers
@@ -378,19 +397,22 @@ struct SplitRef {
     const float *o, *ml;
 };
 
-template <typename Slot>
-__device__ void merge_row(const AttnArgs &a, int row, int nsplit, Slot slot) {
+template <int NH, typename Slot>
+__device__ void merge_heads(const AttnArgs &a, int row, int hh0, int nsplit, Slot slot) {
+    // NH heads per workgroup: head hh0 + tid / (256 / NH), DPT value dims per thread
+    constexpr int TPH = kThreads / NH, DPT = kDv / TPH, NV = DPT / 4;
+    constexpr int B = NH >= 16 ? 4 : 8;  // splits whose loads go out together
     const int tid = threadIdx.x;
-    const int hh = tid >> 4, d0 = (tid & 15) * 32;
+    const int hh = hh0 + tid / TPH, d0 = (tid % TPH) * DPT;
     float M = kNegInf, den = 0.f;
-    f32x4 o[8];
+    f32x4 o[NV];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < nsplit; s0 += 4) {
-        float ms[4], ls[4];
-        f32x4 v[4][8];
+    for (int k = 0; k < NV; ++k) o[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nsplit; s0 += B) {
+        float ms[B], ls[B];
+        f32x4 v[B][NV];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < B; ++q) {
             ms[q] = kNegInf;
             ls[q] = 0.f;
             if (s0 + q < nsplit) {
@@ -399,28 +421,33 @@ __device__ void merge_row(const AttnArgs &a, int row, int nsplit, Slot slot) {
                 ls[q] = sr.ml[hh * 2 + 1];
                 const f32x4 *src = reinterpret_cast<const f32x4 *>(sr.o + hh * kDv + d0);
 #pragma unroll
-                for (int k = 0; k < 8; ++k) v[q][k] = src[k];
+                for (int k = 0; k < NV; ++k) v[q][k] = src[k];
             } else {
 #pragma unroll
-                for (int k = 0; k < 8; ++k) v[q][k] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int k = 0; k < NV; ++k) v[q][k] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
         }
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < B; ++q) {
             if (ms[q] == kNegInf) continue;  // a split that saw no key of this row
             const float m_new = fmaxf(M, ms[q]);
             const float c_old = (M == kNegInf) ? 0.f : exp2f(M - m_new);
             const float c_new = exp2f(ms[q] - m_new);
             den = den * c_old + ls[q] * c_new;
 #pragma unroll
-            for (int k = 0; k < 8; ++k) o[k] = o[k] * c_old + v[q][k] * c_new;
+            for (int k = 0; k < NV; ++k) o[k] = o[k] * c_old + v[q][k] * c_new;
             M = m_new;
         }
     }
     const float inv = 1.f / den;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) store_out4(a, row, hh, d0 + 4 * k, o[k] * inv);
-    if (a.lse && (tid & 15) == 0) a.lse[(size_t)row * kHeads + hh] = (M + log2f(den)) * kLn2;
+    for (int k = 0; k < NV; ++k) store_out4(a, row, hh, d0 + 4 * k, o[k] * inv);
+    if (a.lse && tid % TPH == 0) a.lse[(size_t)row * kHeads + hh] = (M + log2f(den)) * kLn2;
+}
+
+template <typename Slot>
+__device__ void merge_row(const AttnArgs &a, int row, int nsplit, Slot slot) {
+    merge_heads<kHeads>(a, row, 0, nsplit, slot);
 }
 
 // ------------------------------------------------------------ decode path
@@ -567,8 +594,8 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
-    const int R0 = w * a.dec_tiles_per_wg;
-    const int R1 = min(R0 + a.dec_tiles_per_wg, a.dec_total_tiles);
+    const int R0 = w * a.dec_unit_tiles;
+    const int R1 = min(R0 + a.dec_unit_tiles, a.dec_total_tiles);
     if (R0 >= R1) return;
     const int nseg = find_segments(a, R0, R1, s_seg, s_tmp);
     TRACE(1);
@@ -758,24 +785,42 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
     TRACE(4);
 }
 
-// Merge kernel side: workgroup w finishes the request (if any) that started in
-// an earlier workgroup's share and ends in its own.
-__device__ void decode_merge(const AttnArgs &a, int w, int *s_tmp, DecSeg *s_seg) {
-    const int S = a.dec_tiles_per_wg;
-    const int R0 = w * S, R1 = min(R0 + S, a.dec_total_tiles);
-    if (R0 >= R1 || a.ws_dec_o == nullptr) return;
-    if (find_segments(a, R0, R1, s_seg, s_tmp) == 0) return;
-    const DecSeg sg = s_seg[0];
-    const int nt = dec_tiles(sg.p, 1);
-    if (sg.t0 == 0 || sg.t1 != nt) return;  // starts here, or continues past this share
-    const int T = R0 - sg.t0;                // the request's first tile in the list
-    const int w0 = T / S;
-    // slot 2 v holds workgroup v's first segment, 2 v + 1 its last one
-    merge_row(a, sg.row, w - w0 + 1, [&](int s) {
+// Merge kernel side: workgroup (r, part) merges heads part * 16 / hsplit ..
+// of decode request r when its tiles span several decode units.  Unit v
+// keeps its first segment in slot 2 v and its last one in slot 2 v + 1.
+__device__ void decode_merge(const AttnArgs &a, int r, int part, int *s_tmp) {
+    if (a.ws_dec_o == nullptr || r >= a.num_reqs) return;
+    const int tid = threadIdx.x;
+    // T = decode tiles of the requests before r (one block-wide sum per 256 requests)
+    int T = 0;
+    for (int base = 0; base < r; base += kThreads) {
+        const int q = base + tid;
+        int nt = 0;
+        if (q < r) {
+            const int row0 = a.cu_q[q], p = a.prefix[q];
+            nt = (p >= 0 && row0 >= 0 && row0 < a.num_rows) ? dec_tiles(p, a.cu_q[q + 1] - row0) : 0;
+        }
+        int total;
+        block_scan_excl(nt, s_tmp, total);
+        T += total;
+    }
+    const int row = a.cu_q[r], p = a.prefix[r];
+    if (p < 0 || row < 0 || row >= a.num_rows || a.cu_q[r + 1] - row != 1) return;
+    const int S = a.dec_unit_tiles, nt = dec_tiles(p, 1);
+    const int w0 = T / S, w1 = (T + nt - 1) / S;
+    if (w0 == w1) return;  // one unit wrote the row itself
+    auto slot = [&](int s) {
         const int v = w0 + s;
         const size_t sl = 2 * (size_t)v + ((v == w0 && T != w0 * S) ? 1 : 0);
         return SplitRef{a.ws_dec_o + sl * kHeads * kDv, a.ws_dec_ml + sl * kHeads * 2};
-    });
+    };
+    const int n = w1 - w0 + 1;
+    if (a.merge_hsplit == 8)
+        merge_heads<2>(a, row, 2 * part, n, slot);
+    else if (a.merge_hsplit == 4)
+        merge_heads<4>(a, row, 4 * part, n, slot);
+    else
+        merge_heads<16>(a, row, 0, n, slot);
 }
 
 // ------------------------------------------------------------- chunk path
@@ -902,9 +947,17 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int nt = it.i1 - it.i0;  // tokens of this block (1 .. 6)
     const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
+    // queries of tokens 3 pair + j over this wave's half of the latent dims
+    // (issued first: their latency overlaps the page-window load)
+    u32x4 qreg[kPairTokens][9];
+#pragma unroll
+    for (int j = 0; j < kPairTokens; ++j) {
+        const int row = it.row0 + it.i0 + min(kPairTokens * pair + j, nt - 1);  // an idle token re-reads a row
+        const uint16_t *qp = a.q + ((size_t)row * kHeads + h) * kDqk + 9 * half * 32 + g * 8;
+#pragma unroll
+        for (int st = 0; st < 9; ++st) qreg[j][st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
+    }
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
-    // fused append: split 0 of a block writes the block's own new latents
-    if (a.new_kv != nullptr && it.ks == 0) append_rows(a, r, it.p + it.i0, it.row0 + it.i0, it.i1 - it.i0);
     TRACE(2);
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
@@ -915,15 +968,6 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     float *s_hs = reinterpret_cast<float *>(lds_x + kXBytes + kPBytes);             // [wave][token][head]
     int *s_abort = reinterpret_cast<int *>(lds_x + kXBytes + kPBytes + kHsBytes);
 
-    // queries of tokens 3 pair + j over this wave's half of the latent dims
-    u32x4 qreg[kPairTokens][9];
-#pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) {
-        const int row = it.row0 + it.i0 + min(kPairTokens * pair + j, nt - 1);  // an idle token re-reads a row
-        const uint16_t *qp = a.q + ((size_t)row * kHeads + h) * kDqk + 9 * half * 32 + g * 8;
-#pragma unroll
-        for (int st = 0; st < 9; ++st) qreg[j][st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
-    }
     // Key of score i (0..3) of this lane within a tile: 16 half + 4 g + i.
     // A score counts if its key <= elim[j] (the token's causal limit, clipped
     // to the item's key range; -1 for an idle token).
@@ -1149,47 +1193,63 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
             }
         }
     }
+    // fused append: split 0 of a block writes the block's own new latents
+    // (nothing in this launch reads those slots, so it can come last)
+    if (a.new_kv != nullptr && it.ks == 0) append_rows(a, r, it.p + it.i0, it.row0 + it.i0, it.i1 - it.i0);
     TRACE(5);
 }
 
 constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
 
+// Persistent workgroups (one per CU) take work items from a counter in the
+// workspace: the chunk items first (largest blocks first), then the decode
+// units, whose small size fills the tail.  An item's results and partial
+// slots depend only on its index, so the schedule never changes the output
+// bits.  The last workgroup to finish zeroes the counters for the next call.
 __global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) char smem[kMainLds];
     __shared__ int s_tmp[12];
     __shared__ int s_pages[kPageWindow];
     __shared__ DecSeg s_seg[kMaxSeg];
-    const int b = blockIdx.x;
-    TRACE(0);
-#ifdef MLA_TRACE
-    if (threadIdx.x == 0 && b < (1 << 16)) {
-        unsigned xcc, hw;
-        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
-        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
-        g_trace[(size_t)b * 16 + 9] = ((unsigned long long)xcc << 32) | hw;
+    __shared__ int s_item;
+    const int n_items = a.n_chunk_items + a.n_dec_units;
+    for (;;) {
+        if (threadIdx.x == 0) s_item = __hip_atomic_fetch_add(a.work, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        const int item = s_item;
+        if (item >= n_items) break;
+        TRACE_ITEM(item);
+        if (item < a.n_chunk_items)
+            chunk_item(a, item, smem, s_tmp, s_pages);
+        else
+            decode_wg(a, item - a.n_chunk_items, smem, s_tmp, s_pages, s_seg);
+        TRACE(7);
+        __syncthreads();  // LDS (and s_item) free for the next item
     }
-#endif
-    if (b < a.n_dec_wg)
-        decode_wg(a, b, smem, s_tmp, s_pages, s_seg);
-    else
-        chunk_item(a, b - a.n_dec_wg, smem, s_tmp, s_pages);
-    TRACE(7);
+    if (threadIdx.x == 0) {
+        const int done = __hip_atomic_fetch_add(a.work + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (done == (int)gridDim.x - 1) {  // every workgroup has taken its last item
+            __hip_atomic_store(a.work, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.work + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
 }
 
 // Split merges, after the attention kernel (the kernel boundary makes every
-// partial visible): first one workgroup per decode workgroup, then one per
-// (chunk item, block row).
+// partial visible): first merge_hsplit workgroups per request (decode rows
+// split across units), then one per (chunk item, block row).
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     __shared__ int s_tmp[12];
     __shared__ DecSeg s_seg[kMaxSeg];
     const int b = blockIdx.x;
-    if (b < a.n_dec_wg) {
-        decode_merge(a, b, s_tmp, s_seg);
+    const int n_dec = a.num_reqs * a.merge_hsplit;
+    if (b < n_dec) {
+        decode_merge(a, b / a.merge_hsplit, b % a.merge_hsplit, s_tmp);
         return;
     }
     // one workgroup per (chunk item, row of its block): the item with key split
     // 0 merges that row over the block's splits
-    const int item = (b - a.n_dec_wg) / kChunkBlockTokens, j = (b - a.n_dec_wg) % kChunkBlockTokens;
+    const int item = (b - n_dec) / kChunkBlockTokens, j = (b - n_dec) % kChunkBlockTokens;
     Located lc;
     if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
     const ChunkItem it = decode_chunk_item(a, lc);
@@ -1295,14 +1355,14 @@ hipError_t launch_append(const AppendArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_attention(const AttnArgs &a, hipStream_t s) {
-    const int grid = a.n_dec_wg + a.n_chunk_items;
+    const int grid = a.grid;
     if (grid == 0) return hipSuccess;
     hipLaunchKernelGGL(attention_kernel, dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_combine(const AttnArgs &a, hipStream_t s) {
-    const long long grid_ll = (long long)a.n_dec_wg + (long long)a.n_chunk_items * kChunkBlockTokens;
+    const long long grid_ll = (long long)a.num_reqs * a.merge_hsplit + (long long)a.n_chunk_items * kChunkBlockTokens;
     if (grid_ll > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const int grid = (int)grid_ll;
     if (grid == 0) return hipSuccess;
