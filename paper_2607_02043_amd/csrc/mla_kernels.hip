@@ -1158,6 +1158,7 @@ __device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = lh;
     }
     __syncthreads();
+    TRACE(6);
     auto row_sum = [&](int tb) {  // key half 0 + key half 1, in that order
         const int w0 = 2 * (tb / kPairTokens), jj = tb % kPairTokens;
         return s_hs[(w0 * kPairTokens + jj) * kHeads + h] + s_hs[((w0 + 1) * kPairTokens + jj) * kHeads + h];
