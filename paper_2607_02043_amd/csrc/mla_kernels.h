@@ -11,8 +11,9 @@ constexpr int kDv = 512;    // value: first 512 latent dims
 constexpr int kRowBytes = kDqk * 2;
 constexpr int kKeysPerTile = 32;
 constexpr int kPageWindow = 256;   // page ids one work item may touch
-constexpr int kThreads = 256;      // 4 wavefronts of 64
-constexpr int kChunkBlockTokens = 6;                        // tokens per chunk work item
+constexpr int kThreads = 256;      // 4 wavefronts of 64 (merge, append; DMA rounds of the attention kernel)
+constexpr int kAttnThreads = 512;  // attention kernel: 8 wavefronts, two per SIMD
+constexpr int kChunkBlockTokens = 8;                        // tokens per chunk work item
 constexpr int kPartialFloats = kHeads * kDv;                // one row's partial output
 constexpr int kPartialStats = kHeads * 2;                   // one row's (max, sum) per head
 constexpr int kMaxDecSegments = 64;                         // requests one decode workgroup may touch

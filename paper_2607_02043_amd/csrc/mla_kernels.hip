@@ -156,9 +156,17 @@ __device__ __forceinline__ float wave_sum16(float v) {
 }
 
 // LDS byte offset of 16-byte chunk c of key k inside a tile.  Chunk
-// positions are xor-swizzled with the key's low 3 bits so that 8 lanes that
-// read the same chunk of 8 consecutive keys hit 8 different bank groups.
-__device__ __forceinline__ int tile_off(int k, int c) { return (k * kChunksPerRow + (c ^ (k & 7))) * 16; }
+// positions are xor-swizzled inside aligned groups of 8 chunks with a 3-bit
+// function of the key.  Decode tiles use the key's low 3 bits (8 lanes that
+// read the same chunk of 8 consecutive keys hit 8 different bank groups);
+// chunk tiles use bits 1..3 of the key, which keeps the 32x32 MFMA operand
+// reads (32 consecutive keys at one chunk) and the transposing value reads
+// free of bank conflicts.
+template <bool CHUNK>
+__device__ __forceinline__ int tile_swz(int k) {
+    return CHUNK ? (((k & 2) << 1) | ((k >> 2) & 3)) : (k & 7);
+}
+__device__ __forceinline__ int tile_off(int k, int c) { return (k * kChunksPerRow + (c ^ tile_swz<false>(k))) * 16; }
 
 // Transposing LDS read (gfx950): inside each 16-lane group, lane i receives
 // element (i & 3) of the 8 bytes read by lane 4 j + (i >> 2), j = 0..3.
@@ -184,9 +192,10 @@ template <typename CountFn>
 __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn count, int *s_tmp,
                             Located &loc) {
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    if (tid == 0) s_tmp[4] = -1;
+    const int nthr = blockDim.x, nw = nthr >> 6;
+    if (tid == 0) s_tmp[8] = -1;
     int running = 0;
-    for (int base = 0; base < num_reqs; base += kThreads) {
+    for (int base = 0; base < num_reqs; base += nthr) {
         const int r = base + tid;
         int cnt = 0, p = 0, row0 = 0, c = 0;
         if (r < num_reqs) {
@@ -204,8 +213,7 @@ __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn
         if (lane == 63) s_tmp[wv] = inc;
         __syncthreads();
         int off = 0, total = 0;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int k = 0; k < nw; ++k) {
             const int t = s_tmp[k];
             off += (k < wv) ? t : 0;
             total += t;
@@ -213,15 +221,17 @@ __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn
         inc += off;
         const int exc = inc - cnt;
         if (cnt > 0 && target >= running + exc && target < running + inc) {
-            s_tmp[4] = r;
-            s_tmp[5] = target - running - exc;
-            s_tmp[6] = p;
-            s_tmp[7] = row0;
-            s_tmp[8] = c;
+            s_tmp[8] = r;
+            s_tmp[9] = target - running - exc;
+            s_tmp[10] = p;
+            s_tmp[11] = row0;
+            s_tmp[12] = c;
         }
         __syncthreads();
-        if (s_tmp[4] >= 0) {
-            loc = Located{s_tmp[4], s_tmp[5], s_tmp[6], s_tmp[7], s_tmp[8]};
+        if (s_tmp[8] >= 0) {  // the same values in every lane: keep them in scalar registers
+            loc = Located{__builtin_amdgcn_readfirstlane(s_tmp[8]), __builtin_amdgcn_readfirstlane(s_tmp[9]),
+                          __builtin_amdgcn_readfirstlane(s_tmp[10]), __builtin_amdgcn_readfirstlane(s_tmp[11]),
+                          __builtin_amdgcn_readfirstlane(s_tmp[12])};
             return true;
         }
         running += total;
@@ -264,7 +274,7 @@ __device__ __forceinline__ ChunkItem decode_chunk_item(const AttnArgs &a, const 
 __device__ __forceinline__ void load_page_window(const AttnArgs &a, int r, int lp0, int n, int *s_pages) {
     const int32_t *row = a.bt + (size_t)r * a.max_pages;
     n = min(n, kPageWindow);
-    for (int i = threadIdx.x; i < n; i += kThreads) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
         const int lp = lp0 + i;
         int pg = lp < a.max_pages ? row[lp] : 0;
         s_pages[i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
@@ -276,7 +286,7 @@ __device__ __forceinline__ void load_page_window(const AttnArgs &a, int r, int l
 // Instruction i of wave wv fills 1 KB segment i * 4 + wv of the tile.
 // With a fused append, keys p_new .. are the step's new latents: key k comes
 // from row new_row0 + k - p_new of a.new_kv instead of its cache slot.
-template <int KEYS>
+template <int KEYS, bool CHUNK>
 __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages, int lp0, int kbase, int k1,
                                            uint32_t lds_tile, int wv, int lane, int p_new, int new_row0) {
     constexpr int kDma = KEYS * kRowBytes / (kThreads * 16);
@@ -288,7 +298,7 @@ __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages
         const int seg = i * 4 + wv;
         const int u = seg * 64 + lane;
         const int kk = u / kChunksPerRow;
-        const int c = (u - kk * kChunksPerRow) ^ (kk & 7);
+        const int c = (u - kk * kChunksPerRow) ^ tile_swz<CHUNK>(kk);
         int key = kbase + kk;
         key = key < k1 ? key : k1 - 1;
         const int page = s_pages[min((key >> a.log2_page) - lp0, kPageWindow - 1)];
@@ -304,9 +314,10 @@ __device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages
 // DMA of a 32-key tile that lies inside one page: a uniform source base (the
 // tile's first key) in SGPRs plus per-lane offsets fixed for all tiles.
 // Round i of wave wv fills LDS chunk u = 256 i + 64 wv + lane of the tile,
-// which holds source chunk (u % 72) ^ (key & 7) of key u / 72.
+// which holds source chunk (u % 72) ^ swz(key) of key u / 72.
 constexpr int kTileDma = kKeysPerTile * kRowBytes / (kThreads * 16);  // 9 rounds per tile
 // Offsets (< 2^16) packed two per register: round i in the half i & 1 of word i / 2.
+template <bool CHUNK>
 __device__ __forceinline__ void tile_dma_offsets(int wv, int lane, uint32_t (&off)[(kTileDma + 1) / 2]) {
 #pragma unroll
     for (int w = 0; w < (kTileDma + 1) / 2; ++w) off[w] = 0;
@@ -314,7 +325,7 @@ __device__ __forceinline__ void tile_dma_offsets(int wv, int lane, uint32_t (&of
     for (int i = 0; i < kTileDma; ++i) {
         const int u = (i * 4 + wv) * 64 + lane;
         const int kk = u / kChunksPerRow;
-        const int c = (u - kk * kChunksPerRow) ^ (kk & 7);
+        const int c = (u - kk * kChunksPerRow) ^ tile_swz<CHUNK>(kk);
         off[i / 2] |= (uint32_t)(kk * kRowBytes + c * 16) << (16 * (i & 1));
     }
 }
@@ -333,7 +344,7 @@ __device__ __forceinline__ void lds_dma16_sbase(const void *sbase, uint32_t voff
 // with a page id outside the pool are skipped.
 __device__ __forceinline__ void append_rows(const AttnArgs &a, int r, int key0, int row0, int n) {
     const int32_t *btr = a.bt + (size_t)r * a.max_pages;
-    for (int x = threadIdx.x; x < n * kChunksPerRow; x += kThreads) {
+    for (int x = threadIdx.x; x < n * kChunksPerRow; x += blockDim.x) {
         const int i = x / kChunksPerRow, c = x - i * kChunksPerRow;
         const int key = key0 + i;
         const int lp = key >> a.log2_page;
@@ -471,9 +482,9 @@ struct DecSeg {
 
 __device__ __forceinline__ int dec_tiles(int p, int c) { return c == 1 ? ceil_div(p + 1, kDecKeys) : 0; }
 
-// Exclusive prefix sum over the 256 threads of the workgroup (uses s_w[0..3]).
+// Exclusive prefix sum over the threads of the workgroup (uses s_w[0 .. waves - 1]).
 __device__ __forceinline__ int block_scan_excl(int v, int *s_w, int &total) {
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
     int inc = v;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
@@ -484,8 +495,7 @@ __device__ __forceinline__ int block_scan_excl(int v, int *s_w, int &total) {
     __syncthreads();
     int off = 0;
     total = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < nw; ++k) {
         const int t = s_w[k];
         off += (k < wv) ? t : 0;
         total += t;
@@ -498,7 +508,7 @@ __device__ __forceinline__ int block_scan_excl(int v, int *s_w, int &total) {
 __device__ int find_segments(const AttnArgs &a, int R0, int R1, DecSeg *s_seg, int *s_tmp) {
     const int tid = threadIdx.x;
     int running = 0, nseg = 0;
-    for (int base = 0; base < a.num_reqs && running < R1; base += kThreads) {
+    for (int base = 0; base < a.num_reqs && running < R1; base += blockDim.x) {
         const int r = base + tid;
         int nt = 0, p = 0, row0 = 0;
         if (r < a.num_reqs) {
@@ -594,6 +604,9 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, h = lane & 15;
+    // waves 0..3 stream and compute; any further waves of the workgroup only
+    // take part in its barriers
+    const bool active = wv < 4;
     const int R0 = w * a.dec_unit_tiles;
     const int R1 = min(R0 + a.dec_unit_tiles, a.dec_total_tiles);
     if (R0 >= R1) return;
@@ -617,7 +630,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
         const int klast = min(sg.t1 * kDecKeys, sg.p + 1) - 1;
         const int n = (klast >> a.log2_page) - sg.lp0 + 1;
         const int32_t *btr = a.bt + (size_t)sg.r * a.max_pages;
-        for (int i = tid; i < n && sg.pw + i < kPageWindow; i += kThreads) {
+        for (int i = tid; i < n && sg.pw + i < kPageWindow; i += blockDim.x) {
             const int lp = sg.lp0 + i;
             const int pg = lp < a.max_pages ? btr[lp] : 0;
             s_pages[sg.pw + i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
@@ -635,12 +648,12 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
     const int n_units = nseg + (R1 - R0);
     TRACE_VAL(8, 1000000ull * 2 + n_units);
     uint32_t dma_off[(kTileDma + 1) / 2];
-    tile_dma_offsets(wv, lane, dma_off);
+    tile_dma_offsets<false>(wv, lane, dma_off);
     const uint32_t ring = lds_addr(smem);
     float *s_X = reinterpret_cast<float *>(smem + kDecRing * kDecTileBytes);
     Cursor prod{0, -1}, cons{0, -1};
     for (int u = 0; u < kDecRing - 1 && u < n_units; ++u) {
-        issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + u * kDecTileBytes, wv, lane, dma_off);
+        if (active) issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + u * kDecTileBytes, wv, lane, dma_off);
         advance(prod, s_seg);
     }
 
@@ -660,16 +673,24 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
         wait_units_newer(min(kDecRing - 2, n_units - 1 - u));
         __syncthreads();
         if (prod.j < nseg) {
-            issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + ((u + kDecRing - 1) % kDecRing) * kDecTileBytes, wv,
-                       lane, dma_off);
+            if (active)
+                issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + ((u + kDecRing - 1) % kDecRing) * kDecTileBytes,
+                           wv, lane, dma_off);
             advance(prod, s_seg);
         }
         const char *slot = smem + (u % kDecRing) * kDecTileBytes;
         const DecSeg sg = s_seg[cons.j];
         if (cons.t < 0) {  // a new request: its query block
+            if (active) {
 #pragma unroll
-            for (int s2 = 0; s2 < 9; ++s2)
-                qreg[s2] = *reinterpret_cast<const u32x4 *>(slot + (h * kChunksPerRow + (9 * hf + s2) * 4 + g) * 16);
+                for (int s2 = 0; s2 < 9; ++s2)
+                    qreg[s2] = *reinterpret_cast<const u32x4 *>(slot + (h * kChunksPerRow + (9 * hf + s2) * 4 + g) * 16);
+            }
+            advance(cons, s_seg);
+            continue;
+        }
+        if (!active) {  // the partial-score barrier, then the next unit
+            __syncthreads();
             advance(cons, s_seg);
             continue;
         }
@@ -793,7 +814,7 @@ __device__ void decode_merge(const AttnArgs &a, int r, int part, int *s_tmp) {
     const int tid = threadIdx.x;
     // T = decode tiles of the requests before r (one block-wide sum per 256 requests)
     int T = 0;
-    for (int base = 0; base < r; base += kThreads) {
+    for (int base = 0; base < r; base += blockDim.x) {
         const int q = base + tid;
         int nt = 0;
         if (q < r) {
@@ -824,72 +845,26 @@ __device__ void decode_merge(const AttnArgs &a, int r, int part, int *s_tmp) {
 }
 
 // ------------------------------------------------------------- chunk path
-// Chunk rows: one workgroup per block of 6 query tokens and a key range of
-// ks_chunk keys; 32-key tiles stream through a 3-slot DMA ring.
-//  * Scores.  Waves 2p and 2p+1 hold the queries of tokens 3p .. 3p+2, wave 2p
-//    over latent dims 0..287 and wave 2p+1 over dims 288..575, so every K
-//    operand read from LDS feeds three MFMAs per key block.  The pair then
-//    swaps partial scores through LDS so that wave 2p+h holds the full scores
-//    of keys 16h .. 16h+15 of the tile for its three tokens.
+// Chunk rows: one workgroup of 8 wavefronts (two per SIMD) per block of 8
+// query tokens (128 rows of 16 heads) and a key range of ks_chunk keys;
+// 32-key tiles stream through a 3-slot global -> LDS DMA ring (all eight
+// wavefronts issue it).  Two
+// wavefronts per SIMD let one issue matrix work while the other waits on LDS
+// or runs its softmax.
+//  * Scores.  Wave w holds the query of token w (16 heads) over all 576
+//    latent dims (18 operands of 32 dims) and forms S^T = K Q^T for two
+//    16-key blocks with 16x16x32 MFMAs; nothing is exchanged between waves.
 //  * Softmax.  Probabilities against a fixed reference max (no rescaling; see
-//    the passes below), published in LDS as fp16 in MFMA B-operand order.
-//  * P*V.  Every wave accumulates its 128-wide slice of the value dims for all
-//    6 tokens: each transposed V^T operand read is converted to fp16 once and
-//    feeds 6 MFMAs.  fp16 holds every bf16 value in [2^-14, 65504] exactly.
-// The loop is software-pipelined: the softmax of tile t runs in the same
-// stretch of code as the P*V products of tile t - 1, so VALU work issues
-// while the matrix cores are busy; two barriers per tile.
-__device__ __forceinline__ void score_bases(int key, int g, int base[2]) {
-    // chunk 4 st + g of `key` sits at base[st & 1] + 128 (st >> 1): the xor
-    // swizzle only touches the chunk index's low 3 bits
-#pragma unroll
-    for (int e = 0; e < 2; ++e) base[e] = (key * kChunksPerRow + ((4 * e + g) ^ (key & 7))) * 16;
-}
-
-constexpr int kPairTokens = kChunkBlockTokens / 2;  // 3 tokens per wave pair
-
-// Partial scores of one 32-key tile over k-steps 9 HALF .. 9 HALF + 8 (288
-// latent dims) for the wave's 3 tokens, element i of key block kt = key
-// 16 kt + 4 g + i, head l%16.  keep[j] is key block HALF (this wave finishes
-// it), give[j] the other block (handed to the partner).  K operands are read
-// two steps ahead.
-template <int HALF>
-__device__ __forceinline__ void score_half(const char *tile, const u32x4 (&qreg)[kPairTokens][9], int lane,
-                                           f32x4 (&keep)[kPairTokens], f32x4 (&give)[kPairTokens]) {
-    f32x4 s[kPairTokens][2];
-    const int g = lane >> 4;
-    int b0[2], b1[2];
-    score_bases(lane & 15, g, b0);
-    score_bases(16 + (lane & 15), g, b1);
-#pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) s[j][0] = s[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    u32x4 a0[3], a1[3];
-#pragma unroll
-    for (int st = 0; st < 2; ++st) {
-        const int gs = 9 * HALF + st;
-        a0[st] = *reinterpret_cast<const u32x4 *>(tile + b0[gs & 1] + 128 * (gs >> 1));
-        a1[st] = *reinterpret_cast<const u32x4 *>(tile + b1[gs & 1] + 128 * (gs >> 1));
-    }
-#pragma unroll
-    for (int st = 0; st < 9; ++st) {
-        if (st + 2 < 9) {  // operands two steps ahead
-            const int gs = 9 * HALF + st + 2;
-            a0[(st + 2) % 3] = *reinterpret_cast<const u32x4 *>(tile + b0[gs & 1] + 128 * (gs >> 1));
-            a1[(st + 2) % 3] = *reinterpret_cast<const u32x4 *>(tile + b1[gs & 1] + 128 * (gs >> 1));
-        }
-#pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) {
-            s[j][0] = mfma_bf16(a0[st % 3], qreg[j][st], s[j][0]);
-            s[j][1] = mfma_bf16(a1[st % 3], qreg[j][st], s[j][1]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) {
-        keep[j] = s[j][HALF];
-        give[j] = s[j][1 - HALF];
-    }
-}
+//    the passes below), written to LDS as fp16 in the B-operand order of P*V:
+//    slot 8 g + 4 kt + i of lane (g, head) holds key 16 kt + 4 g + i, which
+//    is exactly what the lane's own scores hold, so each lane stores 16 bytes.
+//  * P*V.  Wave w accumulates value dims 64 w .. 64 w + 63 of all 8 tokens
+//    (4 dim blocks x 8 tokens of 16x16 accumulators); V^T comes from
+//    transposing LDS reads with the same key order, converted bf16 -> fp16 in
+//    registers (exact for |v| in [2^-14, 65504]).
+// Per tile: one barrier.  After it, the P*V of tile t and the scores of tile
+// t+1 run back to back (their operands come from different ring slots and P
+// buffers), then the softmax of tile t+1 fills the other P buffer.
 
 // bf16 pairs -> fp16 pairs (exact for |v| in [2^-14, 65504]; larger values
 // clamp to +-65504, smaller ones round toward zero).
@@ -904,300 +879,339 @@ __device__ __forceinline__ uint32_t f16x2_bits(float a, float b) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-// V^T operand of 16 value dims x 32 keys (transposing reads of keys k and
-// k + 16, see tr_base) converted to fp16.
-__device__ __forceinline__ u32x4 load_vt_f16(const char *vb) {
-    const u32x2 lo = lds_read_tr16(vb);
-    const u32x2 hi = lds_read_tr16(vb + 16 * kRowBytes);
-    return u32x4{bf16x2_to_f16x2(lo[0]), bf16x2_to_f16x2(lo[1]), bf16x2_to_f16x2(hi[0]), bf16x2_to_f16x2(hi[1])};
-}
-
+constexpr int kCT = kChunkBlockTokens;                 // 8 tokens per item, one per wave
+constexpr int kQSteps = kDqk / 32;                     // 18 query operands of 32 dims
 constexpr int kChunkRing = 3;
-constexpr int kXBytes = 4 * kPairTokens * 64 * 16;         // score swap: [wave][token][lane] f32x4
-constexpr int kPBytes = 2 * kChunkBlockTokens * 64 * 16;  // fp16 P, two buffers: [buf][token][lane] u32x4
-constexpr int kHsBytes = 4 * kPairTokens * kHeads * 4;     // per-wave half maxima / sums: [wave][token][head]
-constexpr int kChunkLds = kChunkRing * kChunkTileBytes + kXBytes + kPBytes + kHsBytes + 16;
+constexpr int kPTile = kCT * 64 * 16;                  // fp16 P of one tile: [token][lane] 16 bytes
+constexpr int kChunkLds = kChunkRing * kChunkTileBytes + 2 * kPTile + 2 * kCT * kHeads * 4 + 16;
 // Largest exponent (log2 units) a probability may take against the reference
 // max: 2^15 stays inside fp16.
 constexpr float kMaxPExp = 15.f;
 
-// Passes of a chunk item.  The reference max of each (token, head) is fixed
-// for the whole key range, so the accumulators are never rescaled:
-//   kPassMain   reference = max of the first tile.  Each lane also tracks the
-//               max of every score it sees.  If a later score exceeds the
-//               reference by more than 2^15, the pass still runs to the end
-//               (an exit from the middle of the loop costs the accumulators
-//               their registers) and its products are discarded;
-//   kPassExact  then redoes the item against the exact max.
-enum { kPassMain = 0, kPassExact = 1 };
+// Chunk tiles are laid out chunk-major: 16-byte chunk c (8 latent dims) of
+// tile key k (0..31) sits at position 32 c + (k ^ 8 (c & 1)).  Sixteen
+// consecutive keys of one chunk are then 256 contiguous bytes (the K operand
+// reads), and the transposing value reads of 8 keys at two neighbouring
+// chunks fall into disjoint halves of the banks.  DMA round i (36 per tile,
+// 64 positions each) fills chunks 2 i and 2 i + 1: lane l loads chunk
+// 2 i + (l >> 5) of key (l & 31) ^ 8 (l >> 5), so one source address per lane
+// serves every round (+32 bytes per round).  Wave w issues rounds w, w + 8, ...
+constexpr int kChunkDmaRounds = kChunkTileBytes / 1024;  // 36
 
-__device__ void chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages) {
+// The instruction offset OFF moves the LDS destination as well as the
+// global source, so M0 is set to lds_base - OFF.
+template <int OFF>
+__device__ __forceinline__ void lds_dma16_imm(const void *gsrc, uint32_t lds_base) {
+    asm volatile(
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off offset:%2\n\t"
+        :
+        : "{m0}"(lds_base - OFF), "v"(gsrc), "i"(OFF)
+        : "memory");
+}
+template <int OFF>
+__device__ __forceinline__ void lds_dma16_sbase_imm(const void *sbase, uint32_t voff, uint32_t lds_base) {
+    asm volatile(
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, %1 offset:%3\n\t"
+        :
+        : "v"(voff), "s"(sbase), "{m0}"(lds_base - OFF), "i"(OFF)
+        : "memory");
+}
+
+// Passes of a chunk item.  The reference max of each row is fixed for the
+// whole key range, so the accumulators are never rescaled:
+//   main    reference = max of the first tile.  Each lane also tracks the max
+//           of every score it sees.  If a later score exceeds the reference by
+//           more than 2^15, the pass still runs to the end and its products
+//           are discarded;
+//   exact   then the item runs again against the exact max.
+
+// Returns true when the main pass was abandoned: the caller then runs the
+// item again with exact = true (the exact maxima wait in LDS).
+__device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages, bool exact) {
     Located lc;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return false;
     const ChunkItem it = decode_chunk_item(a, lc);
     TRACE(1);
     const int r = it.r;
-    if (it.k0 >= it.k1) return;  // key range past this block's causal limit
-    if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;
-    if (it.nks_eff > 1 && a.ws_chunk_o == nullptr) return;
+    if (it.k0 >= it.k1) return false;  // key range past this block's causal limit
+    if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return false;
+    if (it.nks_eff > 1 && a.ws_chunk_o == nullptr) return false;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int g = lane >> 4, h = lane & 15;
-    const int pair = wv >> 1, half = wv & 1, partner = wv ^ 1;
-    const int nt = it.i1 - it.i0;  // tokens of this block (1 .. 6)
+    const int g = lane >> 4, hd = lane & 15;
+    const int nt = it.i1 - it.i0;  // tokens of this block (1 .. 8)
     const int ntiles = ceil_div(it.k1 - it.k0, kChunkKeys);
     const int lp0 = it.k0 >> a.log2_page;
-    // queries of tokens 3 pair + j over this wave's half of the latent dims
-    // (issued first: their latency overlaps the page-window load)
-    u32x4 qreg[kPairTokens][9];
+    // This wave's token (an idle token repeats the last one; its results are
+    // not stored).  Query operands: lane l holds dims 32 s + 8 g .. + 7 of
+    // head hd, s = 0..17 (issued first: their latency overlaps the page-window
+    // load).
+    const int tk = min(wv, nt - 1);
+    u32x4 qreg[kQSteps];
+    {
+        const uint16_t *qp = a.q + ((size_t)(it.row0 + it.i0 + tk) * kHeads + hd) * kDqk + 8 * g;
 #pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) {
-        const int row = it.row0 + it.i0 + min(kPairTokens * pair + j, nt - 1);  // an idle token re-reads a row
-        const uint16_t *qp = a.q + ((size_t)row * kHeads + h) * kDqk + 9 * half * 32 + g * 8;
-#pragma unroll
-        for (int st = 0; st < 9; ++st) qreg[j][st] = *reinterpret_cast<const u32x4 *>(qp + st * 32);
+        for (int s = 0; s < kQSteps; ++s) qreg[s] = *reinterpret_cast<const u32x4 *>(qp + 32 * s);
     }
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
     TRACE(2);
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
     const uint32_t ring = lds_addr(smem);
-    char *const lds_x = smem + kChunkRing * kChunkTileBytes;
-    f32x4 *s_X = reinterpret_cast<f32x4 *>(lds_x);                                  // [wave][token][lane]
-    uint32_t *s_P = reinterpret_cast<uint32_t *>(lds_x + kXBytes);                  // [buf][token][lane][4]
-    float *s_hs = reinterpret_cast<float *>(lds_x + kXBytes + kPBytes);             // [wave][token][head]
-    int *s_abort = reinterpret_cast<int *>(lds_x + kXBytes + kPBytes + kHsBytes);
+    char *const s_pbuf = smem + kChunkRing * kChunkTileBytes;           // [2][token][lane] 16 bytes
+    float *const s_l = reinterpret_cast<float *>(s_pbuf + 2 * kPTile);  // [token][head] row sums
+    float *const s_mx = s_l + kCT * kHeads;                            // [token][head] exact maxima
+    int *const s_abort = reinterpret_cast<int *>(s_mx + kCT * kHeads);
 
-    // Key of score i (0..3) of this lane within a tile: 16 half + 4 g + i.
-    // A score counts if its key <= elim[j] (the token's causal limit, clipped
-    // to the item's key range; -1 for an idle token).
-    int elim[kPairTokens];
-#pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) {
-        const int tb = kPairTokens * pair + j;
-        elim[j] = tb < nt ? min(it.p + it.i0 + tb, it.k1 - 1) - (16 * half + 4 * g) : -1 - (it.k1 + 64);
-    }
-    // V^T reads: value dims wv*128 + 16 mt + 4 (l & 3) .. + 3 of keys tr_key and
-    // tr_key + 16.  Their 16-byte chunk is wv*16 + 8 (mt >> 2) + (2 (mt & 3) +
-    // ((l & 3) >> 1)); the xor swizzle touches only the low three bits, so four
-    // bases plus immediate offsets cover all mt.
+    // Causal limit of this wave's token (absolute key index, clipped to the
+    // item's key range); wave-uniform.
+    const int lim = __builtin_amdgcn_readfirstlane(min(it.p + it.i0 + tk, it.k1 - 1));
+
+    // K operand of key block kb, step s (keys 16 kb + hd, dims 32 s + 8 g ..):
+    // chunk 4 s + g, so kq_off + 2048 s + 256 kb.
+    const int kq_off = g * 512 + (hd ^ (8 * (g & 1))) * 16;
+    // V^T operand of value block db (dims 64 wv + 16 db + (lane & 15)): two
+    // transposing reads of keys tr_key .. + 3 and tr_key + 16 .. + 3 at dims
+    // 64 wv + 16 db + 4 (lane & 3) .. + 3, i.e. chunk 8 wv + 2 db + ((lane >> 1) & 1):
+    // vt_off + 1024 db (+ 256 for the second read).
     const int tr_key = 4 * g + ((lane & 15) >> 2);
-    int tr_base[4];
-#pragma unroll
-    for (int m4 = 0; m4 < 4; ++m4)
-        tr_base[m4] = (tr_key * kChunksPerRow + wv * 16 + ((2 * m4 + ((lane & 3) >> 1)) ^ (tr_key & 7))) * 16 +
-                      (lane & 1) * 8;
+    const int vt_off = 4096 * wv + ((lane >> 1) & 1) * 512 + (tr_key ^ (8 * ((lane >> 1) & 1))) * 16 + (lane & 1) * 8;
 
-    uint32_t dma_off[(kTileDma + 1) / 2];
-    tile_dma_offsets(wv, lane, dma_off);
-    // DMA of tile t into its ring slot: a full tile inside one page takes the
-    // uniform-base form, any other tile (small pages, the last partial tile)
-    // the general one.  page_of(t) may be read well before the issue.
+    // DMA of tile t into its ring slot.  A full tile inside one page takes a
+    // uniform (scalar) base; any other tile (small pages, the last partial
+    // tile, new latents of a fused append) one address per lane.
+    const int dkey = (lane & 31) ^ (8 * (lane >> 5));           // this lane's key in every round
+    const uint32_t dvoff = dkey * kRowBytes + 16 * (lane >> 5) + 32 * wv;
     const bool in_page = a.page_size >= kChunkKeys;
-    // with a fused append, keys p .. come from the new latents (general path)
     const int cached_end = a.new_kv != nullptr ? min(it.k1, it.p) : it.k1;
     auto page_of = [&](int t) {
         return s_pages[min(((it.k0 + t * kChunkKeys) >> a.log2_page) - lp0, kPageWindow - 1)];
     };
-    auto issue = [&](int t, int page) {
+    auto issue = [&](int t, int slot, int page) {
         const int kbase = it.k0 + t * kChunkKeys;
-        const uint32_t dst = ring + (t % kChunkRing) * kChunkTileBytes;
+        const uint32_t dst = ring + slot * kChunkTileBytes + wv * 1024;
+        const bool fifth = wv + 32 < kChunkDmaRounds;  // waves 0..3 issue a fifth round
         if (in_page && kbase + kChunkKeys <= cached_end) {
             const char *src = reinterpret_cast<const char *>(a.kv) +
                               ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size +
                                (kbase & (a.page_size - 1))) * kRowBytes;
-#pragma unroll
-            for (int i = 0; i < kTileDma; ++i)
-                lds_dma16_sbase(src, (dma_off[i / 2] >> (16 * (i & 1))) & 0xffffu,
-                                __builtin_amdgcn_readfirstlane(dst + (i * 4 + wv) * 1024));
+            lds_dma16_sbase_imm<0>(src, dvoff, __builtin_amdgcn_readfirstlane(dst));
+            lds_dma16_sbase_imm<256>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 8 * 1024));
+            lds_dma16_sbase_imm<512>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 16 * 1024));
+            lds_dma16_sbase_imm<768>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 24 * 1024));
+            if (fifth) lds_dma16_sbase_imm<1024>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 32 * 1024));
         } else {
-            issue_tile<kChunkKeys>(a, s_pages, lp0, kbase, it.k1, dst, wv, lane, it.p, it.row0);
+            // keys past the item's range repeat its last key (a finite cached latent)
+            const int key = min(kbase + dkey, it.k1 - 1);
+            const char *gs;
+            if (a.new_kv != nullptr && key >= it.p) {
+                gs = reinterpret_cast<const char *>(a.new_kv) + (size_t)(it.row0 + key - it.p) * kRowBytes;
+            } else {
+                const int pg = s_pages[min((key >> a.log2_page) - lp0, kPageWindow - 1)];
+                gs = reinterpret_cast<const char *>(a.kv) +
+                     ((size_t)pg * a.page_size + (key & (a.page_size - 1))) * kRowBytes;
+            }
+            gs += 16 * (lane >> 5) + 32 * wv;
+            lds_dma16_imm<0>(gs, __builtin_amdgcn_readfirstlane(dst));
+            lds_dma16_imm<256>(gs, __builtin_amdgcn_readfirstlane(dst + 8 * 1024));
+            lds_dma16_imm<512>(gs, __builtin_amdgcn_readfirstlane(dst + 16 * 1024));
+            lds_dma16_imm<768>(gs, __builtin_amdgcn_readfirstlane(dst + 24 * 1024));
+            if (fifth) lds_dma16_imm<1024>(gs, __builtin_amdgcn_readfirstlane(dst + 32 * 1024));
         }
     };
 
-    float m_ref[kPairTokens], m_lane[kPairTokens], l_run[kPairTokens];
-#pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) m_ref[j] = m_lane[j] = kNegInf;
-    f32x4 acc[kChunkBlockTokens][8];  // [token][value-dim tile of this wave's 128-wide slice]
-    f32x4 keep[kPairTokens];
+    float m_ref = kNegInf, m_lane = kNegInf, l_run = 0.f;
+    f32x4 acc[kCT][4];  // [token][value block db]
     bool bad = false;
 
-    auto scores = [&](int t) {
-        const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
-        f32x4 give[kPairTokens];
-        if (half)
-            score_half<1>(tile, qreg, lane, keep, give);
-        else
-            score_half<0>(tile, qreg, lane, keep, give);
-        // hand the other key half over to the partner
+    // S^T of tile t for this wave's token: lane l, element i of block kb =
+    // key 16 kb + 4 g + i of the tile, head hd.  Two accumulation chains.
+    auto scores = [&](int slot, f32x4 (&s)[2]) {
+        const char *tile = smem + __builtin_amdgcn_readfirstlane(slot * kChunkTileBytes) + kq_off;
+        s[0] = s[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        constexpr int D = 1;  // steps whose K operands are in flight
+        u32x4 av[D][2];
 #pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) s_X[(wv * kPairTokens + j) * 64 + lane] = give[j];
-    };
-    // full scores of this lane's 4 keys of token j (masked), raw dot products
-    auto tile_scores = [&](int t, int j, float raw[4]) {
-        const f32x4 f = keep[j] + s_X[(partner * kPairTokens + j) * 64 + lane];
-        const int rel = elim[j] - (it.k0 + t * kChunkKeys);
+        for (int st = 0; st < D; ++st)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) raw[i] = i <= rel ? f[i] : kNegInf;
+            for (int kb = 0; kb < 2; ++kb)
+                av[st][kb] = *reinterpret_cast<const u32x4 *>(tile + 2048 * st + 256 * kb);
+#pragma unroll
+        for (int st = 0; st < kQSteps; ++st) {
+            u32x4 cur[2] = {av[st % D][0], av[st % D][1]};
+            if (st + D < kQSteps) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+                    av[st % D][kb] = *reinterpret_cast<const u32x4 *>(tile + 2048 * (st + D) + 256 * kb);
+            }
+            s[0] = mfma_bf16(cur[0], qreg[st], s[0]);
+            s[1] = mfma_bf16(cur[1], qreg[st], s[1]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
-    auto softmax = [&](int t, bool main_pass, int j) {
-        float raw[4];
-        tile_scores(t, j, raw);
-        const float xm = fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])) * a.scale_log2;
-        m_lane[j] = fmaxf(m_lane[j], xm);
+    // masked raw scores of tile t
+    auto masked = [&](int t, const f32x4 (&s)[2], float (&x)[8]) {
+        const int kbase = it.k0 + t * kChunkKeys;
+        if (kbase + kChunkKeys - 1 <= lim) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = s[e >> 2][e & 3];
+        } else {
+            const int rel = lim - kbase - 4 * g;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = (16 * (e >> 2) + (e & 3) <= rel) ? s[e >> 2][e & 3] : kNegInf;
+        }
+    };
+    auto lane_max = [&](const float (&x)[8]) {
+        return fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+    };
+    auto softmax = [&](int t, int pbuf, const f32x4 (&s)[2], bool main_pass) {
+        float x[8];
+        masked(t, s, x);
+        const float xm = lane_max(x) * a.scale_log2;
+        m_lane = fmaxf(m_lane, xm);
         // also true for a first visible key after the first tile
-        bad |= main_pass && xm - m_ref[j] > kMaxPExp;
+        bad |= main_pass && xm - m_ref > kMaxPExp;
         // the scaled score is rounded before the max is subtracted, so the max
         // key gets p = 1 exactly; masked scores give p = 0
-        const float mref = m_ref[j] == kNegInf ? 0.f : m_ref[j];
-        float p[4];
+        const float mref = m_ref == kNegInf ? 0.f : m_ref;
+        float p[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int e = 0; e < 8; ++e) {
 #pragma clang fp contract(off)
-            p[i] = __builtin_amdgcn_exp2f(raw[i] * a.scale_log2 - mref);
+            p[e] = __builtin_amdgcn_exp2f(x[e] * a.scale_log2 - mref);
         }
-        l_run[j] += (p[0] + p[1]) + (p[2] + p[3]);
-        const int tb = kPairTokens * pair + j;
-        *reinterpret_cast<u32x2 *>(s_P + (((t & 1) * kChunkBlockTokens + tb) * 64 + lane) * 4 + 2 * half) =
-            u32x2{f16x2_bits(p[0], p[1]), f16x2_bits(p[2], p[3])};
+        l_run += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+        *reinterpret_cast<u32x4 *>(s_pbuf + __builtin_amdgcn_readfirstlane(pbuf * kPTile) + (wv * 64 + lane) * 16) =
+            u32x4{f16x2_bits(p[0], p[1]), f16x2_bits(p[2], p[3]), f16x2_bits(p[4], p[5]), f16x2_bits(p[6], p[7])};
     };
-    auto pv = [&](int t, bool with_softmax, bool main_pass) {  // P*V of tile t (and softmax of t + 1)
-        const char *tile = smem + (t % kChunkRing) * kChunkTileBytes;
-        u32x4 bp[kChunkBlockTokens];
+    // O^T += V^T P^T for tile t (P from buffer t & 1)
+    auto pv = [&](int slot, int pbuf) {
+        const char *tile = smem + __builtin_amdgcn_readfirstlane(slot * kChunkTileBytes) + vt_off;
+        const char *pb = s_pbuf + __builtin_amdgcn_readfirstlane(pbuf * kPTile) + lane * 16;
+        u32x4 av[4];
 #pragma unroll
-        for (int j = 0; j < kChunkBlockTokens; ++j)
-            bp[j] = *reinterpret_cast<const u32x4 *>(s_P + (((t & 1) * kChunkBlockTokens + j) * 64 + lane) * 4);
-        u32x4 av[2];
-        av[0] = load_vt_f16(tile + tr_base[0]);
+        for (int db = 0; db < 4; ++db) {
+            const char *vb = tile + 1024 * db;
+            const u32x2 lo = lds_read_tr16(vb);
+            const u32x2 hi = lds_read_tr16(vb + 256);
+            av[db] = u32x4{bf16x2_to_f16x2(lo[0]), bf16x2_to_f16x2(lo[1]), bf16x2_to_f16x2(hi[0]),
+                           bf16x2_to_f16x2(hi[1])};
+        }
+        u32x4 bp[2];
+        bp[0] = *reinterpret_cast<const u32x4 *>(pb);
 #pragma unroll
-        for (int mt = 0; mt < 8; ++mt) {
-            if (mt + 1 < 8) av[(mt + 1) & 1] = load_vt_f16(tile + tr_base[(mt + 1) & 3] + 128 * ((mt + 1) >> 2));
+        for (int tb = 0; tb < kCT; ++tb) {  // P of token tb + 1 is read one token ahead
+            if (tb + 1 < kCT) bp[(tb + 1) & 1] = *reinterpret_cast<const u32x4 *>(pb + (tb + 1) * 64 * 16);
 #pragma unroll
-            for (int j = 0; j < kChunkBlockTokens; ++j) acc[j][mt] = mfma_f16(av[mt & 1], bp[j], acc[j][mt]);
-            if (with_softmax && (mt & 1) && mt < 2 * kPairTokens) softmax(t + 1, main_pass, mt >> 1);
+            for (int db = 0; db < 4; ++db) acc[tb][db] = mfma_f16(av[db], bp[tb & 1], acc[tb][db]);
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
 
     TRACE(3);
-    for (int pass = kPassMain; pass <= kPassExact; ++pass) {
-        const bool main_pass = pass == kPassMain;
-        if (tid == 0) *s_abort = 0;
-        __syncthreads();  // page window and abort flag ready; the ring is idle
-        for (int t = 0; t < 2 && t < ntiles; ++t) issue(t, page_of(t));
-        wait_units_newer(min(1, ntiles - 1));  // queries and tile 0 landed
-        __syncthreads();
+    const bool main_pass = !exact;
+    if (exact) m_ref = s_mx[wv * kHeads + hd];
+    if (tid == 0) *s_abort = 0;
+    __syncthreads();  // page window and abort flag ready; the ring is idle
+    for (int t = 0; t < 2 && t < ntiles; ++t) issue(t, t, page_of(t));
+    // queries and tile 0 landed (tile 1 may still be in flight: 5 or 4 rounds)
+    if (ntiles == 1)
+        wait_dma_all();
+    else if (wv + 32 < kChunkDmaRounds)
+        asm volatile("s_waitcnt vmcnt(5)" ::: "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    __syncthreads();
 #pragma unroll
-        for (int j = 0; j < kChunkBlockTokens; ++j)
+    for (int tb = 0; tb < kCT; ++tb)
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) l_run[j] = 0.f;
-        bad = false;
+        for (int db = 0; db < 4; ++db) acc[tb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-        // tile 0: scores, the reference max (both key halves), probabilities
-        TRACE_TILE(0, 11);
-        scores(0);
-        __syncthreads();
+    // tile 0: scores, the reference max, probabilities
+    TRACE_TILE(0, 11);
+    {
+        f32x4 s0[2];
+        scores(0, s0);
         if (main_pass) {
-#pragma unroll
-            for (int j = 0; j < kPairTokens; ++j) {
-                float raw[4];
-                tile_scores(0, j, raw);
-                const float hm = wave_max16(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])) * a.scale_log2);
-                if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = hm;
-                m_ref[j] = hm;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int j = 0; j < kPairTokens; ++j)
-                m_ref[j] = fmaxf(m_ref[j], s_hs[(partner * kPairTokens + j) * kHeads + h]);
+            float x[8];
+            masked(0, s0, x);
+            m_ref = wave_max16(lane_max(x) * a.scale_log2);
         }
-#pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) softmax(0, main_pass, j);
-        if (ntiles > 1) wait_dma_all();  // tile 1
+        softmax(0, 0, s0, main_pass);
+    }
+    int slot = 0;  // ring slot of tile t (t % 3)
+    // steady state: after the barrier, P*V of tile t and the scores of t + 1,
+    // then the softmax of t + 1
+    for (int t = 0; t < ntiles; ++t) {
+        TRACE_TILE(t, 11);
+        const int next_page = page_of(min(t + 2, ntiles - 1));
+        if (t + 1 < ntiles) wait_dma_all();  // tile t + 1 (this wave's part)
         if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
-        __syncthreads();
-        if (2 < ntiles) issue(2, page_of(2));
-        // steady state: scores of tile t, then P*V of t - 1 with the softmax of t
-        for (int t = 1; t < ntiles; ++t) {
-            TRACE_TILE(t, 11);
-            const int next_page = page_of(min(t + 2, ntiles - 1));  // consumed after the second barrier
-            scores(t);
-            __syncthreads();
-            TRACE_TILE(t, 12);
-            pv(t - 1, true, main_pass);
-            TRACE_TILE(t, 15);
-            if (t + 1 < ntiles) wait_dma_all();  // tile t + 1
-            if (__builtin_amdgcn_ballot_w64(bad) != 0 && lane == 0) *s_abort = 1;
-            __syncthreads();
-            TRACE_TILE(t, 13);
-            if (t + 2 < ntiles) issue(t + 2, next_page);
-            TRACE_TILE(t, 14);
+        __syncthreads();  // tile t + 1 and P of tile t complete; slot (t + 2) % 3 and P buffer (t + 1) & 1 free
+        TRACE_TILE(t, 12);
+        const int slot1 = slot == kChunkRing - 1 ? 0 : slot + 1;
+        const int slot2 = slot1 == kChunkRing - 1 ? 0 : slot1 + 1;
+        if (t + 2 < ntiles) issue(t + 2, slot2, next_page);
+        pv(slot, t & 1);
+        if (t + 1 < ntiles) {
+            f32x4 s1[2];
+            scores(slot1, s1);
+            softmax(t + 1, (t + 1) & 1, s1, main_pass);
         }
-        pv(ntiles - 1, false, main_pass);
-        // the last barrier passed after every wave's last flag write
-        if (!main_pass || __builtin_amdgcn_readfirstlane(*s_abort) == 0) break;
-        // abandoned: the exact max of both key halves, then the exact pass
-#pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) {
-            const float hm = wave_max16(m_lane[j]);
-            if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = hm;
-            m_ref[j] = hm;
-        }
+        slot = slot1;
+        TRACE_TILE(t, 13);
+    }
+    __syncthreads();  // every wave's last flag write and P*V reads are done
+    if (main_pass && __builtin_amdgcn_readfirstlane(*s_abort) != 0) {
+        // abandoned: publish the exact maxima for the exact pass
+        const float mx = wave_max16(m_lane);
+        if (g == 0) s_mx[wv * kHeads + hd] = mx;
         __syncthreads();
-#pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) m_ref[j] = fmaxf(m_ref[j], s_hs[(partner * kPairTokens + j) * kHeads + h]);
-        __syncthreads();  // every wave read the flag and the maxima
+        return true;
     }
 
     TRACE(4);
-    // per-head sums of each key half, then each wave stores its value-dim slice
-#pragma unroll
-    for (int j = 0; j < kPairTokens; ++j) {
-        const float lh = wave_sum16(l_run[j]);
-        if (g == 0) s_hs[(wv * kPairTokens + j) * kHeads + h] = lh;
+    // row sums of this wave's token
+    {
+        const float lt = wave_sum16(l_run);
+        if (g == 0) s_l[wv * kHeads + hd] = lt;
     }
     __syncthreads();
     TRACE(6);
-    auto row_sum = [&](int tb) {  // key half 0 + key half 1, in that order
-        const int w0 = 2 * (tb / kPairTokens), jj = tb % kPairTokens;
-        return s_hs[(w0 * kPairTokens + jj) * kHeads + h] + s_hs[((w0 + 1) * kPairTokens + jj) * kHeads + h];
-    };
+    // acc[tb][db] element i: value dim 64 wv + 16 db + 4 g + i of token tb, head hd
 #pragma unroll
-    for (int j = 0; j < kChunkBlockTokens; ++j) {
-        if (j >= nt) break;
-        const int row = it.row0 + it.i0 + j;
+    for (int tb = 0; tb < kCT; ++tb) {
+        if (tb >= nt) break;
+        const int row = it.row0 + it.i0 + tb;
         if (it.nks_eff == 1) {
-            const float inv = 1.f / row_sum(j);
+            const float inv = 1.f / s_l[tb * kHeads + hd];
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) store_out4(a, row, h, wv * 128 + mt * 16 + 4 * g, acc[j][mt] * inv);
+            for (int db = 0; db < 4; ++db) store_out4(a, row, hd, 64 * wv + 16 * db + 4 * g, acc[tb][db] * inv);
         } else {
-            const size_t prow = (size_t)item * kChunkBlockTokens + j;
-            float *po = a.ws_chunk_o + (prow * kHeads + h) * kDv;
+            const size_t prow = (size_t)item * kCT + tb;
+            float *po = a.ws_chunk_o + (prow * kHeads + hd) * kDv + 64 * wv + 4 * g;
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) *reinterpret_cast<f32x4 *>(po + wv * 128 + mt * 16 + 4 * g) = acc[j][mt];
+            for (int db = 0; db < 4; ++db) *reinterpret_cast<f32x4 *>(po + 16 * db) = acc[tb][db];
         }
     }
-    if (half == 0 && g == 0) {
-#pragma unroll
-        for (int j = 0; j < kPairTokens; ++j) {
-            const int tb = kPairTokens * pair + j;
-            if (tb >= nt) break;
-            const int row = it.row0 + it.i0 + tb;
-            const float l = row_sum(tb);
-            if (it.nks_eff == 1) {
-                if (a.lse) a.lse[(size_t)row * kHeads + h] = (m_ref[j] + log2f(l)) * kLn2;
-            } else {
-                const size_t prow = (size_t)item * kChunkBlockTokens + tb;
-                a.ws_chunk_ml[(prow * kHeads + h) * 2 + 0] = m_ref[j];
-                a.ws_chunk_ml[(prow * kHeads + h) * 2 + 1] = l;
-            }
+    if (g == 0 && wv < nt) {
+        const int row = it.row0 + it.i0 + wv;
+        const float l = s_l[wv * kHeads + hd];
+        if (it.nks_eff == 1) {
+            if (a.lse) a.lse[(size_t)row * kHeads + hd] = (m_ref + log2f(l)) * kLn2;
+        } else {
+            const size_t prow = (size_t)item * kCT + wv;
+            a.ws_chunk_ml[(prow * kHeads + hd) * 2 + 0] = m_ref;
+            a.ws_chunk_ml[(prow * kHeads + hd) * 2 + 1] = l;
         }
     }
     // fused append: split 0 of a block writes the block's own new latents
     // (nothing in this launch reads those slots, so it can come last)
     if (a.new_kv != nullptr && it.ks == 0) append_rows(a, r, it.p + it.i0, it.row0 + it.i0, it.i1 - it.i0);
     TRACE(5);
+    return false;
 }
 
 constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
@@ -1207,9 +1221,9 @@ constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
 // units, whose small size fills the tail.  An item's results and partial
 // slots depend only on its index, so the schedule never changes the output
 // bits.  The last workgroup to finish zeroes the counters for the next call.
-__global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) char smem[kMainLds];
-    __shared__ int s_tmp[12];
+    __shared__ int s_tmp[16];
     __shared__ int s_pages[kPageWindow];
     __shared__ DecSeg s_seg[kMaxSeg];
     __shared__ int s_item;
@@ -1220,8 +1234,13 @@ __global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
         const int item = s_item;
         if (item >= n_items) break;
         TRACE_ITEM(item);
-        if (item < a.n_chunk_items)
-            chunk_item(a, item, smem, s_tmp, s_pages);
+        if (item < a.n_chunk_items) {
+            // a second, exact pass only if the main one was abandoned
+            for (int pass = 0; pass < 2; ++pass) {
+                if (!chunk_item(a, item, smem, s_tmp, s_pages, pass != 0)) break;
+                __syncthreads();
+            }
+        }
         else
             decode_wg(a, item - a.n_chunk_items, smem, s_tmp, s_pages, s_seg);
         TRACE(7);
@@ -1240,7 +1259,7 @@ __global__ __launch_bounds__(kThreads, 1) void attention_kernel(AttnArgs a) {
 // partial visible): first merge_hsplit workgroups per request (decode rows
 // split across units), then one per (chunk item, block row).
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
-    __shared__ int s_tmp[12];
+    __shared__ int s_tmp[16];
     __shared__ DecSeg s_seg[kMaxSeg];
     const int b = blockIdx.x;
     const int n_dec = a.num_reqs * a.merge_hsplit;
@@ -1358,7 +1377,7 @@ hipError_t launch_append(const AppendArgs &a, hipStream_t s) {
 hipError_t launch_attention(const AttnArgs &a, hipStream_t s) {
     const int grid = a.grid;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL(attention_kernel, dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(attention_kernel, dim3(grid), dim3(kAttnThreads), 0, s, a);
     return hipGetLastError();
 }
 
