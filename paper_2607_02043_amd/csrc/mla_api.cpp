@@ -113,7 +113,7 @@ struct Plan {
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 // Per-CU costs (us, measured on MI355X) used only to size the work items.
-constexpr double kChunkTileUs = 1.5;   // one chunk tile: 8 tokens x 32 keys
+constexpr double kChunkTileUs = 2.3;   // one chunk tile: 8 tokens x 32 keys
 constexpr double kChunkItemUs = 13.0;  // chunk item: lookup, queries, ring fill; epilogue stores
 constexpr double kEmptyItemUs = 1.5;   // a chunk item past its block's causal limit
 constexpr double kDecTileUs = 2.1;     // one decode tile: 1 token x 32 keys

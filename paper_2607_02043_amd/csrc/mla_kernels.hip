@@ -847,8 +847,7 @@ __device__ void decode_merge(const AttnArgs &a, int r, int part, int *s_tmp) {
 // ------------------------------------------------------------- chunk path
 // Chunk rows: one workgroup of 8 wavefronts (two per SIMD) per block of 8
 // query tokens (128 rows of 16 heads) and a key range of ks_chunk keys;
-// 32-key tiles stream through a 3-slot global -> LDS DMA ring (all eight
-// wavefronts issue it).  Two
+// 32-key tiles stream through a 3-slot global -> LDS DMA ring.  Two
 // wavefronts per SIMD let one issue matrix work while the other waits on LDS
 // or runs its softmax.
 //  * Scores.  Wave w holds the query of token w (16 heads) over all 576
@@ -881,21 +880,24 @@ __device__ __forceinline__ uint32_t f16x2_bits(float a, float b) {
 
 constexpr int kCT = kChunkBlockTokens;                 // 8 tokens per item, one per wave
 constexpr int kQSteps = kDqk / 32;                     // 18 query operands of 32 dims
+constexpr int kQRegSteps = 16;                         // the first 16 stay in registers, the rope ones in LDS
 constexpr int kChunkRing = 3;
 constexpr int kPTile = kCT * 64 * 16;                  // fp16 P of one tile: [token][lane] 16 bytes
-constexpr int kChunkLds = kChunkRing * kChunkTileBytes + 2 * kPTile + 2 * kCT * kHeads * 4 + 16;
+constexpr int kQLdsBytes = (kQSteps - kQRegSteps) * kCT * 64 * 16;  // rope query operands: [step][token][lane]
+constexpr int kChunkLds = kChunkRing * kChunkTileBytes + 2 * kPTile + kQLdsBytes + 2 * kCT * kHeads * 4 + 16;
 // Largest exponent (log2 units) a probability may take against the reference
 // max: 2^15 stays inside fp16.
 constexpr float kMaxPExp = 15.f;
 
 // Chunk tiles are laid out chunk-major: 16-byte chunk c (8 latent dims) of
-// tile key k (0..31) sits at position 32 c + (k ^ 8 (c & 1)).  Sixteen
-// consecutive keys of one chunk are then 256 contiguous bytes (the K operand
-// reads), and the transposing value reads of 8 keys at two neighbouring
-// chunks fall into disjoint halves of the banks.  DMA round i (36 per tile,
-// 64 positions each) fills chunks 2 i and 2 i + 1: lane l loads chunk
-// 2 i + (l >> 5) of key (l & 31) ^ 8 (l >> 5), so one source address per lane
-// serves every round (+32 bytes per round).  Wave w issues rounds w, w + 8, ...
+// tile key k (0..31) sits at position 32 c + (k ^ 16 (c & 1)), i.e. the two
+// 16-key halves of every odd chunk are swapped.  Sixteen consecutive keys of
+// one chunk are then 256 contiguous bytes, and the K operand reads (four
+// neighbouring chunks at once) measured free of bank conflicts in this
+// arrangement.  DMA round i (36 per tile, 64 positions each) fills chunks 2 i
+// and 2 i + 1: lane l loads chunk 2 i + (l >> 5) of key (l & 31) ^ 16 (l >> 5),
+// so one source address per lane serves every round (+32 bytes per round).
+// Wave w issues rounds w, w + 8, ...
 constexpr int kChunkDmaRounds = kChunkTileBytes / 1024;  // 36
 
 // The instruction offset OFF moves the LDS destination as well as the
@@ -949,11 +951,18 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     // head hd, s = 0..17 (issued first: their latency overlaps the page-window
     // load).
     const int tk = min(wv, nt - 1);
-    u32x4 qreg[kQSteps];
+    u32x4 qreg[kQRegSteps];
+    char *const s_q = smem + kChunkRing * kChunkTileBytes + 2 * kPTile;  // rope query operands
     {
         const uint16_t *qp = a.q + ((size_t)(it.row0 + it.i0 + tk) * kHeads + hd) * kDqk + 8 * g;
 #pragma unroll
-        for (int s = 0; s < kQSteps; ++s) qreg[s] = *reinterpret_cast<const u32x4 *>(qp + 32 * s);
+        for (int s = 0; s < kQRegSteps; ++s) qreg[s] = *reinterpret_cast<const u32x4 *>(qp + 32 * s);
+        u32x4 qr[kQSteps - kQRegSteps];
+#pragma unroll
+        for (int s = kQRegSteps; s < kQSteps; ++s) qr[s - kQRegSteps] = *reinterpret_cast<const u32x4 *>(qp + 32 * s);
+#pragma unroll
+        for (int s = 0; s < kQSteps - kQRegSteps; ++s)
+            *reinterpret_cast<u32x4 *>(s_q + ((s * kCT + wv) * 64 + lane) * 16) = qr[s];
     }
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
     TRACE(2);
@@ -961,7 +970,7 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
 
     const uint32_t ring = lds_addr(smem);
     char *const s_pbuf = smem + kChunkRing * kChunkTileBytes;           // [2][token][lane] 16 bytes
-    float *const s_l = reinterpret_cast<float *>(s_pbuf + 2 * kPTile);  // [token][head] row sums
+    float *const s_l = reinterpret_cast<float *>(s_q + kQLdsBytes);     // [token][head] row sums
     float *const s_mx = s_l + kCT * kHeads;                            // [token][head] exact maxima
     int *const s_abort = reinterpret_cast<int *>(s_mx + kCT * kHeads);
 
@@ -970,38 +979,48 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int lim = __builtin_amdgcn_readfirstlane(min(it.p + it.i0 + tk, it.k1 - 1));
 
     // K operand of key block kb, step s (keys 16 kb + hd, dims 32 s + 8 g ..):
-    // chunk 4 s + g, so kq_off + 2048 s + 256 kb.
-    const int kq_off = g * 512 + (hd ^ (8 * (g & 1))) * 16;
+    // chunk 4 s + g, at kq_off[kb] + 2048 s.
+    int kq_off[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) kq_off[kb] = g * 512 + 256 * (kb ^ (g & 1)) + 16 * hd;
     // V^T operand of value block db (dims 64 wv + 16 db + (lane & 15)): two
-    // transposing reads of keys tr_key .. + 3 and tr_key + 16 .. + 3 at dims
-    // 64 wv + 16 db + 4 (lane & 3) .. + 3, i.e. chunk 8 wv + 2 db + ((lane >> 1) & 1):
-    // vt_off + 1024 db (+ 256 for the second read).
-    const int tr_key = 4 * g + ((lane & 15) >> 2);
-    const int vt_off = 4096 * wv + ((lane >> 1) & 1) * 512 + (tr_key ^ (8 * ((lane >> 1) & 1))) * 16 + (lane & 1) * 8;
+    // transposing reads of keys tr_key .. + 3 (e = 0) and tr_key + 16 .. + 3
+    // (e = 1) at dims 64 wv + 16 db + 4 (lane & 3) .. + 3, i.e. chunk
+    // 8 wv + 2 db + b with b = (lane >> 1) & 1: vt_off[e] + 1024 db.
+    const int tr_key = 4 * g + ((lane & 15) >> 2), tb_odd = (lane >> 1) & 1;
+    int vt_off[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+        vt_off[e] = 4096 * wv + 512 * tb_odd + 16 * tr_key + 256 * (e ^ tb_odd) + (lane & 1) * 8;
 
-    // DMA of tile t into its ring slot.  A full tile inside one page takes a
-    // uniform (scalar) base; any other tile (small pages, the last partial
-    // tile, new latents of a fused append) one address per lane.
-    const int dkey = (lane & 31) ^ (8 * (lane >> 5));           // this lane's key in every round
-    const uint32_t dvoff = dkey * kRowBytes + 16 * (lane >> 5) + 32 * wv;
+    // DMA of tile t into its ring slot, issued by waves 4..7 only (nine rounds
+    // each: round i = (wv - 4) + 4 j).  Issuing stalls a wave for a while; the
+    // other wave of the same SIMD meanwhile runs ahead on its matrix work, so
+    // the two wavefronts of a SIMD drift apart by about that much and the
+    // softmax of one overlaps the products of the other.  A full tile inside
+    // one page takes a uniform (scalar) base; any other tile (small pages, the
+    // last partial tile, new latents of a fused append) one address per lane.
+    const bool dma_wave = wv >= 4;
+    const int dw = wv & 3;
+    const int dkey = (lane & 31) ^ (16 * (lane >> 5));           // this lane's key in every round
+    const uint32_t dvoff = dkey * kRowBytes + 16 * (lane >> 5) + 32 * dw;
     const bool in_page = a.page_size >= kChunkKeys;
     const int cached_end = a.new_kv != nullptr ? min(it.k1, it.p) : it.k1;
     auto page_of = [&](int t) {
         return s_pages[min(((it.k0 + t * kChunkKeys) >> a.log2_page) - lp0, kPageWindow - 1)];
     };
     auto issue = [&](int t, int slot, int page) {
+        if (!dma_wave) return;
         const int kbase = it.k0 + t * kChunkKeys;
-        const uint32_t dst = ring + slot * kChunkTileBytes + wv * 1024;
-        const bool fifth = wv + 32 < kChunkDmaRounds;  // waves 0..3 issue a fifth round
+        const uint32_t dst = ring + slot * kChunkTileBytes + dw * 1024;
         if (in_page && kbase + kChunkKeys <= cached_end) {
             const char *src = reinterpret_cast<const char *>(a.kv) +
                               ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size +
                                (kbase & (a.page_size - 1))) * kRowBytes;
-            lds_dma16_sbase_imm<0>(src, dvoff, __builtin_amdgcn_readfirstlane(dst));
-            lds_dma16_sbase_imm<256>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 8 * 1024));
-            lds_dma16_sbase_imm<512>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 16 * 1024));
-            lds_dma16_sbase_imm<768>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 24 * 1024));
-            if (fifth) lds_dma16_sbase_imm<1024>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 32 * 1024));
+#define MLA_CHUNK_DMA_S(j) lds_dma16_sbase_imm<128 * (j)>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 4096 * (j)))
+            MLA_CHUNK_DMA_S(0); MLA_CHUNK_DMA_S(1); MLA_CHUNK_DMA_S(2); MLA_CHUNK_DMA_S(3); MLA_CHUNK_DMA_S(4);
+            MLA_CHUNK_DMA_S(5); MLA_CHUNK_DMA_S(6); MLA_CHUNK_DMA_S(7); MLA_CHUNK_DMA_S(8);
+#undef MLA_CHUNK_DMA_S
         } else {
             // keys past the item's range repeat its last key (a finite cached latent)
             const int key = min(kbase + dkey, it.k1 - 1);
@@ -1013,12 +1032,11 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
                 gs = reinterpret_cast<const char *>(a.kv) +
                      ((size_t)pg * a.page_size + (key & (a.page_size - 1))) * kRowBytes;
             }
-            gs += 16 * (lane >> 5) + 32 * wv;
-            lds_dma16_imm<0>(gs, __builtin_amdgcn_readfirstlane(dst));
-            lds_dma16_imm<256>(gs, __builtin_amdgcn_readfirstlane(dst + 8 * 1024));
-            lds_dma16_imm<512>(gs, __builtin_amdgcn_readfirstlane(dst + 16 * 1024));
-            lds_dma16_imm<768>(gs, __builtin_amdgcn_readfirstlane(dst + 24 * 1024));
-            if (fifth) lds_dma16_imm<1024>(gs, __builtin_amdgcn_readfirstlane(dst + 32 * 1024));
+            gs += 16 * (lane >> 5) + 32 * dw;
+#define MLA_CHUNK_DMA_V(j) lds_dma16_imm<128 * (j)>(gs, __builtin_amdgcn_readfirstlane(dst + 4096 * (j)))
+            MLA_CHUNK_DMA_V(0); MLA_CHUNK_DMA_V(1); MLA_CHUNK_DMA_V(2); MLA_CHUNK_DMA_V(3); MLA_CHUNK_DMA_V(4);
+            MLA_CHUNK_DMA_V(5); MLA_CHUNK_DMA_V(6); MLA_CHUNK_DMA_V(7); MLA_CHUNK_DMA_V(8);
+#undef MLA_CHUNK_DMA_V
         }
     };
 
@@ -1029,25 +1047,30 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     // S^T of tile t for this wave's token: lane l, element i of block kb =
     // key 16 kb + 4 g + i of the tile, head hd.  Two accumulation chains.
     auto scores = [&](int slot, f32x4 (&s)[2]) {
-        const char *tile = smem + __builtin_amdgcn_readfirstlane(slot * kChunkTileBytes) + kq_off;
+        const char *tile = smem + __builtin_amdgcn_readfirstlane(slot * kChunkTileBytes);
         s[0] = s[1] = f32x4{0.f, 0.f, 0.f, 0.f};
-        constexpr int D = 1;  // steps whose K operands are in flight
+        constexpr int D = 2;  // steps whose K operands are in flight
         u32x4 av[D][2];
 #pragma unroll
         for (int st = 0; st < D; ++st)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
-                av[st][kb] = *reinterpret_cast<const u32x4 *>(tile + 2048 * st + 256 * kb);
+                av[st][kb] = *reinterpret_cast<const u32x4 *>(tile + kq_off[kb] + 2048 * st);
 #pragma unroll
         for (int st = 0; st < kQSteps; ++st) {
             u32x4 cur[2] = {av[st % D][0], av[st % D][1]};
             if (st + D < kQSteps) {
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
-                    av[st % D][kb] = *reinterpret_cast<const u32x4 *>(tile + 2048 * (st + D) + 256 * kb);
+                    av[st % D][kb] = *reinterpret_cast<const u32x4 *>(tile + kq_off[kb] + 2048 * (st + D));
             }
-            s[0] = mfma_bf16(cur[0], qreg[st], s[0]);
-            s[1] = mfma_bf16(cur[1], qreg[st], s[1]);
+            u32x4 qb;
+            if (st < kQRegSteps)
+                qb = qreg[st];
+            else
+                qb = *reinterpret_cast<const u32x4 *>(s_q + (((st - kQRegSteps) * kCT + wv) * 64 + lane) * 16);
+            s[0] = mfma_bf16(cur[0], qb, s[0]);
+            s[1] = mfma_bf16(cur[1], qb, s[1]);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -1088,24 +1111,27 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     };
     // O^T += V^T P^T for tile t (P from buffer t & 1)
     auto pv = [&](int slot, int pbuf) {
-        const char *tile = smem + __builtin_amdgcn_readfirstlane(slot * kChunkTileBytes) + vt_off;
+        const char *tile = smem + __builtin_amdgcn_readfirstlane(slot * kChunkTileBytes);
         const char *pb = s_pbuf + __builtin_amdgcn_readfirstlane(pbuf * kPTile) + lane * 16;
+        constexpr int PD = 3;  // P operands in flight
+        u32x4 bp[PD];
+#pragma unroll
+        for (int tb = 0; tb < PD; ++tb) bp[tb] = *reinterpret_cast<const u32x4 *>(pb + tb * 64 * 16);
         u32x4 av[4];
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-            const char *vb = tile + 1024 * db;
-            const u32x2 lo = lds_read_tr16(vb);
-            const u32x2 hi = lds_read_tr16(vb + 256);
+            const u32x2 lo = lds_read_tr16(tile + vt_off[0] + 1024 * db);
+            const u32x2 hi = lds_read_tr16(tile + vt_off[1] + 1024 * db);
             av[db] = u32x4{bf16x2_to_f16x2(lo[0]), bf16x2_to_f16x2(lo[1]), bf16x2_to_f16x2(hi[0]),
                            bf16x2_to_f16x2(hi[1])};
         }
-        u32x4 bp[2];
-        bp[0] = *reinterpret_cast<const u32x4 *>(pb);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int tb = 0; tb < kCT; ++tb) {  // P of token tb + 1 is read one token ahead
-            if (tb + 1 < kCT) bp[(tb + 1) & 1] = *reinterpret_cast<const u32x4 *>(pb + (tb + 1) * 64 * 16);
+        for (int tb = 0; tb < kCT; ++tb) {
+            const u32x4 cur = bp[tb % PD];
+            if (tb + PD < kCT) bp[tb % PD] = *reinterpret_cast<const u32x4 *>(pb + (tb + PD) * 64 * 16);
 #pragma unroll
-            for (int db = 0; db < 4; ++db) acc[tb][db] = mfma_f16(av[db], bp[tb & 1], acc[tb][db]);
+            for (int db = 0; db < 4; ++db) acc[tb][db] = mfma_f16(av[db], cur, acc[tb][db]);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -1116,13 +1142,11 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     if (tid == 0) *s_abort = 0;
     __syncthreads();  // page window and abort flag ready; the ring is idle
     for (int t = 0; t < 2 && t < ntiles; ++t) issue(t, t, page_of(t));
-    // queries and tile 0 landed (tile 1 may still be in flight: 5 or 4 rounds)
-    if (ntiles == 1)
+    // queries and tile 0 landed (tile 1's nine rounds may still be in flight)
+    if (ntiles == 1 || !dma_wave)
         wait_dma_all();
-    else if (wv + 32 < kChunkDmaRounds)
-        asm volatile("s_waitcnt vmcnt(5)" ::: "memory");
     else
-        asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+        wait_dma_keep9();
     __syncthreads();
 #pragma unroll
     for (int tb = 0; tb < kCT; ++tb)
@@ -1154,7 +1178,9 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         const int slot1 = slot == kChunkRing - 1 ? 0 : slot + 1;
         const int slot2 = slot1 == kChunkRing - 1 ? 0 : slot1 + 1;
         if (t + 2 < ntiles) issue(t + 2, slot2, next_page);
+        TRACE_TILE(t, 14);
         pv(slot, t & 1);
+        TRACE_TILE(t, 15);
         if (t + 1 < ntiles) {
             f32x4 s1[2];
             scores(slot1, s1);
