@@ -232,7 +232,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
     // Finishing time of the decode units (equal cost u) poured onto the loads
     // left by the chunk items, plus the merge of the requests they split.
     auto with_decode = [&](const std::vector<double> &loads, long long U) {
-        const long long n = ceil_div_ll(dec_total, U);
+        const long long n = ceil_div_ll(ceil_div_ll(dec_total, U), 2);  // work items: pairs of units
         const double u = kDecUnitUs + kDecTileUs * (double)U;
         long long split_parts = 0;
         for (const DecReq &d : dec) {
@@ -292,7 +292,8 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
                     est = 1e300;
                     for (long long U : units) {
                         const double u = kDecUnitUs + kDecTileUs * (double)U;
-                        est = std::min(est, std::max(mx, (sum + (double)ceil_div_ll(dec_total, U) * u) / G));
+                        est = std::min(est, std::max(mx, (sum + (double)ceil_div_ll(ceil_div_ll(dec_total, U), 2) * u) /
+                                                                 G));
                     }
                 }
                 cd.est = est + cd.merge_us;
@@ -332,10 +333,10 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
     if (nci > (1LL << 27)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
     pl->ks_chunk = (int)ks_best;
     pl->n_chunk_items = (int)nci;
-    pl->n_dec_units = (int)n_units;
+    pl->n_dec_units = (int)ceil_div_ll(n_units, 2);  // a work item is a pair of units, one per wave group
     pl->dec_unit_tiles = (int)U;
     pl->dec_total_tiles = (int)dec_total;
-    pl->grid = (int)std::min<long long>(G, nci + n_units);
+    pl->grid = (int)std::min<long long>(G, nci + pl->n_dec_units);
     long long max_parts = 1;
     for (const DecReq &d : dec) {
         const long long parts = (d.first_tile + d.tiles - 1) / U - d.first_tile / U + 1;

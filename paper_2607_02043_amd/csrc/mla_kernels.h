@@ -32,8 +32,8 @@ struct AttnArgs {
     float *lse;
     float *ws_chunk_o;    // [n_chunk_items][block tokens][16][512]
     float *ws_chunk_ml;   // [n_chunk_items][block tokens][16][2]
-    float *ws_dec_o;      // [2 n_dec_units][16][512]: first / last segment of each decode unit
-    float *ws_dec_ml;     // [2 n_dec_units][16][2]
+    float *ws_dec_o;      // [2 units][16][512]: first / last segment of each decode unit
+    float *ws_dec_ml;     // [2 units][16][2]
     int32_t *work;        // [2]: next work item, workgroups done; zero between calls
     int32_t num_reqs;
     int32_t num_rows;
@@ -44,7 +44,8 @@ struct AttnArgs {
     float scale_log2;     // softmax scale * log2(e)
     int32_t ks_chunk;          // keys per chunk work item (a multiple of 64)
     int32_t n_chunk_items;     // work items 0 .. n_chunk_items - 1
-    int32_t n_dec_units;       // then the decode units: slices of the flattened decode tile list
+    int32_t n_dec_units;       // then the decode items: pairs of units (slices of the flattened decode
+                               // tile list), one unit per wave group
     int32_t dec_unit_tiles;    // 32-key decode tiles per unit
     int32_t dec_total_tiles;
     int32_t grid;              // persistent workgroups of the attention launch

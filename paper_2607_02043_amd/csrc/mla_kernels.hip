@@ -39,8 +39,10 @@ constexpr int kChunksPerRow = kRowBytes / 16;  // 72 16-byte chunks per latent
 // decode path
 constexpr int kDecKeys = kKeysPerTile;  // 32
 constexpr int kDecTileBytes = kDecKeys * kRowBytes;  // 36864
-constexpr int kDecRing = 4;
-constexpr int kDecLds = kDecRing * kDecTileBytes + 4 * kHeads * 20 * 4;  // ring + partial score blocks
+constexpr int kDecRing = 2;                                   // ring slots of each decode wave group
+constexpr int kDecGroupBytes = kDecRing * kDecTileBytes;
+constexpr int kDecXBytes = 4 * kHeads * 20 * 4;               // partial score blocks of a group
+constexpr int kDecLds = 2 * kDecGroupBytes + 2 * kDecXBytes;  // two groups: rings, then score blocks
 // chunk path
 constexpr int kChunkKeys = kKeysPerTile;  // 32
 constexpr int kChunkTileBytes = kChunkKeys * kRowBytes;  // 36864
@@ -356,6 +358,21 @@ __device__ __forceinline__ void append_rows(const AttnArgs &a, int r, int key0, 
     }
 }
 
+// The same for one 256-thread group of a larger workgroup (gtid = thread index in it).
+__device__ __forceinline__ void append_rows_group(const AttnArgs &a, int r, int key0, int row0, int n, int gtid) {
+    const int32_t *btr = a.bt + (size_t)r * a.max_pages;
+    for (int x = gtid; x < n * kChunksPerRow; x += kThreads) {
+        const int i = x / kChunksPerRow, c = x - i * kChunksPerRow;
+        const int key = key0 + i;
+        const int lp = key >> a.log2_page;
+        const int page = lp < a.max_pages ? btr[lp] : -1;
+        if ((unsigned)page >= (unsigned)a.num_pages) continue;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(a.new_kv + (size_t)(row0 + i) * kDqk + c * 8);
+        *reinterpret_cast<u32x4 *>(a.kv_out + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kDqk +
+                                   c * 8) = v;
+    }
+}
+
 // Scores of 16 keys (tile rows key_base .. key_base + 15) against one token's
 // query operand: lane l gets S[key_base + 4 (l/16) + i][head l%16], i = 0..3.
 // Reads are staged 6 steps at a time; two accumulation chains.
@@ -600,20 +617,50 @@ __device__ __forceinline__ void wait_units_newer(int n) {  // n of the later uni
         asm volatile("s_waitcnt vmcnt(18)" ::: "memory");
 }
 
-__device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int *s_pages, DecSeg *s_seg) {
+// Barrier of the four wavefronts of one wave group, through an arrival
+// counter in LDS; epoch (wave-uniform) counts the group's barriers so far.
+// Each wave first waits for its own LDS accesses, so what it wrote before the
+// barrier is visible to the group after it.  The wait is bounded (far beyond
+// any real skew), so a broken count can only give wrong results, not a hang.
+__device__ __forceinline__ void group_barrier(int *ctr, int &epoch) {
+    ++epoch;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const int target = 4 * epoch;
+    for (int spin = 0; spin < (1 << 16); ++spin) {
+        const int seen = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
+        if (seen >= target) break;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    asm volatile("" ::: "memory");
+}
+
+__device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int (*s_pages_g)[kPageWindow],
+                          DecSeg (*s_seg_g)[kMaxSeg], int *s_gbar) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = wv >> 2, gw = wv & 3, gtid = tid & 255;  // wave group, wave and thread inside it
     const int g = lane >> 4, h = lane & 15;
-    // waves 0..3 stream and compute; any further waves of the workgroup only
-    // take part in its barriers
-    const bool active = wv < 4;
-    const int R0 = w * a.dec_unit_tiles;
-    const int R1 = min(R0 + a.dec_unit_tiles, a.dec_total_tiles);
-    if (R0 >= R1) return;
-    const int nseg = find_segments(a, R0, R1, s_seg, s_tmp);
+    const int S = a.dec_unit_tiles;
+    // Item w is the pair of decode units 2 w and 2 w + 1 (S tiles each), one per
+    // wave group.  Both groups find their segments (block-wide scans).
+    int nseg2[2], nunits2[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int R0 = (2 * w + q) * S;
+        const int R1 = min(R0 + S, a.dec_total_tiles);
+        nseg2[q] = R0 < R1 ? find_segments(a, R0, R1, s_seg_g[q], s_tmp) : 0;
+        nunits2[q] = nseg2[q] > 0 ? nseg2[q] + (R1 - R0) : 0;
+    }
     TRACE(1);
-    if (nseg == 0) return;
-    if (tid == 0) {  // page-window offsets of the segments
+    const int n_iter = max(nunits2[0], nunits2[1]);
+    if (n_iter == 0) return;  // both groups idle (uniform)
+    const int v = 2 * w + grp;  // this group's unit
+    const int R0 = v * S;
+    const int nseg = nseg2[grp], n_units = nunits2[grp];
+    DecSeg *const s_seg = s_seg_g[grp];
+    int *const s_pages = s_pages_g[grp];
+    if (gtid == 0) {  // page-window offsets of the segments
         int pw = 0;
         for (int j = 0; j < nseg; ++j) {
             const DecSeg sg = s_seg[j];
@@ -630,88 +677,87 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
         const int klast = min(sg.t1 * kDecKeys, sg.p + 1) - 1;
         const int n = (klast >> a.log2_page) - sg.lp0 + 1;
         const int32_t *btr = a.bt + (size_t)sg.r * a.max_pages;
-        for (int i = tid; i < n && sg.pw + i < kPageWindow; i += blockDim.x) {
+        for (int i = gtid; i < n && sg.pw + i < kPageWindow; i += kThreads) {
             const int lp = sg.lp0 + i;
             const int pg = lp < a.max_pages ? btr[lp] : 0;
             s_pages[sg.pw + i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
         }
     }
-    if (a.new_kv != nullptr) {  // fused append: the workgroup holding a request's last tile writes its latent
+    if (a.new_kv != nullptr) {  // fused append: the group holding a request's last tile writes its latent
         for (int j = 0; j < nseg; ++j) {
             const DecSeg sg = s_seg[j];
-            if (sg.t1 == dec_tiles(sg.p, 1)) append_rows(a, sg.r, sg.p, sg.row, 1);
+            if (sg.t1 == dec_tiles(sg.p, 1)) append_rows_group(a, sg.r, sg.p, sg.row, 1, gtid);
         }
     }
+    if (tid < 2) s_gbar[tid] = 0;
     __syncthreads();
+    if (n_units == 0) return;  // this group has no unit (the other one may)
+    int epoch = 0;
+    int *const gbar = s_gbar + grp;
     TRACE(2);
-
-    const int n_units = nseg + (R1 - R0);
     TRACE_VAL(8, 1000000ull * 2 + n_units);
-    uint32_t dma_off[(kTileDma + 1) / 2];
-    tile_dma_offsets<false>(wv, lane, dma_off);
-    const uint32_t ring = lds_addr(smem);
-    float *s_X = reinterpret_cast<float *>(smem + kDecRing * kDecTileBytes);
-    Cursor prod{0, -1}, cons{0, -1};
-    for (int u = 0; u < kDecRing - 1 && u < n_units; ++u) {
-        if (active) issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + u * kDecTileBytes, wv, lane, dma_off);
-        advance(prod, s_seg);
-    }
 
-    u32x4 qreg[9];  // this wave's half of the query operand: steps 9 (wv >> 1) .. + 9
+    uint32_t dma_off[(kTileDma + 1) / 2];
+    tile_dma_offsets<false>(gw, lane, dma_off);
+    const uint32_t ring = lds_addr(smem) + grp * kDecGroupBytes;
+    float *s_X = reinterpret_cast<float *>(smem + 2 * kDecGroupBytes + grp * kDecXBytes);
+    Cursor prod{0, -1}, cons{0, -1};
+    issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring, gw, lane, dma_off);
+    advance(prod, s_seg);
+
+    u32x4 qreg[9];  // this wave's half of the query operand: steps 9 (gw >> 1) .. + 9
     f32x4 acc[8];
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_ref = kNegInf, l_run = 0.f;
-    const int hf = wv >> 1;
-    const int kq = 16 * (wv & 1) + (lane & 15);             // key this lane scores
+    const int hf = gw >> 1;
+    const int kq = 16 * (gw & 1) + (lane & 15);             // key this lane scores
     const int tr_key = 4 * g + ((lane & 15) >> 2);          // transposing-read source row
-    const int tr_dv = wv * 128 + 4 * (lane & 3);            // and its first value dim
+    const int tr_dv = gw * 128 + 4 * (lane & 3);            // and its first value dim
 
     TRACE(3);
+    // The two groups run independently, each with barriers of its own four
+    // wavefronts (two per unit).
     for (int u = 0; u < n_units; ++u) {
         TRACE_TILE(u, 10);
-        wait_units_newer(min(kDecRing - 2, n_units - 1 - u));
-        __syncthreads();
-        if (prod.j < nseg) {
-            if (active)
-                issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + ((u + kDecRing - 1) % kDecRing) * kDecTileBytes,
-                           wv, lane, dma_off);
-            advance(prod, s_seg);
-        }
-        const char *slot = smem + (u % kDecRing) * kDecTileBytes;
-        const DecSeg sg = s_seg[cons.j];
-        if (cons.t < 0) {  // a new request: its query block
-            if (active) {
+        wait_dma_all();                // unit u (the only one in flight)
+        group_barrier(gbar, epoch);    // unit u landed; slot (u + 1) % 2 is free
+        bool tile_unit = false;
+        DecSeg sg{};
+        const char *slot = smem + grp * kDecGroupBytes + (u % kDecRing) * kDecTileBytes;
+        {
+            if (prod.j < nseg) {
+                issue_unit(a, s_seg[prod.j], prod.t, s_pages, ring + ((u + 1) % kDecRing) * kDecTileBytes, gw, lane,
+                           dma_off);
+                advance(prod, s_seg);
+            }
+            sg = s_seg[cons.j];
+            if (cons.t < 0) {  // a new request: its query block
 #pragma unroll
                 for (int s2 = 0; s2 < 9; ++s2)
                     qreg[s2] = *reinterpret_cast<const u32x4 *>(slot + (h * kChunksPerRow + (9 * hf + s2) * 4 + g) * 16);
-            }
-            advance(cons, s_seg);
-            continue;
-        }
-        if (!active) {  // the partial-score barrier, then the next unit
-            __syncthreads();
-            advance(cons, s_seg);
-            continue;
-        }
-        TRACE_TILE(u, 11);
-        const int kbase = cons.t * kDecKeys;
-        // partial scores: keys 16 (wv & 1) .. + 16, dims of steps 9 hf .. 9 hf + 8
-        f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-        {
-            u32x4 av[9];
+                advance(cons, s_seg);
+            } else {
+                tile_unit = true;
+                TRACE_TILE(u, 11);
+                // partial scores: keys 16 (gw & 1) .. + 16, dims of steps 9 hf .. 9 hf + 8
+                f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+                u32x4 av[9];
 #pragma unroll
-            for (int s2 = 0; s2 < 9; ++s2)
-                av[s2] = *reinterpret_cast<const u32x4 *>(slot + tile_off(kq, (9 * hf + s2) * 4 + g));
+                for (int s2 = 0; s2 < 9; ++s2)
+                    av[s2] = *reinterpret_cast<const u32x4 *>(slot + tile_off(kq, (9 * hf + s2) * 4 + g));
 #pragma unroll
-            for (int s2 = 0; s2 < 9; s2 += 2) {
-                sa = mfma_bf16(av[s2], qreg[s2], sa);
-                if (s2 + 1 < 9) sb = mfma_bf16(av[s2 + 1], qreg[s2 + 1], sb);
+                for (int s2 = 0; s2 < 9; s2 += 2) {
+                    sa = mfma_bf16(av[s2], qreg[s2], sa);
+                    if (s2 + 1 < 9) sb = mfma_bf16(av[s2 + 1], qreg[s2 + 1], sb);
+                }
+                *reinterpret_cast<f32x4 *>(s_X + (gw * kHeads + h) * kXStride + 4 * g) = sa + sb;
             }
         }
-        *reinterpret_cast<f32x4 *>(s_X + (wv * kHeads + h) * kXStride + 4 * g) = sa + sb;
-        __syncthreads();
+        if (!tile_unit) continue;
+        group_barrier(gbar, epoch);  // partial score blocks complete
         TRACE_TILE(u, 12);
+        const int kbase = cons.t * kDecKeys;
         // full scores of this lane's head: x[kt][i] = key 16 kt + 4 g + i (kt = 0, 1)
         f32x4 x[2];
 #pragma unroll
@@ -730,8 +776,8 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
             }
         }
         mt = wave_max16(mt);
-        // Lazy rescale (the same decision in every wave): keep the reference max
-        // unless the tile max exceeds it by more than 2^8.
+        // Lazy rescale (the same decision in every wave of the group): keep the
+        // reference max unless the tile max exceeds it by more than 2^8.
         if (__builtin_amdgcn_ballot_w64(mt > m_ref + 8.f) != 0) {
             const float m_new = fmaxf(m_ref, mt);
             const float alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
@@ -784,15 +830,15 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
                 const float inv = 1.f / l_tot;
 #pragma unroll
                 for (int mt2 = 0; mt2 < 8; ++mt2)
-                    store_out4(a, sg.row, h, wv * 128 + mt2 * 16 + 4 * g, acc[mt2] * inv);
-                if (a.lse && wv == 0 && g == 0) a.lse[(size_t)sg.row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
+                    store_out4(a, sg.row, h, gw * 128 + mt2 * 16 + 4 * g, acc[mt2] * inv);
+                if (a.lse && gw == 0 && g == 0) a.lse[(size_t)sg.row * kHeads + h] = (m_ref + log2f(l_tot)) * kLn2;
             } else if (a.ws_dec_o != nullptr) {
-                const size_t slot_id = 2 * (size_t)w + (jseg == 0 ? 0 : 1);
+                const size_t slot_id = 2 * (size_t)v + (jseg == 0 ? 0 : 1);
                 float *po = a.ws_dec_o + (slot_id * kHeads + h) * kDv;
 #pragma unroll
                 for (int mt2 = 0; mt2 < 8; ++mt2)
-                    *reinterpret_cast<f32x4 *>(po + wv * 128 + mt2 * 16 + 4 * g) = acc[mt2];
-                if (wv == 0 && g == 0) {
+                    *reinterpret_cast<f32x4 *>(po + gw * 128 + mt2 * 16 + 4 * g) = acc[mt2];
+                if (gw == 0 && g == 0) {
                     a.ws_dec_ml[(slot_id * kHeads + h) * 2 + 0] = m_ref;
                     a.ws_dec_ml[(slot_id * kHeads + h) * 2 + 1] = l_tot;
                 }
@@ -803,6 +849,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
             l_run = 0.f;
         }
     }
+    (void)R0;
     TRACE(4);
 }
 
@@ -898,7 +945,6 @@ constexpr float kMaxPExp = 15.f;
 // and 2 i + 1: lane l loads chunk 2 i + (l >> 5) of key (l & 31) ^ 16 (l >> 5),
 // so one source address per lane serves every round (+32 bytes per round).
 // Wave w issues rounds w, w + 8, ...
-constexpr int kChunkDmaRounds = kChunkTileBytes / 1024;  // 36
 
 // The instruction offset OFF moves the LDS destination as well as the
 // global source, so M0 is set to lds_base - OFF.
@@ -1250,8 +1296,9 @@ constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
 __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) char smem[kMainLds];
     __shared__ int s_tmp[16];
-    __shared__ int s_pages[kPageWindow];
-    __shared__ DecSeg s_seg[kMaxSeg];
+    __shared__ int s_pages[2][kPageWindow];  // chunk items use the first window
+    __shared__ DecSeg s_seg[2][kMaxSeg];
+    __shared__ int s_gbar[2];
     __shared__ int s_item;
     const int n_items = a.n_chunk_items + a.n_dec_units;
     for (;;) {
@@ -1263,12 +1310,12 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) 
         if (item < a.n_chunk_items) {
             // a second, exact pass only if the main one was abandoned
             for (int pass = 0; pass < 2; ++pass) {
-                if (!chunk_item(a, item, smem, s_tmp, s_pages, pass != 0)) break;
+                if (!chunk_item(a, item, smem, s_tmp, s_pages[0], pass != 0)) break;
                 __syncthreads();
             }
         }
         else
-            decode_wg(a, item - a.n_chunk_items, smem, s_tmp, s_pages, s_seg);
+            decode_wg(a, item - a.n_chunk_items, smem, s_tmp, s_pages, s_seg, s_gbar);
         TRACE(7);
         __syncthreads();  // LDS (and s_item) free for the next item
     }
@@ -1286,7 +1333,6 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) 
 // split across units), then one per (chunk item, block row).
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     __shared__ int s_tmp[16];
-    __shared__ DecSeg s_seg[kMaxSeg];
     const int b = blockIdx.x;
     const int n_dec = a.num_reqs * a.merge_hsplit;
     if (b < n_dec) {
