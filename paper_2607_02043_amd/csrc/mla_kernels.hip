@@ -936,16 +936,15 @@ constexpr int kChunkLds = kChunkRing * kChunkTileBytes + 2 * kPTile + kQLdsBytes
 // max: 2^15 stays inside fp16.
 constexpr float kMaxPExp = 15.f;
 
-// Chunk tiles are laid out chunk-major: 16-byte chunk c (8 latent dims) of
-// tile key k (0..31) sits at position 32 c + (k ^ 16 (c & 1)), i.e. the two
-// 16-key halves of every odd chunk are swapped.  Sixteen consecutive keys of
-// one chunk are then 256 contiguous bytes, and the K operand reads (four
-// neighbouring chunks at once) measured free of bank conflicts in this
-// arrangement.  DMA round i (36 per tile, 64 positions each) fills chunks 2 i
-// and 2 i + 1: lane l loads chunk 2 i + (l >> 5) of key (l & 31) ^ 16 (l >> 5),
-// so one source address per lane serves every round (+32 bytes per round).
-// Wave w issues rounds w, w + 8, ...
-
+// Chunk tiles are laid out by octets of chunks: 16-byte chunk c (8 latent
+// dims) of tile key k (0..31) sits at position 256 (c >> 3) + 8 k +
+// ((c & 7) ^ (k & 7)), i.e. the eight chunks (128 bytes) of a key that share
+// an octet stay together, xor-swizzled with the key's low three bits.  One
+// DMA round (64 positions) then reads eight keys' 128-byte pieces, one cache
+// line per key, and the 16-key operand reads keep the bank pattern of a
+// row-major tile (conflict-free).  Round j fills octet j >> 2, keys
+// 8 (j & 3) .. + 7: lane l loads chunk 8 (j >> 2) + ((l & 7) ^ ((l >> 3) & 7))
+// of key 8 (j & 3) + (l >> 3).
 // The instruction offset OFF moves the LDS destination as well as the
 // global source, so M0 is set to lds_base - OFF.
 template <int OFF>
@@ -1025,19 +1024,19 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     const int lim = __builtin_amdgcn_readfirstlane(min(it.p + it.i0 + tk, it.k1 - 1));
 
     // K operand of key block kb, step s (keys 16 kb + hd, dims 32 s + 8 g ..):
-    // chunk 4 s + g, at kq_off[kb] + 2048 s.
+    // chunk 4 s + g, at kq_off[s & 1] + 2048 kb + 4096 (s >> 1).
     int kq_off[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) kq_off[kb] = g * 512 + 256 * (kb ^ (g & 1)) + 16 * hd;
+    for (int e = 0; e < 2; ++e) kq_off[e] = 128 * hd + 16 * ((4 * e + g) ^ (hd & 7));
     // V^T operand of value block db (dims 64 wv + 16 db + (lane & 15)): two
-    // transposing reads of keys tr_key .. + 3 (e = 0) and tr_key + 16 .. + 3
-    // (e = 1) at dims 64 wv + 16 db + 4 (lane & 3) .. + 3, i.e. chunk
-    // 8 wv + 2 db + b with b = (lane >> 1) & 1: vt_off[e] + 1024 db.
-    const int tr_key = 4 * g + ((lane & 15) >> 2), tb_odd = (lane >> 1) & 1;
-    int vt_off[2];
+    // transposing reads of keys tr_key .. + 3 and tr_key + 16 .. + 3 at dims
+    // 64 wv + 16 db + 4 (lane & 3) .. + 3, i.e. chunk 8 wv + 2 db + b with
+    // b = (lane >> 1) & 1: vt_off[db] (+ 2048 for the second read).
+    const int tr_key = 4 * g + ((lane & 15) >> 2);
+    int vt_off[4];
 #pragma unroll
-    for (int e = 0; e < 2; ++e)
-        vt_off[e] = 4096 * wv + 512 * tb_odd + 16 * tr_key + 256 * (e ^ tb_odd) + (lane & 1) * 8;
+    for (int db = 0; db < 4; ++db)
+        vt_off[db] = 4096 * wv + 128 * tr_key + 16 * ((2 * db + ((lane >> 1) & 1)) ^ (tr_key & 7)) + 8 * (lane & 1);
 
     // DMA of tile t into its ring slot, issued by waves 4..7 only (nine rounds
     // each: round i = (wv - 4) + 4 j).  Issuing stalls a wave for a while; the
@@ -1048,8 +1047,8 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     // last partial tile, new latents of a fused append) one address per lane.
     const bool dma_wave = wv >= 4;
     const int dw = wv & 3;
-    const int dkey = (lane & 31) ^ (16 * (lane >> 5));           // this lane's key in every round
-    const uint32_t dvoff = dkey * kRowBytes + 16 * (lane >> 5) + 32 * dw;
+    const int dkey = 8 * dw + (lane >> 3);  // this lane's key in every round of this wave
+    const uint32_t dvoff = dkey * kRowBytes + 16 * ((lane & 7) ^ ((lane >> 3) & 7));
     const bool in_page = a.page_size >= kChunkKeys;
     const int cached_end = a.new_kv != nullptr ? min(it.k1, it.p) : it.k1;
     auto page_of = [&](int t) {
@@ -1058,12 +1057,12 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     auto issue = [&](int t, int slot, int page) {
         if (!dma_wave) return;
         const int kbase = it.k0 + t * kChunkKeys;
-        const uint32_t dst = ring + slot * kChunkTileBytes + dw * 1024;
+        const uint32_t dst = ring + slot * kChunkTileBytes + dw * 1024;  // round r = dw + 4 r'
         if (in_page && kbase + kChunkKeys <= cached_end) {
             const char *src = reinterpret_cast<const char *>(a.kv) +
                               ((size_t)__builtin_amdgcn_readfirstlane(page) * a.page_size +
                                (kbase & (a.page_size - 1))) * kRowBytes;
-#define MLA_CHUNK_DMA_S(j) lds_dma16_sbase_imm<128 * (j)>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 4096 * (j)))
+#define MLA_CHUNK_DMA_S(r) lds_dma16_sbase_imm<128 * (r)>(src, dvoff, __builtin_amdgcn_readfirstlane(dst + 4096 * (r)))
             MLA_CHUNK_DMA_S(0); MLA_CHUNK_DMA_S(1); MLA_CHUNK_DMA_S(2); MLA_CHUNK_DMA_S(3); MLA_CHUNK_DMA_S(4);
             MLA_CHUNK_DMA_S(5); MLA_CHUNK_DMA_S(6); MLA_CHUNK_DMA_S(7); MLA_CHUNK_DMA_S(8);
 #undef MLA_CHUNK_DMA_S
@@ -1078,8 +1077,8 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
                 gs = reinterpret_cast<const char *>(a.kv) +
                      ((size_t)pg * a.page_size + (key & (a.page_size - 1))) * kRowBytes;
             }
-            gs += 16 * (lane >> 5) + 32 * dw;
-#define MLA_CHUNK_DMA_V(j) lds_dma16_imm<128 * (j)>(gs, __builtin_amdgcn_readfirstlane(dst + 4096 * (j)))
+            gs += 16 * ((lane & 7) ^ ((lane >> 3) & 7));
+#define MLA_CHUNK_DMA_V(r) lds_dma16_imm<128 * (r)>(gs, __builtin_amdgcn_readfirstlane(dst + 4096 * (r)))
             MLA_CHUNK_DMA_V(0); MLA_CHUNK_DMA_V(1); MLA_CHUNK_DMA_V(2); MLA_CHUNK_DMA_V(3); MLA_CHUNK_DMA_V(4);
             MLA_CHUNK_DMA_V(5); MLA_CHUNK_DMA_V(6); MLA_CHUNK_DMA_V(7); MLA_CHUNK_DMA_V(8);
 #undef MLA_CHUNK_DMA_V
@@ -1101,14 +1100,15 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         for (int st = 0; st < D; ++st)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
-                av[st][kb] = *reinterpret_cast<const u32x4 *>(tile + kq_off[kb] + 2048 * st);
+                av[st][kb] = *reinterpret_cast<const u32x4 *>(tile + kq_off[st & 1] + 2048 * kb + 4096 * (st >> 1));
 #pragma unroll
         for (int st = 0; st < kQSteps; ++st) {
             u32x4 cur[2] = {av[st % D][0], av[st % D][1]};
             if (st + D < kQSteps) {
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
-                    av[st % D][kb] = *reinterpret_cast<const u32x4 *>(tile + kq_off[kb] + 2048 * (st + D));
+                    av[st % D][kb] = *reinterpret_cast<const u32x4 *>(tile + kq_off[(st + D) & 1] + 2048 * kb +
+                                                                      4096 * ((st + D) >> 1));
             }
             u32x4 qb;
             if (st < kQRegSteps)
@@ -1166,8 +1166,8 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
         u32x4 av[4];
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
-            const u32x2 lo = lds_read_tr16(tile + vt_off[0] + 1024 * db);
-            const u32x2 hi = lds_read_tr16(tile + vt_off[1] + 1024 * db);
+            const u32x2 lo = lds_read_tr16(tile + vt_off[db]);
+            const u32x2 hi = lds_read_tr16(tile + vt_off[db] + 2048);
             av[db] = u32x4{bf16x2_to_f16x2(lo[0]), bf16x2_to_f16x2(lo[1]), bf16x2_to_f16x2(hi[0]),
                            bf16x2_to_f16x2(hi[1])};
         }
