@@ -109,26 +109,112 @@ def main():
                     help="time append_latent_kv + mixed_step_attn instead of the fused mixed_step")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also report step latency vs prefill chunk length on workload 4 (C = 0 .. 4096)")
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
                                    "(each decode node is an independent one-GPU unit)"}))
         sys.exit(2)
 
     import torch
 
-    import paper_2607_02043_amd as mla
     from paper_2607_02043_amd import workloads as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    dev = torch.device("cuda:0")
     wl = W.config(args.config, chunk=args.chunk) if args.config == 4 else W.config(args.config)
+    m = measure(args, wl, args.steps, args.warmup, calib=args.calib_copy_mib)
+    work, b, L = m["work"], wl.batch, wl.num_layers
+    out_bf16 = args.out_dtype == "bf16"
+    us_per_step, attn_us = m["us_per_step"], m["attn_us"]
+
+    # the timed call: the fused step (append + attention), or the attention call alone
+    call_bytes = work["attn_bytes"] if args.two_call else work["step_bytes"]
+    attn_gbs = call_bytes / (attn_us * 1e-6) / 1e9
+    attn_tflops = work["flops"] / (attn_us * 1e-6) / 1e12
+    step_bytes = work["step_bytes"] * L
+    step_flops = work["flops"] * L
+    ideal_us = ideal_time_us(step_bytes, step_flops)
+    bound = "hbm" if step_bytes / HBM_PEAK_GBS >= step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e3) else "mfma"
+    if bound == "hbm":
+        roof = {"bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        roof = {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+    roof["traffic"] = profiled_traffic(args.config) if not (out_bf16 or args.two_call) else None
+    roof["kernel"] = ("mixed_step_attn (attention_kernel + combine_kernel)" if args.two_call
+                      else "mixed_step (attention_kernel with the fused append + combine_kernel)")
+    roof["per_launch_us"] = round(attn_us, 3)
+    roof["algorithmic_bytes"] = call_bytes
+    roof["algorithmic_flops"] = work["flops"]
+
+    result = {
+        "metric": METRIC,
+        "value": round(us_per_step, 3),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_per_step / 1e3, 6),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": L, "page_size": b.page_size, "requests": b.num_reqs,
+                   "rows": work["rows"], "decode_rows": wl.num_decode, "chunks": [list(x) for x in wl.chunks],
+                   "out_dtype": args.out_dtype, "rotating_sets": m["n_rot"], "parallelism": "single GPU",
+                   "entry": "append_latent_kv + mixed_step_attn" if args.two_call else "mixed_step"},
+        "step": {"ideal_us": round(ideal_us, 3), "roofline_frac": round(ideal_us / us_per_step, 4),
+                 "bound": bound, "TB_per_s": round(step_bytes / (us_per_step * 1e-6) / 1e12, 3),
+                 "TFLOP_per_s": round(step_flops / (us_per_step * 1e-6) / 1e12, 2),
+                 "algorithmic_bytes": step_bytes, "algorithmic_flops": step_flops,
+                 "attention_call_us": {"mean": round(attn_us, 3), "p10": round(m["p10"], 3),
+                                       "p50": round(m["p50"], 3), "p90": round(m["p90"], 3)}},
+        "roofline": roof,
+    }
+
+    if args.sweep:
+        # step latency vs prefill chunk length at the fixed decode batch of
+        # workload 4 (the paper's chi counts decode + prefill tokens: 256 + C)
+        curve = []
+        for c in W.CHUNK_SWEEP:
+            wc = W.config(4, chunk=c)
+            mc = measure(args, wc, max(10, args.steps // 4), max(3, args.warmup // 4))
+            wk = mc["work"]
+            ideal_c = ideal_time_us(wk["step_bytes"], wk["flops"])
+            curve.append({"chunk": c, "chi": wc.num_decode + c, "us_per_step": round(mc["us_per_step"], 2),
+                          "ideal_us": round(ideal_c, 2), "roofline_frac": round(ideal_c / mc["us_per_step"], 4)})
+            log(f"[bench] sweep C={c}: {mc['us_per_step']:.1f} us/step (ideal {ideal_c:.1f})")
+        result["curve"] = {"workload": "256 decode (uniform 512..16384) + C-token chunk at prefix 0, page 64",
+                           "points": curve}
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.config)
+    print(json.dumps(result), flush=True)
+
+
+def ideal_time_us(step_bytes, step_flops):
+    return max(step_bytes / (HBM_PEAK_GBS * 1e9), step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6
+
+
+def measure(args, wl, steps, warmup, calib=0):
+    """Upload one workload (rotating buffer sets), time `steps` whole steps
+    after `warmup` untimed ones, then the same steps again with HIP events
+    around each attention call on its stream."""
+    import torch
+
+    import paper_2607_02043_amd as mla
+    from paper_2607_02043_amd import workloads as W
+
+    dev = torch.device("cuda:0")
     b = wl.batch
     out_bf16 = args.out_dtype == "bf16"
     work = algorithmic_work(b, 2 if out_bf16 else 4)
     L = wl.num_layers
-    log(f"[bench] workload {args.config}: {wl.name}; rows={work['rows']} keys={work['keys']} pairs={work['pairs']}")
+    log(f"[bench] workload: {wl.name}; rows={work['rows']} keys={work['keys']} pairs={work['pairs']}")
 
     db = mla.DeviceBatch.from_batch(b, device=dev)
     ws = mla.workspace_for(db, device=dev)
@@ -175,90 +261,45 @@ def main():
             if ev is not None:
                 ev[j][1].record(stream)
 
-    for k in range(args.warmup):
+    for k in range(warmup):
         step(k)
     torch.cuda.synchronize()
 
-    if args.calib_copy_mib > 0:
-        n = args.calib_copy_mib << 20
+    if calib > 0:
+        n = calib << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
-        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+        log(f"[bench] calibration copy of {calib} MiB done")
         del src, dst
 
     # timed region: whole steps
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         step(k)
     torch.cuda.synchronize()
     t_total = time.perf_counter() - t_start
-    us_per_step = t_total / args.steps * 1e6
+    us_per_step = t_total / steps * 1e6
 
     # same steps again with HIP events around the attention call (on its stream)
     evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in range(L)]
-           for _ in range(args.steps)]
+           for _ in range(steps)]
     torch.cuda.synchronize()
-    for k in range(args.steps):
+    for k in range(steps):
         step(k, evs[k])
     torch.cuda.synchronize()
     attn_ms = [e0.elapsed_time(e1) for row in evs for e0, e1 in row]
     attn_us = float(np.mean(attn_ms)) * 1e3
-    attn_us_p10, attn_us_p50, attn_us_p90 = (float(np.percentile(attn_ms, q)) * 1e3 for q in (10, 50, 90))
-    log(f"[bench] step {us_per_step:.2f} us; attention call mean {attn_us:.2f} us (p10 {attn_us_p10:.2f}, "
-        f"p50 {attn_us_p50:.2f}, p90 {attn_us_p90:.2f})")
-
-    # the timed call: the fused step (append + attention), or the attention call alone
-    call_bytes = work["attn_bytes"] if args.two_call else work["step_bytes"]
-    attn_gbs = call_bytes / (attn_us * 1e-6) / 1e9
-    attn_tflops = work["flops"] / (attn_us * 1e-6) / 1e12
-    step_bytes = work["step_bytes"] * L
-    step_flops = work["flops"] * L
-    ideal_us = max(step_bytes / (HBM_PEAK_GBS * 1e9), step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6
-    bound = "hbm" if step_bytes / HBM_PEAK_GBS >= step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e3) else "mfma"
-    if bound == "hbm":
-        roof = {"bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None}
-    else:
-        roof = {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
-    roof["traffic"] = profiled_traffic(args.config) if not (out_bf16 or args.two_call) else None
-    roof["kernel"] = ("mixed_step_attn (attention_kernel + combine_kernel)" if args.two_call
-                      else "mixed_step (attention_kernel with the fused append + combine_kernel)")
-    roof["per_launch_us"] = round(attn_us, 3)
-    roof["algorithmic_bytes"] = call_bytes
-    roof["algorithmic_flops"] = work["flops"]
-
-    result = {
-        "metric": METRIC,
-        "value": round(us_per_step, 3),
-        "unit": "us/step",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(us_per_step / 1e3, 6),
-        "higher_is_better": False,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": wl.name, "layers": L, "page_size": b.page_size, "requests": b.num_reqs,
-                   "rows": work["rows"], "decode_rows": wl.num_decode, "chunks": [list(x) for x in wl.chunks],
-                   "out_dtype": args.out_dtype, "rotating_sets": n_rot, "parallelism": "single GPU",
-                   "entry": "append_latent_kv + mixed_step_attn" if args.two_call else "mixed_step"},
-        "step": {"ideal_us": round(ideal_us, 3), "roofline_frac": round(ideal_us / us_per_step, 4),
-                 "bound": bound, "TB_per_s": round(step_bytes / (us_per_step * 1e-6) / 1e12, 3),
-                 "TFLOP_per_s": round(step_flops / (us_per_step * 1e-6) / 1e12, 2),
-                 "algorithmic_bytes": step_bytes, "algorithmic_flops": step_flops},
-        "roofline": roof,
-    }
-
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, args.config)
-    print(json.dumps(result), flush=True)
+    p10, p50, p90 = (float(np.percentile(attn_ms, q)) * 1e3 for q in (10, 50, 90))
+    log(f"[bench] step {us_per_step:.2f} us; attention call mean {attn_us:.2f} us (p10 {p10:.2f}, "
+        f"p50 {p50:.2f}, p90 {p90:.2f})")
+    del rotations, layer_sets
+    torch.cuda.empty_cache()
+    return {"work": work, "us_per_step": us_per_step, "attn_us": attn_us, "p10": p10, "p50": p50, "p90": p90,
+            "n_rot": n_rot}
 
 
 def cpu_baseline(wl, cfg):

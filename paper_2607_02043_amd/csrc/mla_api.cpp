@@ -113,12 +113,12 @@ struct Plan {
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 // Per-CU costs (us, measured on MI355X) used only to size the work items.
-constexpr double kChunkTileUs = 2.3;   // one chunk tile: 8 tokens x 32 keys
-constexpr double kChunkItemUs = 13.0;  // chunk item: lookup, queries, ring fill; epilogue stores
+constexpr double kChunkTileUs = 2.2;   // one chunk tile: 8 tokens x 32 keys
+constexpr double kChunkItemUs = 14.0;  // chunk item: lookup, queries, ring fill; epilogue stores
 constexpr double kEmptyItemUs = 1.5;   // a chunk item past its block's causal limit
-constexpr double kDecTileUs = 2.1;     // one decode tile: 1 token x 32 keys
-constexpr double kDecUnitUs = 5.5;     // decode unit start-up
-constexpr double kMergeGBs = 4000.0;   // partial rows written and merged, whole chip
+constexpr double kDecTileUs = 3.5;     // one decode tile of a unit (the two units of an item run side by side)
+constexpr double kDecUnitUs = 5.5;     // decode item start-up
+constexpr double kMergeGBs = 2000.0;   // partial rows written and merged, whole chip
 constexpr int kCounterBytes = 256;     // work-queue counters at the start of the workspace
 
 struct DecReq {
