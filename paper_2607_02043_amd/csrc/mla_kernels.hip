@@ -617,6 +617,16 @@ __device__ __forceinline__ void wait_units_newer(int n) {  // n of the later uni
         asm volatile("s_waitcnt vmcnt(18)" ::: "memory");
 }
 
+// threadIdx.x behind an empty asm: values derived from it inside a work item
+// are then computed per item instead of being hoisted out of the persistent
+// loop, where they would stay live across both paths and spill to scratch (a
+// scratch reload waits on vmcnt, i.e. on every DMA in flight).
+__device__ __forceinline__ int item_tid() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
 // Barrier of the four wavefronts of one wave group, through an arrival
 // counter in LDS; epoch (wave-uniform) counts the group's barriers so far.
 // Each wave first waits for its own LDS accesses, so what it wrote before the
@@ -637,7 +647,7 @@ __device__ __forceinline__ void group_barrier(int *ctr, int &epoch) {
 
 __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int (*s_pages_g)[kPageWindow],
                           DecSeg (*s_seg_g)[kMaxSeg], int *s_gbar) {
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = item_tid(), lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = wv >> 2, gw = wv & 3, gtid = tid & 255;  // wave group, wave and thread inside it
     const int g = lane >> 4, h = lane & 15;
@@ -985,7 +995,7 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
     if (it.k0 >= it.k1) return false;  // key range past this block's causal limit
     if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return false;
     if (it.nks_eff > 1 && a.ws_chunk_o == nullptr) return false;
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = item_tid(), lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, hd = lane & 15;
     const int nt = it.i1 - it.i0;  // tokens of this block (1 .. 8)
@@ -1010,6 +1020,10 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
             *reinterpret_cast<u32x4 *>(s_q + ((s * kCT + wv) * 64 + lane) * 16) = qr[s];
     }
     load_page_window(a, r, lp0, ((it.k1 - 1) >> a.log2_page) - lp0 + 1, s_pages);
+    // The query loads must count as complete before the tile DMAs go out: a
+    // wait the compiler places later for them would also wait for those DMAs.
+#pragma unroll
+    for (int s = 0; s < kQRegSteps; ++s) asm volatile("" : "+v"(qreg[s]));
     TRACE(2);
     TRACE_VAL(8, 1000000ull * 1 + ntiles);
 
