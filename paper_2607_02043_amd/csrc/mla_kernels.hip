@@ -429,7 +429,7 @@ template <int NH, typename Slot>
 __device__ void merge_heads(const AttnArgs &a, int row, int hh0, int nsplit, Slot slot) {
     // NH heads per workgroup: head hh0 + tid / (256 / NH), DPT value dims per thread
     constexpr int TPH = kThreads / NH, DPT = kDv / TPH, NV = DPT / 4;
-    constexpr int B = NH >= 16 ? 4 : 8;  // splits whose loads go out together
+    constexpr int B = NH >= 16 ? 2 : NH >= 4 ? 8 : 16;  // splits whose loads go out together
     const int tid = threadIdx.x;
     const int hh = hh0 + tid / TPH, d0 = (tid % TPH) * DPT;
     float M = kNegInf, den = 0.f;
