@@ -1342,13 +1342,18 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) 
     }
 }
 
+// Merge workgroups of split decode rows (none when no decode row was split).
+__host__ __device__ __forceinline__ int merge_dec_wgs(const AttnArgs &a) {
+    return a.ws_dec_o != nullptr ? a.num_reqs * a.merge_hsplit : 0;
+}
+
 // Split merges, after the attention kernel (the kernel boundary makes every
 // partial visible): first merge_hsplit workgroups per request (decode rows
 // split across units), then one per (chunk item, block row).
 __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     __shared__ int s_tmp[16];
     const int b = blockIdx.x;
-    const int n_dec = a.num_reqs * a.merge_hsplit;
+    const int n_dec = merge_dec_wgs(a);
     if (b < n_dec) {
         decode_merge(a, b / a.merge_hsplit, b % a.merge_hsplit, s_tmp);
         return;
@@ -1468,7 +1473,9 @@ hipError_t launch_attention(const AttnArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_combine(const AttnArgs &a, hipStream_t s) {
-    const long long grid_ll = (long long)a.num_reqs * a.merge_hsplit + (long long)a.n_chunk_items * kChunkBlockTokens;
+    // only the kinds that left partials get workgroups
+    const long long grid_ll =
+        (long long)merge_dec_wgs(a) + (a.ws_chunk_o != nullptr ? (long long)a.n_chunk_items * kChunkBlockTokens : 0);
     if (grid_ll > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     const int grid = (int)grid_ll;
     if (grid == 0) return hipSuccess;
