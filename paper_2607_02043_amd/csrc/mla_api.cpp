@@ -128,6 +128,9 @@ struct DecReq {
 // Does a decode unit of S tiles respect the kernel's limits (segments and
 // page-window entries per unit)?
 bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long S, int page_size) {
+    // a unit of S tiles touches at most S requests and, per request, at most
+    // its keys / page_size + 2 pages
+    if (S <= mla::kMaxDecSegments && S * mla::kKeysPerTile / page_size + 2 * S <= mla::kPageWindow) return true;
     size_t k = 0;
     for (long long R0 = 0; R0 < total; R0 += S) {
         const long long R1 = std::min(R0 + S, total);
@@ -159,21 +162,49 @@ std::vector<double> simulate_chunks(const std::vector<double> &items, int G) {
     return heap;
 }
 
+// Workgroup loads as runs of equal values, ascending.
+struct LoadRun {
+    double load;
+    long long count;
+};
+std::vector<LoadRun> load_runs(std::vector<double> loads) {
+    std::sort(loads.begin(), loads.end());
+    std::vector<LoadRun> runs;
+    for (double L : loads) {
+        if (!runs.empty() && runs.back().load == L)
+            ++runs.back().count;
+        else
+            runs.push_back(LoadRun{L, 1});
+    }
+    return runs;
+}
+
 // Finishing time when n equal units of cost u follow, each taken by the first
-// free workgroup: the last unit starts at the smallest t by which n units
-// have started, i.e. sum_i ceil((t - L_i) / u) >= n over loads L_i < t.
-double fill_units(const std::vector<double> &loads, long long n, double u) {
-    double mx = 0.0;
-    for (double L : loads) mx = std::max(mx, L);
-    if (n <= 0) return mx;
+// free workgroup, on top of the workgroup loads.  The last unit starts at the
+// smallest t with sum over loads L < t of ceil((t - L) / u) >= n; the water
+// level of the n units over the least-loaded workgroups bounds that t to
+// [level - u, level].
+double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
+    const double mx = runs.empty() ? 0.0 : runs.back().load;
+    if (n <= 0 || runs.empty()) return mx;
+    double sum = 0.0, level = 0.0;
+    long long cnt = 0;
+    for (size_t k = 0; k < runs.size(); ++k) {
+        sum += runs[k].load * (double)runs[k].count;
+        cnt += runs[k].count;
+        level = (sum + (double)n * u) / (double)cnt;
+        if (k + 1 == runs.size() || level <= runs[k + 1].load) break;
+    }
     auto started = [&](double t) {
-        long long k = 0;
-        for (double L : loads)
-            if (L < t) k += (long long)std::ceil((t - L) / u - 1e-9);
-        return k;
+        long long c = 0;
+        for (const LoadRun &r : runs) {
+            if (r.load >= t) break;
+            c += r.count * (long long)std::ceil((t - r.load) / u - 1e-9);
+        }
+        return c;
     };
-    double lo = 0.0, hi = mx + (double)n * u + u;
-    for (int it = 0; it < 24 && hi - lo > 0.01 * u; ++it) {
+    double lo = std::max(0.0, level - u), hi = level;
+    for (int it = 0; it < 10; ++it) {
         const double mid = 0.5 * (lo + hi);
         if (started(mid) >= n)
             hi = mid;
@@ -231,7 +262,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
     }
     // Finishing time of the decode units (equal cost u) poured onto the loads
     // left by the chunk items, plus the merge of the requests they split.
-    auto with_decode = [&](const std::vector<double> &loads, long long U) {
+    auto with_decode = [&](const std::vector<LoadRun> &loads, long long U) {
         const long long n = ceil_div_ll(ceil_div_ll(dec_total, U), 2);  // work items: pairs of units
         const double u = kDecUnitUs + kDecTileUs * (double)U;
         long long split_parts = 0;
@@ -253,7 +284,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
         struct Cand {
             long long ks;
             double merge_us, est;
-            std::vector<double> loads;
+            std::vector<LoadRun> loads;
         };
         std::vector<Cand> cands;
         std::vector<double> items;
@@ -265,7 +296,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
             for (const auto &pc : chunks) {
                 const long long p = pc.first, c = pc.second;
                 const long long nrb = ceil_div_ll(c, BM), nks = ceil_div_ll(p + c, k);
-                if ((long long)items.size() + nrb * nks > 16LL * G) {
+                if ((long long)items.size() + nrb * nks > 4LL * G) {
                     too_many = true;
                     break;
                 }
@@ -281,11 +312,11 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
                 }
             }
             if (!too_many) {
-                Cand cd{k, (double)split_rows * row_bytes / (kMergeGBs * 1e3), 0.0, simulate_chunks(items, G)};
+                Cand cd{k, (double)split_rows * row_bytes / (kMergeGBs * 1e3), 0.0, load_runs(simulate_chunks(items, G))};
                 double mx = 0.0, sum = 0.0;
-                for (double L : cd.loads) {
-                    mx = std::max(mx, L);
-                    sum += L;
+                for (const LoadRun &r : cd.loads) {
+                    mx = std::max(mx, r.load);
+                    sum += r.load * (double)r.count;
                 }
                 double est = mx;
                 if (dec_total > 0) {
