@@ -1,0 +1,64 @@
+// Host-only harness around the library's work planner (the translation unit
+// is included as is; the three launch functions are stubbed because nothing is
+// launched here).  Input on stdin, one batch per line:
+//   ncu page_size R q_0 p_0 q_1 p_1 ...
+// Output, one line per batch:
+//   ok ks n_chunk_items n_dec_items unit_tiles dec_total grid merge_hsplit chunk_split dec_split bytes
+//      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us
+// or "err <status> <message>".
+#include "../../paper_2607_02043_amd/csrc/mla_api.cpp"
+
+#include <chrono>
+#include <iostream>
+#include <sstream>
+#include <string>
+
+namespace mla {
+hipError_t launch_append(const AppendArgs &, hipStream_t) { return hipSuccess; }
+hipError_t launch_attention(const AttnArgs &, hipStream_t) { return hipSuccess; }
+hipError_t launch_combine(const AttnArgs &, hipStream_t) { return hipSuccess; }
+}  // namespace mla
+
+int main() {
+    std::string line;
+    while (std::getline(std::cin, line)) {
+        std::istringstream in(line);
+        int ncu = 0, P = 0, R = 0;
+        if (!(in >> ncu >> P >> R)) continue;
+        std::vector<int32_t> q(R), p(R);
+        long long maxk = 1;
+        for (int i = 0; i < R; ++i) {
+            in >> q[i] >> p[i];
+            maxk = std::max<long long>(maxk, (long long)q[i] + p[i]);
+        }
+        static const int32_t fake = 0;  // device pointers are never dereferenced by the planner
+        mla_batch b{};
+        b.num_reqs = R;
+        b.page_size = P;
+        b.num_pages = 1 << 30;
+        b.max_pages_per_req = (int)((maxk + P - 1) / P);
+        b.q_lens = q.data();
+        b.prefix_lens = p.data();
+        b.cu_q_dev = &fake;
+        b.prefix_lens_dev = &fake;
+        b.block_table_dev = &fake;
+        Shape sh;
+        int st = check_batch(&b, &sh);
+        Plan pl{};
+        double us = 0.0;
+        if (st == MLA_OK && sh.R > 0) {
+            const auto t0 = std::chrono::steady_clock::now();
+            st = make_plan_uncached(&b, sh, ncu, &pl);
+            us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+        }
+        if (st != MLA_OK) {
+            std::cout << "err " << st << " " << g_err << "\n";
+            continue;
+        }
+        std::cout << "ok " << pl.ks_chunk << " " << pl.n_chunk_items << " " << pl.n_dec_units << " "
+                  << pl.dec_unit_tiles << " " << pl.dec_total_tiles << " " << pl.grid << " " << pl.merge_hsplit << " "
+                  << (int)pl.chunk_split << " " << (int)pl.dec_split << " " << pl.bytes << " " << pl.off_chunk_o << " "
+                  << pl.off_chunk_ml << " " << pl.off_dec_o << " " << pl.off_dec_ml << " " << us << "\n";
+    }
+    return 0;
+}

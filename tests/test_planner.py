@@ -1,0 +1,156 @@
+"""The host work planner (host code, no GPU): the real planner source is built
+into a small harness and its plans are checked against the kernels' limits and
+the mapping the device recomputes.
+
+Checked for random ragged batches: the chunk item count and key split, the
+decode unit size against the per-unit segment and page-window limits, the
+number of units and items, the merge fan-out, the workspace layout (counter
+block, then partial slots that fit every split row), and the planning time."""
+import math
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "tests", "planner", "plan_harness.cpp")
+
+KEYS_PER_TILE, BLOCK_TOKENS, MAX_SEG, PAGE_WINDOW = 32, 8, 64, 256
+PARTIAL_FLOATS, PARTIAL_STATS, COUNTER_BYTES = 16 * 512, 16 * 2, 256
+
+
+@pytest.fixture(scope="module")
+def harness(tmp_path_factory):
+    cxx = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(cxx):
+        pytest.skip("hipcc not available")
+    exe = str(tmp_path_factory.mktemp("planner") / "plan_harness")
+    inc = [f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(ROOT, 'paper_2607_02043_amd', 'csrc')}"]
+    subprocess.run([cxx, "-O2", "-std=c++17", *inc, SRC, "-o", exe], check=True, capture_output=True)
+    return exe
+
+
+def plan(exe, batches):
+    text = "".join(f"{ncu} {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n"
+                   for ncu, P, q, p in batches)
+    out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True).stdout.splitlines()
+    assert len(out) == len(batches)
+    res = []
+    for line in out:
+        f = line.split()
+        if f[0] == "err":
+            res.append(("err", int(f[1]), " ".join(f[2:])))
+            continue
+        keys = ["ks", "n_chunk_items", "n_dec_items", "U", "dec_total", "grid", "hsplit", "chunk_split",
+                "dec_split", "bytes", "off_co", "off_cml", "off_do", "off_dml"]
+        d = {k: int(v) for k, v in zip(keys, f[1:15])}
+        d["us"] = float(f[15])
+        res.append(d)
+    return res
+
+
+def random_batch(rng, ncu):
+    P = int(rng.choice([1, 2, 16, 32, 64, 256]))
+    n_dec = int(rng.integers(0, 300))
+    n_chunk = int(rng.integers(0, 5)) if n_dec else int(rng.integers(1, 5))
+    cap = 4096 if P >= 16 else 1024
+    q = [1] * n_dec + [int(rng.integers(2, 2049)) for _ in range(n_chunk)]
+    p = [int(rng.integers(0, cap)) for _ in range(n_dec)] + [int(rng.integers(0, 8193)) for _ in range(n_chunk)]
+    perm = rng.permutation(len(q))
+    return ncu, P, [q[i] for i in perm], [p[i] for i in perm]
+
+
+def unit_limits(dec, U, P):
+    """(max segments, max page-window entries) over the units of U tiles of
+    the flattened decode tile list (dec: [(first_tile, tiles, p)])."""
+    total = sum(t for _, t, _ in dec)
+    worst_seg = worst_pages = 0
+    for R0 in range(0, total, U):
+        R1 = min(R0 + U, total)
+        segs = pages = 0
+        for first, tiles, p in dec:
+            if first + tiles <= R0 or first >= R1:
+                continue
+            t0, t1 = max(R0 - first, 0), min(R1 - first, tiles)
+            k0, klast = t0 * KEYS_PER_TILE, min(t1 * KEYS_PER_TILE, p + 1) - 1
+            pages += klast // P - k0 // P + 1
+            segs += 1
+        worst_seg, worst_pages = max(worst_seg, segs), max(worst_pages, pages)
+    return worst_seg, worst_pages
+
+
+def check_plan(batch, d):
+    ncu, P, q, p = batch
+    chunks = [(pi, qi) for qi, pi in zip(q, p) if qi > 1]
+    dec, first = [], 0
+    for qi, pi in zip(q, p):
+        if qi == 1:
+            nt = -(-(pi + 1) // KEYS_PER_TILE)
+            dec.append((first, nt, pi))
+            first += nt
+    ks = d["ks"]
+    # chunk items: ceil(c / 8) blocks x ceil((p + c) / ks) key splits per request
+    assert d["n_chunk_items"] == sum(-(-c // BLOCK_TOKENS) * -(-(pp + c) // ks) for pp, c in chunks)
+    assert d["chunk_split"] == int(any(pp + c > ks for pp, c in chunks))
+    if chunks:
+        assert ks % 64 == 0 and ks >= 64
+        assert ks <= max(64, (PAGE_WINDOW - 1) * P // 64 * 64)  # an item's keys fit the page window
+    assert d["dec_total"] == first
+    if dec:
+        U = d["U"]
+        assert 1 <= U <= first
+        units = -(-first // U)
+        assert d["n_dec_items"] == -(-units // 2)
+        seg, pages = unit_limits(dec, U, P)
+        assert seg <= MAX_SEG and pages <= PAGE_WINDOW
+        parts = max((f + t - 1) // U - f // U + 1 for f, t, _ in dec)
+        assert d["dec_split"] == int(parts > 1)
+        assert d["hsplit"] == (8 if parts > 16 else 4 if parts > 4 else 1)
+    else:
+        units = 0
+        assert d["n_dec_items"] == 0 and d["dec_split"] == 0
+    assert 1 <= d["grid"] <= ncu and d["grid"] <= d["n_chunk_items"] + d["n_dec_items"]
+    # workspace: counters, then 256-byte aligned partial slots
+    off = COUNTER_BYTES
+    align = lambda v: (v + 255) // 256 * 256
+    if d["chunk_split"]:
+        assert d["off_co"] == off
+        off = align(off + d["n_chunk_items"] * BLOCK_TOKENS * PARTIAL_FLOATS * 4)
+        assert d["off_cml"] == off
+        off = align(off + d["n_chunk_items"] * BLOCK_TOKENS * PARTIAL_STATS * 4)
+    if d["dec_split"]:
+        assert d["off_do"] == off
+        off = align(off + 2 * units * PARTIAL_FLOATS * 4)
+        assert d["off_dml"] == off
+        off = align(off + 2 * units * PARTIAL_STATS * 4)
+    assert d["bytes"] == off
+
+
+def test_plans_of_random_batches_respect_the_kernel_limits(harness):
+    rng = np.random.default_rng(7)
+    batches = [random_batch(rng, int(rng.choice([64, 256, 304]))) for _ in range(60)]
+    for b, d in zip(batches, plan(harness, batches)):
+        assert not isinstance(d, tuple), (b[:2], d)
+        check_plan(b, d)
+
+
+def test_plans_of_the_benchmark_workloads(harness):
+    from paper_2607_02043_amd import workloads as W
+    wls = [W.config(1), W.config(2), W.config(3), W.config(4, chunk=0), W.config(4, chunk=2048), W.config(5)]
+    batches = [(256, w.batch.page_size, [int(x) for x in w.batch.q_lens], [int(x) for x in w.batch.prefix_lens])
+               for w in wls]
+    res = plan(harness, batches)
+    for b, d in zip(batches, res):
+        check_plan(b, d)
+        assert d["us"] < 5000, d["us"]  # a plan is recomputed whenever the lengths change
+    # decode-only: one item of two equal units per CU
+    assert res[3]["n_chunk_items"] == 0 and res[3]["n_dec_items"] == 256
+
+
+def test_single_request_extremes(harness):
+    cases = [(256, 64, [1], [0]), (256, 1, [1], [0]), (256, 64, [2], [0]), (256, 16, [1], [1 << 20]),
+             (256, 64, [4096], [1 << 16]), (1, 64, [1, 1, 300], [5, 70, 1000])]
+    for b, d in zip(cases, plan(harness, cases)):
+        check_plan(b, d)
