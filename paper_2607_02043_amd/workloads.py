@@ -51,6 +51,8 @@ CANARY_BF16 = 0x7FC0  # quiet NaN
 
 _BLOCK = 1 << 22
 _STREAM_CACHE, _STREAM_NEW, _STREAM_Q = 0, 1, 2
+_STREAM_HIDDEN, _STREAM_ATTN_OUT = 3, 4
+_STREAM_W = 10  # + index of the weight
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -75,8 +77,8 @@ def _threads() -> int:
     return max(1, min(16, n))
 
 
-def random_bf16(n_values: int, scale: float, seed: int, layer: int, stream: int) -> np.ndarray:
-    """n_values bf16 bit patterns of scale * N(0,1), block-seeded (see module doc)."""
+def random_bf16(n_values: int, scale: float, seed: int, layer: int, stream: int, offset: float = 0.0) -> np.ndarray:
+    """n_values bf16 bit patterns of offset + scale * N(0,1), block-seeded (see module doc)."""
     out = np.empty(n_values, dtype=np.uint16)
     nblk = (n_values + _BLOCK - 1) // _BLOCK
 
@@ -87,6 +89,8 @@ def random_bf16(n_values: int, scale: float, seed: int, layer: int, stream: int)
         x = rng.standard_normal(hi - lo, dtype=np.float32)
         if scale != 1.0:
             x *= np.float32(scale)
+        if offset != 0.0:
+            x += np.float32(offset)
         out[lo:hi] = f32_to_bf16_bits(x)
 
     if nblk <= 1:
@@ -272,3 +276,64 @@ def custom(prefix_lens: Sequence[int], q_lens: Sequence[int], page_size: int = 6
                        table_slack_pages=table_slack_pages)
     nd = int((np.asarray(q_lens) == 1).sum())
     return Workload(name=name, seed=seed, value_scale=value_scale, batch=batch, num_decode=nd)
+
+
+# ---------------------------------------------------------------------------
+# Projection weights of one attention layer and its input, for the layer step
+# (hidden width 2048, 16 heads, 128 + 64 query dims per head, 512 + 64 latent
+# dims, 128 value dims per head).  Weights are random: the trained model is
+# not used.  Each is offset + scale * N(0,1) with scale = 1/sqrt(fan-in), so
+# every projection of unit-variance inputs has unit-variance outputs; the
+# RMSNorm gain is 1 + 0.1 N(0,1).
+# ---------------------------------------------------------------------------
+HIDDEN = 2048
+QK_NOPE, QK_ROPE, V_HEAD = 128, 64, 128
+
+
+@dataclasses.dataclass
+class ProjWeights:
+    """bf16 bit patterns, in the layouts of the C ABI (mla_layer.h)."""
+
+    w_q: np.ndarray      # [16 * 192][2048]
+    w_dkv: np.ndarray    # [576][2048]
+    kv_gain: np.ndarray  # [512]
+    w_uk_t: np.ndarray   # [16][512][128]
+    w_uv: np.ndarray     # [16][128][512]
+    w_o: np.ndarray      # [2048][16 * 128]
+    rms_eps: float = 1e-6
+    rope_base: float = 10000.0
+
+
+def make_proj_weights(seed: int = 0, layer: int = 0) -> ProjWeights:
+    def draw(k, shape, fan_in, offset=0.0, scale=None):
+        n = int(np.prod(shape))
+        sc = scale if scale is not None else 1.0 / math.sqrt(fan_in)
+        return random_bf16(n, sc, seed, layer, _STREAM_W + k, offset).reshape(shape)
+
+    qk = QK_NOPE + QK_ROPE
+    return ProjWeights(
+        w_q=draw(0, (NUM_HEADS * qk, HIDDEN), HIDDEN),
+        w_dkv=draw(1, (D_QK, HIDDEN), HIDDEN),
+        kv_gain=draw(2, (D_LATENT,), 1, offset=1.0, scale=0.1),
+        w_uk_t=draw(3, (NUM_HEADS, D_LATENT, QK_NOPE), QK_NOPE),
+        w_uv=draw(4, (NUM_HEADS, V_HEAD, D_LATENT), D_LATENT),
+        w_o=draw(5, (HIDDEN, NUM_HEADS * V_HEAD), NUM_HEADS * V_HEAD),
+    )
+
+
+def random_hidden(num_rows: int, seed: int = 0, layer: int = 0, scale: float = 1.0) -> np.ndarray:
+    """Layer input: bf16 bits [T][2048] of scale * N(0,1)."""
+    return random_bf16(num_rows * HIDDEN, scale, seed, layer, _STREAM_HIDDEN).reshape(num_rows, HIDDEN)
+
+
+def random_attn_out(num_rows: int, seed: int = 0, layer: int = 0, scale: float = 1.0) -> np.ndarray:
+    """An attention output to feed the post-attention projections alone:
+    float32 [T][16][512] of scale * N(0,1) (block-seeded like random_bf16)."""
+    n = num_rows * NUM_HEADS * D_V
+    out = np.empty(n, dtype=np.float32)
+    for b in range((n + _BLOCK - 1) // _BLOCK):
+        lo, hi = b * _BLOCK, min(n, (b + 1) * _BLOCK)
+        out[lo:hi] = np.random.default_rng([seed, layer, _STREAM_ATTN_OUT, b]).standard_normal(hi - lo, dtype=np.float32)
+    if scale != 1.0:
+        out *= np.float32(scale)
+    return out.reshape(num_rows, NUM_HEADS, D_V)
