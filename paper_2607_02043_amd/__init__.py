@@ -26,6 +26,10 @@ NUM_HEADS, D_QK, D_V = 16, 576, 512
 
 EXPORTED = ("mla_abi_version", "mla_last_error", "mixed_step_workspace_bytes", "append_latent_kv",
             "mixed_step_attn", "mixed_step")
+# include/mla_layer.h
+EXPORTED_LAYER = ("mla_proj_workspace_bytes", "mla_pre_attn", "mla_post_attn", "mla_layer_workspace_bytes",
+                  "mla_attention_layer")
+HIDDEN = 2048
 
 
 class MlaError(RuntimeError):
@@ -45,6 +49,19 @@ class mla_batch(ctypes.Structure):
         ("cu_q_dev", ctypes.c_void_p),
         ("prefix_lens_dev", ctypes.c_void_p),
         ("block_table_dev", ctypes.c_void_p),
+    ]
+
+
+class mla_proj_weights(ctypes.Structure):
+    _fields_ = [
+        ("w_q", ctypes.c_void_p),
+        ("w_dkv", ctypes.c_void_p),
+        ("kv_gain", ctypes.c_void_p),
+        ("w_uk_t", ctypes.c_void_p),
+        ("w_uv", ctypes.c_void_p),
+        ("w_o", ctypes.c_void_p),
+        ("rms_eps", ctypes.c_float),
+        ("rope_base", ctypes.c_float),
     ]
 
 
@@ -73,6 +90,19 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_float, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_size_t, ctypes.c_void_p]
         L.mixed_step.restype = ctypes.c_int
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        wp = ctypes.POINTER(mla_proj_weights)
+        L.mla_proj_workspace_bytes.argtypes = [i32]
+        L.mla_proj_workspace_bytes.restype = sz
+        L.mla_pre_attn.argtypes = [ctypes.POINTER(mla_batch), vp, wp, vp, vp, vp, sz, vp]
+        L.mla_pre_attn.restype = ctypes.c_int
+        L.mla_post_attn.argtypes = [i32, vp, i32, wp, vp, i32, vp, sz, vp]
+        L.mla_post_attn.restype = ctypes.c_int
+        L.mla_layer_workspace_bytes.argtypes = [ctypes.POINTER(mla_batch)]
+        L.mla_layer_workspace_bytes.restype = sz
+        L.mla_attention_layer.argtypes = [ctypes.POINTER(mla_batch), vp, wp, vp, ctypes.c_float, vp, i32, vp, sz,
+                                          vp]
+        L.mla_attention_layer.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -179,4 +209,69 @@ def workspace_for(batch: DeviceBatch, device="cuda"):
     bytes: every completed call leaves its counters zero."""
     import torch
     n = mixed_step_workspace_bytes(batch)
+    return torch.zeros(n, dtype=torch.uint8, device=device) if n > 0 else None
+
+
+# --------------------------------------------------------------------------
+# Projections around the attention and the whole layer (include/mla_layer.h)
+# --------------------------------------------------------------------------
+class DeviceProjWeights:
+    """Device copies (int16 tensors holding bf16 bits) of one layer's
+    projection weights, from a workloads.ProjWeights or any object with the
+    same fields (numpy uint16 arrays in the C ABI's layouts)."""
+
+    FIELDS = ("w_q", "w_dkv", "kv_gain", "w_uk_t", "w_uv", "w_o")
+
+    def __init__(self, weights, device="cuda"):
+        import torch
+        self.tensors = {}
+        for f in self.FIELDS:
+            arr = np.ascontiguousarray(getattr(weights, f)).view(np.int16)
+            self.tensors[f] = torch.from_numpy(arr.copy()).to(device)
+        self.c = mla_proj_weights(**{f: _ptr(self.tensors[f]) for f in self.FIELDS},
+                                  rms_eps=float(weights.rms_eps), rope_base=float(weights.rope_base))
+
+
+def mla_proj_workspace_bytes(num_rows: int) -> int:
+    return int(lib().mla_proj_workspace_bytes(int(num_rows)))
+
+
+def mla_layer_workspace_bytes(batch: DeviceBatch) -> int:
+    n = int(lib().mla_layer_workspace_bytes(ctypes.byref(batch.c)))
+    err = lib().mla_last_error().decode()
+    if n == 0 and err:
+        raise MlaError(MLA_ERR_INVALID_ARG, err)
+    return n
+
+
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def mla_pre_attn(batch: DeviceBatch, hidden, weights: DeviceProjWeights, q_abs, new_latents, workspace,
+                 stream=None) -> None:
+    """hidden bf16 [T][2048] -> q_abs bf16 [T][16][576], new_latents bf16 [T][576]."""
+    _check(lib().mla_pre_attn(ctypes.byref(batch.c), _ptr(hidden), ctypes.byref(weights.c), _ptr(q_abs),
+                              _ptr(new_latents), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def mla_post_attn(attn_out, weights: DeviceProjWeights, out, workspace, stream=None) -> None:
+    """attn_out [T][16][512] (fp32 or bf16) -> out [T][2048] (fp32 or bf16: dtypes pick the modes)."""
+    T = int(attn_out.shape[0])
+    _check(lib().mla_post_attn(T, _ptr(attn_out), _out_mode(attn_out), ctypes.byref(weights.c), _ptr(out),
+                               _out_mode(out), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def mla_attention_layer(batch: DeviceBatch, hidden, weights: DeviceProjWeights, kv_cache, softmax_scale: float, out,
+                        workspace, stream=None) -> None:
+    """One attention layer: projections, append + attention, projections."""
+    _check(lib().mla_attention_layer(ctypes.byref(batch.c), _ptr(hidden), ctypes.byref(weights.c), _ptr(kv_cache),
+                                     float(softmax_scale), _ptr(out), _out_mode(out), _ptr(workspace),
+                                     _nbytes(workspace), _stream(stream)))
+
+
+def layer_workspace_for(batch: DeviceBatch, device="cuda"):
+    """A workspace for mla_attention_layer with its counters zeroed (None if 0 bytes)."""
+    import torch
+    n = mla_layer_workspace_bytes(batch)
     return torch.zeros(n, dtype=torch.uint8, device=device) if n > 0 else None

@@ -8,7 +8,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmlastep.so")
-SOURCES = ["mla_kernels.hip", "mla_api.cpp"]
+SOURCES = ["mla_kernels.hip", "mla_api.cpp", "proj_kernels.hip", "proj_api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

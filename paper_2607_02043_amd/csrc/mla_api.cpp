@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "mla_kernels.h"
+#include "api_util.h"
 
 namespace {
 
@@ -438,6 +439,36 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
 }
 
 }  // namespace
+
+namespace mla {
+
+int set_error(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int attn_workspace(const mla_batch *batch, size_t *bytes) {
+    *bytes = 0;
+    Shape sh;
+    int st = check_batch(batch, &sh);
+    if (st != MLA_OK || sh.R == 0) return st;
+    Plan pl;
+    st = make_plan(batch, sh, &pl);
+    if (st == MLA_OK) *bytes = pl.bytes;
+    return st;
+}
+
+int batch_rows(const mla_batch *batch, int *num_rows) {
+    Shape sh;
+    const int st = check_batch(batch, &sh);
+    *num_rows = st == MLA_OK ? sh.T : 0;
+    return st;
+}
+
+}  // namespace mla
 
 extern "C" {
 

@@ -1,0 +1,73 @@
+// Launch-side description of the projection kernels of libmlastep (host <-> device).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace proj {
+
+constexpr int kHidden = 2048;                 // model width
+constexpr int kHeads = 16;
+constexpr int kNope = 128;                    // per-head query dims without position
+constexpr int kRope = 64;                     // rope dims (per head for queries, shared for keys)
+constexpr int kQkHead = kNope + kRope;        // 192
+constexpr int kQCols = kHeads * kQkHead;      // 3072
+constexpr int kLatent = 512;                  // compressed latent
+constexpr int kDqk = kLatent + kRope;         // 576
+constexpr int kVHead = 128;                   // per-head value dims after the up-projection
+constexpr int kOCols = kHeads * kVHead;       // 2048
+
+constexpr int kBN = 64;   // output columns per workgroup of the fp32-activation GEMM
+constexpr int kBK = 64;   // reduction depth per pipeline stage
+
+enum Epilogue : int {
+    kStoreBf16 = 0,  // C (bf16, row stride ldc)
+    kStoreF32 = 1,   // C (fp32, row stride ldc)
+    kQkvSplit = 2,   // first projection: nope -> qn bf16, rope -> qpe fp32, latent -> kvf fp32
+};
+
+// C[z][m][n] = sum_k A[z][m][k] * B[z][n][k]: both operands K-contiguous.
+// Element strides; z = blockIdx.z.  Columns n >= n_split take their B rows
+// from b2 (row n - n_split), so two weight matrices act as one.
+struct GemmArgs {
+    const void *a;        // bf16 bits or fp32 (a_f32)
+    long long lda, a_bstride;
+    const uint16_t *b;
+    const uint16_t *b2;
+    long long ldb, b_bstride;
+    int n_split;
+    int M, N, K;
+    void *c;
+    long long ldc, c_bstride;
+    // kQkvSplit outputs
+    uint16_t *qn;         // [M][16][128] bf16
+    float *qpe;           // [M][16][64]
+    float *kvf;           // [M][576]
+};
+
+struct RowArgs {
+    const float *qpe;         // [T][16][64]
+    const float *kvf;         // [T][576]
+    const uint16_t *gamma;    // [512] bf16
+    const int32_t *cu_q;      // [R + 1]
+    const int32_t *prefix;    // [R]
+    uint16_t *q_abs;          // [T][16][576]: writes dims 512..575 of every head
+    uint16_t *latent;         // [T][576]
+    int32_t num_reqs;
+    int32_t num_rows;
+    float eps;
+    double log2_base;         // log2 of the rope base
+};
+
+// Tile shape of one GEMM launch: bm x bn outputs per workgroup, `depth` LDS
+// stages.  Instantiated: bn 64 with (bm, depth) (32, 6), (64, 4), (128, 3);
+// bn 128 with (32, 4), (64, 3), (128, 2), (128, 3).  fp32 activations use
+// bn = 64, depth 2 and any bm of 32, 64, 128 (N a multiple of 64).
+struct GemmShape {
+    int bm, bn, depth, epi;
+};
+
+// The launch covers ceil(M / bm) * ceil(N / bn) tiles x batch.
+hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int batch, hipStream_t s);
+hipError_t launch_rope_norm(const RowArgs &r, hipStream_t s);
+
+}  // namespace proj
