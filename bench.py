@@ -111,6 +111,9 @@ def main():
                     help="also run one device copy of this many MiB (counter calibration)")
     ap.add_argument("--sweep", action="store_true",
                     help="also report step latency vs prefill chunk length on workload 4 (C = 0 .. 4096)")
+    ap.add_argument("--layer", action="store_true",
+                    help="time the whole attention layer (projections + append + attention, mla_attention_layer) "
+                         "instead of the mixed step alone")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -124,6 +127,12 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     wl = W.config(args.config, chunk=args.chunk) if args.config == 4 else W.config(args.config)
+    if args.layer:
+        result = layer_bench(args, wl)
+        if not args.no_cpu_baseline:
+            result["cpu_baseline"] = cpu_baseline(wl, args.config, layer=True)
+        print(json.dumps(result), flush=True)
+        return
     m = measure(args, wl, args.steps, args.warmup, calib=args.calib_copy_mib)
     work, b, L = m["work"], wl.batch, wl.num_layers
     out_bf16 = args.out_dtype == "bf16"
@@ -194,6 +203,146 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.config)
     print(json.dumps(result), flush=True)
+
+
+# Projection shapes of one layer (hidden 2048, 16 heads, 128 + 64 query dims,
+# 512 + 64 latent dims, 128 value dims per head).
+PROJ_FLOPS_PER_ROW = 2 * (2048 * 3648 + 16 * 128 * 512 + 16 * 512 * 128 + 2048 * 2048)
+PROJ_WEIGHT_BYTES = 2 * (3648 * 2048 + 512 + 16 * 512 * 128 + 16 * 128 * 512 + 2048 * 2048)
+
+
+def layer_work(batch):
+    """Algorithmic bytes and flops of one attention layer: the mixed step's
+    (keys once, block table, new latents written) plus the weights read once,
+    the hidden input read and the fp32 output written; the intermediates
+    between kernels (queries, attention output) are not counted, a fused
+    layer would not move them."""
+    a = algorithmic_work(batch)
+    T = a["rows"]
+    pages = int(np.ceil((batch.prefix_lens.astype(np.int64) + batch.q_lens) / batch.page_size).sum())
+    step_bytes = 1152 * a["keys"] + 4 * pages + 1152 * T + PROJ_WEIGHT_BYTES + T * (2048 * 2 + 2048 * 4)
+    proj_flops = PROJ_FLOPS_PER_ROW * T
+    return {"bytes": step_bytes, "flops": a["flops"] + proj_flops, "attn_flops": a["flops"],
+            "proj_flops": proj_flops, "rows": T, "keys": a["keys"], "pairs": a["pairs"]}
+
+
+def layer_bench(args, wl):
+    """Whole attention layers (mla_attention_layer) of the workload: W warm-up
+    steps, K timed steps of all layers, then the same steps again with HIP
+    events around the three phases (projections before, mixed step, after)."""
+    import torch
+
+    import paper_2607_02043_amd as mla
+    from paper_2607_02043_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    b = wl.batch
+    L = wl.num_layers
+    work = layer_work(b)
+    T = work["rows"]
+    log(f"[bench] layer mode: {wl.name}; rows={T} keys={work['keys']}")
+    db = mla.DeviceBatch.from_batch(b, device=dev)
+
+    def up(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
+
+    t0 = time.time()
+    layers = []
+    for layer in range(L):
+        li = wl.layer(layer)
+        layers.append({"pool": up(li.pool), "w": mla.DeviceProjWeights(W.make_proj_weights(wl.seed, layer), dev),
+                       "hidden": up(W.random_hidden(T, wl.seed, layer)),
+                       "out": torch.empty((T, 2048), dtype=torch.float32, device=dev)})
+        del li
+    log(f"[bench] inputs generated and uploaded in {time.time() - t0:.1f}s")
+    set_bytes = sum(d["pool"].numel() * 2 + d["hidden"].numel() * 2 + T * 2048 * 4 for d in layers) + \
+        L * PROJ_WEIGHT_BYTES
+    n_rot = 1 if args.no_rotate else max(1, math.ceil(ROTATE_TARGET_BYTES / set_bytes))
+    rotations = [layers] + [[{"pool": d["pool"].clone(), "w": d["w"], "hidden": d["hidden"].clone(),
+                              "out": torch.empty_like(d["out"])} for d in layers] for _ in range(n_rot - 1)]
+    # rotated copies share the weights only when one set already exceeds the rotation target
+    if n_rot > 1:
+        for k in range(1, n_rot):
+            for j, d in enumerate(rotations[k]):
+                d["w"] = mla.DeviceProjWeights(W.make_proj_weights(wl.seed, 1000 * k + j), dev)
+    log(f"[bench] {n_rot} rotating buffer set(s) of {set_bytes / 2**20:.1f} MiB")
+    ws = mla.layer_workspace_for(db, device=dev)
+    stream = torch.cuda.current_stream()
+    scale = W.SOFTMAX_SCALE
+
+    def step(k):
+        for d in rotations[k % n_rot]:
+            mla.mla_attention_layer(db, d["hidden"], d["w"], d["pool"], scale, d["out"], ws, stream)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(k)
+    torch.cuda.synchronize()
+    us_per_step = (time.perf_counter() - t_start) / args.steps * 1e6
+
+    # phases, with HIP events on the stream: the same calls mla_attention_layer makes
+    q = torch.empty((T, 16, 576), dtype=torch.int16, device=dev)
+    lat = torch.empty((T, 576), dtype=torch.int16, device=dev)
+    o = torch.empty((T, 16, 512), dtype=torch.bfloat16, device=dev)
+    pws = torch.empty(mla.mla_proj_workspace_bytes(T), dtype=torch.uint8, device=dev)
+    aws = mla.workspace_for(db, device=dev)
+    ph = {"pre": [], "attn": [], "post": []}
+    n_ev = max(8, min(args.steps, 50))
+    for k in range(n_ev):
+        for d in rotations[k % n_rot]:
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record(stream)
+            mla.mla_pre_attn(db, d["hidden"], d["w"], q, lat, pws, stream)
+            e[1].record(stream)
+            mla.mixed_step(db, q, lat, d["pool"], scale, o, None, aws, stream)
+            e[2].record(stream)
+            mla.mla_post_attn(o, d["w"], d["out"], pws, stream)
+            e[3].record(stream)
+            ph["pre"].append((e[0], e[1]))
+            ph["attn"].append((e[1], e[2]))
+            ph["post"].append((e[2], e[3]))
+    torch.cuda.synchronize()
+    us = {k: float(np.mean([a.elapsed_time(z) for a, z in v])) * 1e3 for k, v in ph.items()}
+    log(f"[bench] layer step {us_per_step:.1f} us; phases: pre {us['pre']:.1f}, mixed step {us['attn']:.1f}, "
+        f"post {us['post']:.1f} us")
+
+    bytes_all, flops_all = work["bytes"] * L, work["flops"] * L
+    ideal = ideal_time_us(bytes_all, flops_all)
+    proj_us = us["pre"] + us["post"]
+    proj_tflops = work["proj_flops"] / (proj_us * 1e-6) / 1e12
+    a = algorithmic_work(b, 2)
+    attn_bound_hbm = a["step_bytes"] / HBM_PEAK_GBS >= a["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e3)
+    if attn_bound_hbm:
+        ach = a["step_bytes"] / (us["attn"] * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
+    else:
+        ach = a["flops"] / (us["attn"] * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4)}
+    roof.update({"traffic": None, "kernel": "mixed_step inside the layer (bf16 attention output)",
+                 "per_launch_us": round(us["attn"], 3)})
+    return {
+        "metric": "MLA attention-layer step µs/step (projections + append + attention); % of combined roofline",
+        "value": round(us_per_step, 3), "unit": "us/step", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(us_per_step / 1e3, 6), "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic (random weights)",
+        "config": {"workload": wl.name, "layers": L, "rows": T, "page_size": b.page_size,
+                   "rotating_sets": n_rot, "parallelism": "single GPU", "entry": "mla_attention_layer",
+                   "out_dtype": "f32"},
+        "step": {"ideal_us": round(ideal, 3), "roofline_frac": round(ideal / us_per_step, 4),
+                 "TB_per_s": round(bytes_all / (us_per_step * 1e-6) / 1e12, 3),
+                 "TFLOP_per_s": round(flops_all / (us_per_step * 1e-6) / 1e12, 2),
+                 "algorithmic_bytes": bytes_all, "algorithmic_flops": flops_all},
+        "phases_us": {k: round(v, 2) for k, v in us.items()},
+        "projections": {"flops": work["proj_flops"], "us": round(proj_us, 2), "TFLOP_per_s": round(proj_tflops, 1),
+                        "mfma_frac": round(proj_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                        "weight_bytes": PROJ_WEIGHT_BYTES},
+        "roofline": roof,
+    }
 
 
 def ideal_time_us(step_bytes, step_flops):
@@ -302,10 +451,12 @@ def measure(args, wl, steps, warmup, calib=0):
             "n_rot": n_rot}
 
 
-def cpu_baseline(wl, cfg):
+def cpu_baseline(wl, cfg, layer=False):
     """The fp64 oracle as it stands, timed on this host on a bounded sample."""
     import oracle
     from paper_2607_02043_amd import workloads as W
+    if layer:
+        return cpu_baseline_layer(wl)
 
     threads = len(os.sched_getaffinity(0))
     b = wl.batch
@@ -337,6 +488,50 @@ def cpu_baseline(wl, cfg):
     value_us = per_layer_s * wl.num_layers * 1e6
     return {"value": round(value_us, 1), "unit": "us/step", "cores": threads, "kind": "oracle",
             "sample": sample + f"; median of 3; x{wl.num_layers} layer(s)",
+            "cpu": _cpu_model()}
+
+
+def cpu_baseline_layer(wl):
+    """The layer oracle (numpy fp64 projections around the C attention
+    oracle) on a bounded sample: the projections of a seeded sample of rows
+    and the attention of those rows, scaled to the whole step."""
+    from oracle import proj_oracle as PO
+    from paper_2607_02043_amd import workloads as W
+
+    threads = len(os.sched_getaffinity(0))
+    b = wl.batch
+    li = wl.layer(0)
+    T = b.num_rows
+    wo = PO.Weights.from_bits(W.make_proj_weights(wl.seed, 0))
+    hidden = W.random_hidden(T, wl.seed, 0)
+    rng = np.random.default_rng(0)
+    n = min(T, 64)
+    rows = np.sort(rng.choice(T, size=n, replace=False))
+    pos = PO.positions(b.q_lens, b.prefix_lens)
+    import oracle
+    t_pre, t_rest = [], []
+    for _ in range(3):
+        t = time.perf_counter()
+        # every row's projections (the attention needs all new latents), the sampled rows' attention and output
+        q_abs, lat = PO.pre_attn(pos, PO.bf16_value(hidden), wo, rounded=True)
+        t_pre.append(time.perf_counter() - t)
+        t = time.perf_counter()
+        pool_after = oracle.append(b, lat, li.pool)
+        o, _ = oracle.attend(b, q_abs, pool_after, W.SOFTMAX_SCALE, rows=rows, threads=threads)
+        PO.post_attn(o, wo, rounded=True)
+        t_rest.append(time.perf_counter() - t)
+    # projections before attention measured whole; attention + output projection scaled by the sampled pair share
+    work = algorithmic_work(b)
+    cu = b.cu_q
+    req_of = np.searchsorted(cu, rows, side="right") - 1
+    pairs = (b.prefix_lens[req_of].astype(np.int64) + (rows - cu[req_of]) + 1).sum()
+    frac = min(1.0, float(pairs) / work["pairs"])
+    per_layer_s = float(np.median(t_pre)) + float(np.median(t_rest)) / frac
+    return {"value": round(per_layer_s * wl.num_layers * 1e6, 1), "unit": "us/step", "cores": threads,
+            "kind": "oracle",
+            "sample": f"projections of all {T} rows, then attention and output projection of {n} seeded rows "
+                      f"({frac * 100:.2f}% of the query-key pairs) scaled by that share; median of 3; "
+                      f"x{wl.num_layers} layer(s)",
             "cpu": _cpu_model()}
 
 

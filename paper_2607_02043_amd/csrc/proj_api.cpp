@@ -53,26 +53,37 @@ int cu_count() {
     return ncu;
 }
 
-// Tile shape of a GEMM launch: 128-wide column tiles (64 for fp32
-// activations), and the tallest row tile that still gives every CU a
-// workgroup.  MLA_GEMM_BM / MLA_GEMM_BN / MLA_GEMM_D override the choice
-// (for tuning; an override outside the instantiated shapes fails the launch).
+// Tile shape of a GEMM launch, from measurements of the layer's GEMMs at 256
+// to 4160 rows: the largest of the LDS-ring tiles 128 x 128 (2 stages),
+// 64 x 128 (3), 64 x 64 (4), 32 x 64 (6) that still gives at least 0.85
+// workgroups per CU (fewer leaves CUs idle; more is a second round of
+// workgroups for large tiles), and the register-staged 256 x 128 tile for the
+// narrow batched value up-projection once it has 1024 rows.  fp32 activations
+// use 64-column tiles.  MLA_GEMM_BM / MLA_GEMM_BN / MLA_GEMM_D override the
+// choice (for tuning; a shape that is not instantiated fails the launch).
 proj::GemmShape pick_shape(long long M, int N, int batch, int epi, bool a_f32) {
-    proj::GemmShape t{32, a_f32 ? proj::kBN : 128, 0, epi};
-    const int ncu = cu_count();
-    for (int bm : {128, 64}) {
-        const long long wgs = (M + bm - 1) / bm * ((N + t.bn - 1) / t.bn) * batch;
-        if (wgs >= ncu) {
-            t.bm = bm;
-            break;
+    struct Cand {
+        int bm, bn, depth;
+    };
+    static const Cand ring[] = {{128, 128, 2}, {64, 128, 3}, {64, 64, 4}, {32, 64, 6}};
+    proj::GemmShape t{32, 64, 6, epi};
+    const long long need = (long long)cu_count() * 85 / 100;
+    if (!a_f32 && N <= 128 && M >= 1024) {
+        t = {256, 128, 0, epi};
+    } else {
+        for (const Cand &c : ring) {
+            t = {c.bm, c.bn, c.depth, epi};
+            if ((M + c.bm - 1) / c.bm * ((N + c.bn - 1) / c.bn) * batch >= need) break;
         }
+    }
+    if (a_f32) {
+        t.bn = proj::kBN;
+        t.bm = std::min(t.bm, 128);
     }
     if (int v = env_int("MLA_GEMM_BM")) t.bm = v;
     if (!a_f32)
         if (int v = env_int("MLA_GEMM_BN")) t.bn = v;
-    if (t.bn == 64) t.depth = t.bm == 128 ? 3 : t.bm == 64 ? 4 : 6;
-    else t.depth = t.bm == 128 ? 2 : t.bm == 64 ? 3 : 4;
-    if (int v = env_int("MLA_GEMM_D")) t.depth = v;
+    if (const char *e = std::getenv("MLA_GEMM_D")) t.depth = std::atoi(e);
     return t;
 }
 
@@ -97,7 +108,7 @@ int check_weights(const mla_proj_weights *w, bool pre) {
 
 int launch(const GemmArgs &g, int epi, bool a_f32, int batch, hipStream_t s, const char *what) {
     const proj::GemmShape t = pick_shape(g.M, g.N, batch, epi, a_f32);
-    if (g.n_split % t.bn != 0)
+    if (g.n_split < g.N && g.n_split % t.bn != 0)
         return mla::set_error(MLA_ERR_INVALID_ARG, "%s GEMM: column split %d is not a multiple of the tile width %d",
                               what, g.n_split, t.bn);
     const hipError_t e = proj::launch_gemm(g, t, a_f32, batch, s);

@@ -58,10 +58,13 @@ struct RowArgs {
     double log2_base;         // log2 of the rope base
 };
 
-// Tile shape of one GEMM launch: bm x bn outputs per workgroup, `depth` LDS
-// stages.  Instantiated: bn 64 with (bm, depth) (32, 6), (64, 4), (128, 3);
-// bn 128 with (32, 4), (64, 3), (128, 2), (128, 3).  fp32 activations use
-// bn = 64, depth 2 and any bm of 32, 64, 128 (N a multiple of 64).
+// Tile shape of one GEMM launch: bm x bn outputs per workgroup; `depth` > 0
+// picks the LDS ring fed by direct loads with that many stages, 0 the
+// register-staged kernel.  Instantiated: ring, bn 64 with (bm, depth) (32, 6),
+// (64, 4), (128, 3); ring, bn 128 with (32, 4), (64, 3), (128, 2), (128, 3);
+// register-staged (bm, bn) (128, 256) and (256, 128) on eight waves, (32,
+// 128), (64, 128), (128, 128) on four.  fp32 activations use bn = 64 and any
+// bm of 32, 64, 128 (N a multiple of 64).
 struct GemmShape {
     int bm, bn, depth, epi;
 };

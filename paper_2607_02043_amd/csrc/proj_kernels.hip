@@ -197,6 +197,105 @@ __global__ __launch_bounds__(256) void gemm_ring_kernel(const GemmArgs g) {
     store_tile<EPI, MB, NB>(g, acc, m0 + wr + 4 * (lane >> 4), n0 + (wave & 1) * WN + (lane & 15), z);
 }
 
+// bf16 activations, register-staged: each thread loads its share of the
+// next two stages into registers (two register sets) while the current stage
+// is consumed from LDS, then writes the older set to the other LDS buffer.
+// Register loads stream from L2 well above the rate of direct global -> LDS
+// loads, and the projection GEMMs re-read both operands from L2 many times.
+// WR x WC waves, each computing a (BM / WR) x (BN / WC) block.
+template <int BM, int BN, int WR, int WC, int EPI>
+__global__ __launch_bounds__(64 * WR * WC) void gemm_reg_kernel(const GemmArgs g) {
+    constexpr int NT = 64 * WR * WC;
+    constexpr int ROWS = BM + BN;
+    constexpr int STAGE = ROWS * 8;  // 16-byte slots per stage
+    constexpr int LPT = STAGE / NT;  // loads per thread per stage
+    static_assert(STAGE % NT == 0, "a stage must split evenly over the threads");
+    constexpr int WM = BM / WR, MB = WM / 16;
+    constexpr int WN = BN / WC, NB = WN / 16;
+    __shared__ u32x4 sm[2 * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int m0, n0;
+    tile_of(g.M, g.N, BM, BN, &m0, &n0);
+    const int z = blockIdx.z;
+
+    // Chunk c = tid + NT i: row c / 8, k-chunk c % 8 (eight threads read one
+    // row's 128 bytes).  Rows past M or N repeat the last row; never stored.
+    const uint16_t *src[LPT];
+    int dst[LPT];
+    const uint16_t *bseg = n0 >= g.n_split ? g.b2 : g.b;
+    const int nbase = n0 >= g.n_split ? g.n_split : 0;
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) {
+        const int c = tid + NT * i;
+        const int row = c >> 3, kc = c & 7;
+        dst[i] = slot(row, kc);
+        if (row < BM) {
+            const int r = min(m0 + row, g.M - 1);
+            src[i] = static_cast<const uint16_t *>(g.a) + z * g.a_bstride + (long long)r * g.lda + kc * 8;
+        } else {
+            const int n = min(n0 + row - BM, g.N - 1) - nbase;
+            src[i] = bseg + z * g.b_bstride + (long long)n * g.ldb + kc * 8;
+        }
+    }
+    u32x4 r0[LPT], r1[LPT];
+    auto load = [&](u32x4(&r)[LPT], int st) {
+#pragma unroll
+        for (int i = 0; i < LPT; ++i) r[i] = *reinterpret_cast<const u32x4 *>(src[i] + st * kBK);
+    };
+    auto store = [&](const u32x4(&r)[LPT], int buf) {
+#pragma unroll
+        for (int i = 0; i < LPT; ++i) sm[buf * STAGE + dst[i]] = r[i];
+    };
+
+    f32x4 acc[MB][NB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int wr = (wave / WC) * WM;
+    const int wc = BM + (wave % WC) * WN;
+    auto compute = [&](int buf) {
+        const u32x4 *cur = sm + buf * STAGE;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            const int kc = s * 4 + (lane >> 4);
+            u32x4 fa[MB], fb[NB];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) fa[mb] = cur[slot(wr + mb * 16 + (lane & 15), kc)];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) fb[nb] = cur[slot(wc + nb * 16 + (lane & 15), kc)];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = mfma(fa[mb], fb[nb], acc[mb][nb]);
+        }
+    };
+
+    // Loads past the last stage re-read the last stage (in bounds, never
+    // stored): the loads stay unconditional, so the two register sets are not
+    // merged at branch joins (a copy of a register still being loaded waits
+    // for every load in flight).
+    const int nk = g.K / kBK;
+    load(r0, 0);
+    load(r1, min(1, nk - 1));
+    store(r0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+        // stage kt in buffer 0, stage kt + 1 in r1, stage kt + 2 loading into r0
+        load(r0, min(kt + 2, nk - 1));
+        compute(0);
+        if (kt + 1 < nk) store(r1, 1);
+        __syncthreads();
+        if (kt + 1 >= nk) break;
+        load(r1, min(kt + 3, nk - 1));
+        compute(1);
+        if (kt + 2 < nk) store(r0, 0);
+        __syncthreads();
+    }
+    store_tile<EPI, MB, NB>(g, acc, m0 + wr + 4 * (lane >> 4), n0 + (wc - BM) + (lane & 15), z);
+}
+
 // fp32 activations, converted to bf16 (nearest even) in registers; two LDS
 // stages, the next one held in registers while the current one is consumed.
 template <int BM, int EPI>
@@ -282,17 +381,29 @@ __global__ __launch_bounds__(256) void gemm_f32a_kernel(const GemmArgs g) {
 // Rope rotates pairs (2i, 2i + 1) by pos * base^(-2i / 64); the angle and its
 // sine and cosine are taken in double, the rotation in fp32.  The latent's
 // 512 compressed dims are RMS-normalised in fp32 and scaled by the gain.
+//
+// The request of a row is found by a wave-parallel search of cu_q: each
+// level, 64 lanes test 64 evenly spaced entries of the remaining range, so a
+// level costs one load per lane and the range shrinks 64-fold.
+__device__ __forceinline__ int request_of(const int32_t *cu_q, int num_reqs, int row, int lane) {
+    int lo = 0, n = num_reqs;  // answer in [lo, lo + n): the last r with cu_q[r] <= row
+    while (n > 1) {
+        const int step = (n + 63) >> 6;
+        const int idx = lo + lane * step;
+        const bool le = idx < lo + n && cu_q[idx] <= row;
+        const int k = __popcll(__ballot(le)) - 1;  // cu_q is increasing: the true lanes are a prefix
+        lo += k * step;
+        n = min(step, n - k * step);
+    }
+    return lo;
+}
+
 __global__ __launch_bounds__(256) void rope_norm_kernel(const RowArgs r) {
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= r.num_rows) return;
     const int lane = threadIdx.x & 63;
-    int lo = 0, hi = r.num_reqs - 1;  // last request whose first row is <= row
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (r.cu_q[mid] <= row) lo = mid;
-        else hi = mid - 1;
-    }
-    const int pos = r.prefix[lo] + row - r.cu_q[lo];
+    const int req = request_of(r.cu_q, r.num_reqs, row, lane);
+    const int pos = r.prefix[req] + row - r.cu_q[req];
 
     const int i = lane & 31;
     const double ang = (double)pos * exp2(-(double)(2 * i) / (double)kRope * r.log2_base);
@@ -335,6 +446,16 @@ hipError_t launch_ring(const GemmArgs &g, int epi, dim3 grid, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int BM, int BN, int WR, int WC>
+hipError_t launch_reg(const GemmArgs &g, int epi, dim3 grid, hipStream_t s) {
+    constexpr int NT = 64 * WR * WC;
+    if (epi == kStoreBf16) gemm_reg_kernel<BM, BN, WR, WC, kStoreBf16><<<grid, NT, 0, s>>>(g);
+    else if (epi == kStoreF32) gemm_reg_kernel<BM, BN, WR, WC, kStoreF32><<<grid, NT, 0, s>>>(g);
+    else if (epi == kQkvSplit) gemm_reg_kernel<BM, BN, WR, WC, kQkvSplit><<<grid, NT, 0, s>>>(g);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
 template <int BM>
 hipError_t launch_f32a(const GemmArgs &g, int epi, dim3 grid, hipStream_t s) {
     if (epi == kStoreBf16) gemm_f32a_kernel<BM, kStoreBf16><<<grid, 256, 0, s>>>(g);
@@ -364,6 +485,11 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int ba
     // BN = 64 tiles must not straddle a head (the split epilogue handles any column, the others any N)
     const int key = t.bm * 1000 + t.bn * 10 + t.depth;
     switch (key) {
+        case 128 * 1000 + 256 * 10 + 0: return launch_reg<128, 256, 2, 4>(g, t.epi, grid, s);
+        case 256 * 1000 + 128 * 10 + 0: return launch_reg<256, 128, 4, 2>(g, t.epi, grid, s);
+        case 128 * 1000 + 128 * 10 + 0: return launch_reg<128, 128, 2, 2>(g, t.epi, grid, s);
+        case 64 * 1000 + 128 * 10 + 0: return launch_reg<64, 128, 2, 2>(g, t.epi, grid, s);
+        case 32 * 1000 + 128 * 10 + 0: return launch_reg<32, 128, 2, 2>(g, t.epi, grid, s);
         case 32 * 1000 + 64 * 10 + 6: return launch_ring<32, 64, 6>(g, t.epi, grid, s);
         case 64 * 1000 + 64 * 10 + 4: return launch_ring<64, 64, 4>(g, t.epi, grid, s);
         case 128 * 1000 + 64 * 10 + 3: return launch_ring<128, 64, 3>(g, t.epi, grid, s);

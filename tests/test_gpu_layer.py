@@ -42,7 +42,8 @@ def weights():
 
 # GEMM tile shapes (rows, columns, LDS stages) forced through the library's
 # tuning variables; None keeps the library's own choice.
-SHAPES = [None, (32, 64, 6), (64, 64, 4), (128, 64, 3), (32, 128, 4), (64, 128, 3), (128, 128, 2), (128, 128, 3)]
+SHAPES = [None, (32, 64, 6), (64, 64, 4), (128, 64, 3), (32, 128, 4), (64, 128, 3), (128, 128, 2), (128, 128, 3),
+          (32, 128, 0), (64, 128, 0), (128, 128, 0), (128, 256, 0), (256, 128, 0)]
 _VARS = ("MLA_GEMM_BM", "MLA_GEMM_BN", "MLA_GEMM_D")
 
 
@@ -154,7 +155,8 @@ def test_pre_attn_parity(case, gemm_shape, weights):
     check_bf16(lat_gpu, lat_ref, lat_exact, "new latents", mags=m_lat)
 
 
-@pytest.mark.parametrize("gemm_shape", [None, (32, 64, 6), (64, 128, 3), (128, 128, 2)], indirect=True)
+@pytest.mark.parametrize("gemm_shape", [None, (32, 64, 6), (64, 128, 3), (128, 128, 2), (32, 128, 0), (128, 256, 0)],
+                         indirect=True)
 @pytest.mark.parametrize("attn_bf16,out_bf16", [(False, False), (True, False), (False, True)])
 def test_post_attn_parity(attn_bf16, out_bf16, gemm_shape, weights):
     import torch
