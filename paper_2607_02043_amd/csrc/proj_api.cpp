@@ -161,10 +161,10 @@ int pre_attn(const mla_batch *batch, int T, const uint16_t *hidden, const mla_pr
     r.num_rows = T;
     r.eps = w->rms_eps;
     r.log2_base = std::log2((double)w->rope_base);
-    hipError_t e = launch_rope_norm(r, s);
-    if (e != hipSuccess) return mla::set_error(MLA_ERR_HIP, "rope / norm kernel launch: %s", hipGetErrorString(e));
-
     GemmArgs u{};
+    // the rope / norm rows ride along as extra workgroups of the absorption launch
+    u.rope = r;
+    u.rope_wgs = rope_norm_wgs(T);
     u.a = qn;
     u.lda = kHeads * kNope;
     u.a_bstride = kNope;

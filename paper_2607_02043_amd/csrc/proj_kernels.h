@@ -25,6 +25,20 @@ enum Epilogue : int {
     kQkvSplit = 2,   // first projection: nope -> qn bf16, rope -> qpe fp32, latent -> kvf fp32
 };
 
+struct RowArgs {
+    const float *qpe;         // [T][16][64]
+    const float *kvf;         // [T][576]
+    const uint16_t *gamma;    // [512] bf16
+    const int32_t *cu_q;      // [R + 1]
+    const int32_t *prefix;    // [R]
+    uint16_t *q_abs;          // [T][16][576]: writes dims 512..575 of every head
+    uint16_t *latent;         // [T][576]
+    int32_t num_reqs;
+    int32_t num_rows;
+    float eps;
+    double log2_base;         // log2 of the rope base
+};
+
 // C[z][m][n] = sum_k A[z][m][k] * B[z][n][k]: both operands K-contiguous.
 // Element strides; z = blockIdx.z.  Columns n >= n_split take their B rows
 // from b2 (row n - n_split), so two weight matrices act as one.
@@ -42,21 +56,13 @@ struct GemmArgs {
     uint16_t *qn;         // [M][16][128] bf16
     float *qpe;           // [M][16][64]
     float *kvf;           // [M][576]
+    // Optional rope / norm rows run by rope_wgs extra workgroups of the
+    // launch (blockIdx.x past the tiles, z = 0): independent work that
+    // overlaps the GEMM instead of taking a launch of its own.
+    RowArgs rope;
+    int rope_wgs;
 };
 
-struct RowArgs {
-    const float *qpe;         // [T][16][64]
-    const float *kvf;         // [T][576]
-    const uint16_t *gamma;    // [512] bf16
-    const int32_t *cu_q;      // [R + 1]
-    const int32_t *prefix;    // [R]
-    uint16_t *q_abs;          // [T][16][576]: writes dims 512..575 of every head
-    uint16_t *latent;         // [T][576]
-    int32_t num_reqs;
-    int32_t num_rows;
-    float eps;
-    double log2_base;         // log2 of the rope base
-};
 
 // Tile shape of one GEMM launch: bm x bn outputs per workgroup; `depth` > 0
 // picks the LDS ring fed by direct loads with that many stages, 0 the
@@ -69,8 +75,9 @@ struct GemmShape {
     int bm, bn, depth, epi;
 };
 
-// The launch covers ceil(M / bm) * ceil(N / bn) tiles x batch.
+// The launch covers ceil(M / bm) * ceil(N / bn) tiles x batch, plus
+// g.rope_wgs workgroups of rope / norm rows (four rows each).
 hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int batch, hipStream_t s);
-hipError_t launch_rope_norm(const RowArgs &r, hipStream_t s);
+inline int rope_norm_wgs(int num_rows) { return (num_rows + 3) / 4; }
 
 }  // namespace proj

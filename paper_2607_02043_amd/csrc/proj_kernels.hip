@@ -96,6 +96,66 @@ __device__ __forceinline__ void store_tile(const GemmArgs &g, const f32x4 (&acc)
     }
 }
 
+// One wave per row.  Position of row t of request r: prefix_r + (t - cu_q[r]).
+// Rope rotates pairs (2i, 2i + 1) by pos * base^(-2i / 64); the angle and its
+// sine and cosine are taken in double, the rotation in fp32.  The latent's
+// 512 compressed dims are RMS-normalised in fp32 and scaled by the gain.
+//
+// The request of a row is found by a wave-parallel search of cu_q: each
+// level, 64 lanes test 64 evenly spaced entries of the remaining range, so a
+// level costs one load per lane and the range shrinks 64-fold.
+__device__ __forceinline__ int request_of(const int32_t *cu_q, int num_reqs, int row, int lane) {
+    int lo = 0, n = num_reqs;  // answer in [lo, lo + n): the last r with cu_q[r] <= row
+    while (n > 1) {
+        const int step = (n + 63) >> 6;
+        const int idx = lo + lane * step;
+        const bool le = idx < lo + n && cu_q[idx] <= row;
+        const int k = __popcll(__ballot(le)) - 1;  // cu_q is increasing: the true lanes are a prefix
+        lo += k * step;
+        n = min(step, n - k * step);
+    }
+    return lo;
+}
+
+__device__ __forceinline__ void rope_norm_rows(const RowArgs &r, int wg) {
+    const int row = wg * 4 + (threadIdx.x >> 6);
+    if (row >= r.num_rows) return;
+    const int lane = threadIdx.x & 63;
+    const int req = request_of(r.cu_q, r.num_reqs, row, lane);
+    const int pos = r.prefix[req] + row - r.cu_q[req];
+
+    const int i = lane & 31;
+    const double ang = (double)pos * exp2(-(double)(2 * i) / (double)kRope * r.log2_base);
+    double sd, cd;
+    sincos(ang, &sd, &cd);
+    const float sn = (float)sd, cs = (float)cd;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const int h = (lane >> 5) + 2 * k;
+        const float2 x = *reinterpret_cast<const float2 *>(r.qpe + ((long long)row * kHeads + h) * kRope + 2 * i);
+        *reinterpret_cast<uint32_t *>(r.q_abs + ((long long)row * kHeads + h) * kDqk + kLatent + 2 * i) =
+            pack2(x.x * cs - x.y * sn, x.x * sn + x.y * cs);
+    }
+    if (lane < 32) {
+        const float2 x = *reinterpret_cast<const float2 *>(r.kvf + (long long)row * kDqk + kLatent + 2 * i);
+        *reinterpret_cast<uint32_t *>(r.latent + (long long)row * kDqk + kLatent + 2 * i) =
+            pack2(x.x * cs - x.y * sn, x.x * sn + x.y * cs);
+    }
+
+    const float *src = r.kvf + (long long)row * kDqk + lane * 8;
+    const float4 a = *reinterpret_cast<const float4 *>(src), b = *reinterpret_cast<const float4 *>(src + 4);
+    float ss = a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    const float inv = 1.0f / sqrtf(ss / (float)kLatent + r.eps);
+    const u32x4 gw = *reinterpret_cast<const u32x4 *>(r.gamma + lane * 8);
+    const u32x4 y = {pack2(a.x * inv * bf16_lo(gw[0]), a.y * inv * bf16_hi(gw[0])),
+                     pack2(a.z * inv * bf16_lo(gw[1]), a.w * inv * bf16_hi(gw[1])),
+                     pack2(b.x * inv * bf16_lo(gw[2]), b.y * inv * bf16_hi(gw[2])),
+                     pack2(b.z * inv * bf16_lo(gw[3]), b.w * inv * bf16_hi(gw[3]))};
+    *reinterpret_cast<u32x4 *>(r.latent + (long long)row * kDqk + lane * 8) = y;
+}
+
 // Tile of workgroup blockIdx.x.  Tiles are ordered in groups of kGroup row
 // tiles: within a group the row tile varies fastest, then the column tile.
 // Workgroups are dealt to the 8 XCDs round-robin, so the order is renumbered
@@ -118,6 +178,15 @@ __device__ __forceinline__ void tile_of(int M, int N, int BM, int BN, int *m0, i
     *n0 = (r / gm) * BN;
 }
 
+// Workgroups past the tiles run the launch's rope / norm rows (z = 0) or
+// nothing; true when this workgroup is one of them.
+__device__ __forceinline__ bool is_rope_wg(const GemmArgs &g, int BM, int BN) {
+    const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+    if ((int)blockIdx.x < tiles) return false;
+    if (blockIdx.z == 0) rope_norm_rows(g.rope, blockIdx.x - tiles);
+    return true;
+}
+
 // bf16 activations.  D-stage LDS ring filled by direct loads; four waves in
 // a 2 x 2 grid, each computing a (BM / 2) x (BN / 2) block.
 template <int BM, int BN, int D, int EPI>
@@ -130,6 +199,7 @@ __global__ __launch_bounds__(256) void gemm_ring_kernel(const GemmArgs g) {
     static_assert(STAGE % 256 == 0, "a stage must split evenly over four waves");
     __shared__ __attribute__((aligned(1024))) u32x4 ring[D * STAGE];
 
+    if (is_rope_wg(g, BM, BN)) return;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int m0, n0;
     tile_of(g.M, g.N, BM, BN, &m0, &n0);
@@ -214,6 +284,7 @@ __global__ __launch_bounds__(64 * WR * WC) void gemm_reg_kernel(const GemmArgs g
     constexpr int WN = BN / WC, NB = WN / 16;
     __shared__ u32x4 sm[2 * STAGE];
 
+    if (is_rope_wg(g, BM, BN)) return;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     int m0, n0;
     tile_of(g.M, g.N, BM, BN, &m0, &n0);
@@ -377,66 +448,6 @@ __global__ __launch_bounds__(256) void gemm_f32a_kernel(const GemmArgs g) {
     store_tile<EPI, MB, 2>(g, acc, m0 + wr + 4 * (lane >> 4), n0 + (wave & 1) * 32 + (lane & 15), z);
 }
 
-// One wave per row.  Position of row t of request r: prefix_r + (t - cu_q[r]).
-// Rope rotates pairs (2i, 2i + 1) by pos * base^(-2i / 64); the angle and its
-// sine and cosine are taken in double, the rotation in fp32.  The latent's
-// 512 compressed dims are RMS-normalised in fp32 and scaled by the gain.
-//
-// The request of a row is found by a wave-parallel search of cu_q: each
-// level, 64 lanes test 64 evenly spaced entries of the remaining range, so a
-// level costs one load per lane and the range shrinks 64-fold.
-__device__ __forceinline__ int request_of(const int32_t *cu_q, int num_reqs, int row, int lane) {
-    int lo = 0, n = num_reqs;  // answer in [lo, lo + n): the last r with cu_q[r] <= row
-    while (n > 1) {
-        const int step = (n + 63) >> 6;
-        const int idx = lo + lane * step;
-        const bool le = idx < lo + n && cu_q[idx] <= row;
-        const int k = __popcll(__ballot(le)) - 1;  // cu_q is increasing: the true lanes are a prefix
-        lo += k * step;
-        n = min(step, n - k * step);
-    }
-    return lo;
-}
-
-__global__ __launch_bounds__(256) void rope_norm_kernel(const RowArgs r) {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= r.num_rows) return;
-    const int lane = threadIdx.x & 63;
-    const int req = request_of(r.cu_q, r.num_reqs, row, lane);
-    const int pos = r.prefix[req] + row - r.cu_q[req];
-
-    const int i = lane & 31;
-    const double ang = (double)pos * exp2(-(double)(2 * i) / (double)kRope * r.log2_base);
-    double sd, cd;
-    sincos(ang, &sd, &cd);
-    const float sn = (float)sd, cs = (float)cd;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        const int h = (lane >> 5) + 2 * k;
-        const float2 x = *reinterpret_cast<const float2 *>(r.qpe + ((long long)row * kHeads + h) * kRope + 2 * i);
-        *reinterpret_cast<uint32_t *>(r.q_abs + ((long long)row * kHeads + h) * kDqk + kLatent + 2 * i) =
-            pack2(x.x * cs - x.y * sn, x.x * sn + x.y * cs);
-    }
-    if (lane < 32) {
-        const float2 x = *reinterpret_cast<const float2 *>(r.kvf + (long long)row * kDqk + kLatent + 2 * i);
-        *reinterpret_cast<uint32_t *>(r.latent + (long long)row * kDqk + kLatent + 2 * i) =
-            pack2(x.x * cs - x.y * sn, x.x * sn + x.y * cs);
-    }
-
-    const float *src = r.kvf + (long long)row * kDqk + lane * 8;
-    const float4 a = *reinterpret_cast<const float4 *>(src), b = *reinterpret_cast<const float4 *>(src + 4);
-    float ss = a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w + b.x * b.x + b.y * b.y + b.z * b.z + b.w * b.w;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
-    const float inv = 1.0f / sqrtf(ss / (float)kLatent + r.eps);
-    const u32x4 gw = *reinterpret_cast<const u32x4 *>(r.gamma + lane * 8);
-    const u32x4 y = {pack2(a.x * inv * bf16_lo(gw[0]), a.y * inv * bf16_hi(gw[0])),
-                     pack2(a.z * inv * bf16_lo(gw[1]), a.w * inv * bf16_hi(gw[1])),
-                     pack2(b.x * inv * bf16_lo(gw[2]), b.y * inv * bf16_hi(gw[2])),
-                     pack2(b.z * inv * bf16_lo(gw[3]), b.w * inv * bf16_hi(gw[3]))};
-    *reinterpret_cast<u32x4 *>(r.latent + (long long)row * kDqk + lane * 8) = y;
-}
-
 template <int BM, int BN, int D>
 hipError_t launch_ring(const GemmArgs &g, int epi, dim3 grid, hipStream_t s) {
     if (epi == kStoreBf16) gemm_ring_kernel<BM, BN, D, kStoreBf16><<<grid, 256, 0, s>>>(g);
@@ -470,10 +481,11 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int ba
     if (g.M <= 0 || batch <= 0) return hipSuccess;
     if (g.K % kBK != 0 || g.K <= 0 || g.N <= 0) return hipErrorInvalidValue;
     const int bn = a_f32 ? kBN : t.bn;
-    const long long tiles = (long long)((g.M + t.bm - 1) / t.bm) * ((g.N + bn - 1) / bn);
-    if (tiles > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const long long tiles = (long long)((g.M + t.bm - 1) / t.bm) * ((g.N + bn - 1) / bn) + g.rope_wgs;
+    if (tiles > 0x7FFFFFFF || g.rope_wgs < 0) return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles, 1, (unsigned)batch);
     if (a_f32) {
+        if (g.rope_wgs != 0) return hipErrorInvalidValue;
         if (g.N % kBN != 0) return hipErrorInvalidValue;
         switch (t.bm) {
             case 32: return launch_f32a<32>(g, t.epi, grid, s);
@@ -501,10 +513,5 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int ba
     }
 }
 
-hipError_t launch_rope_norm(const RowArgs &r, hipStream_t s) {
-    if (r.num_rows <= 0) return hipSuccess;
-    rope_norm_kernel<<<(r.num_rows + 3) / 4, 256, 0, s>>>(r);
-    return hipGetLastError();
-}
 
 }  // namespace proj
