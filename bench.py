@@ -229,7 +229,10 @@ def layer_work(batch):
 def layer_bench(args, wl):
     """Whole attention layers (mla_attention_layer) of the workload: W warm-up
     steps, K timed steps of all layers, then the same steps again with HIP
-    events around the three phases (projections before, mixed step, after)."""
+    events around the three phases (projections before, mixed step, after).
+    The phases are those of the absorbed sequence, every row on the absorbed
+    kernel; the layer call itself may send long chunk requests to the
+    multi-head path instead, so the phases need not add up to the step."""
     import torch
 
     import paper_2607_02043_amd as mla
@@ -283,7 +286,8 @@ def layer_bench(args, wl):
     torch.cuda.synchronize()
     us_per_step = (time.perf_counter() - t_start) / args.steps * 1e6
 
-    # phases, with HIP events on the stream: the same calls mla_attention_layer makes
+    # phases, with HIP events on the stream: the calls mla_attention_layer makes
+    # when no request takes the multi-head path
     q = torch.empty((T, 16, 576), dtype=torch.int16, device=dev)
     lat = torch.empty((T, 576), dtype=torch.int16, device=dev)
     o = torch.empty((T, 16, 512), dtype=torch.bfloat16, device=dev)

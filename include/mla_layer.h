@@ -39,6 +39,9 @@
  *                             up-projection of head h, transposed once when
  *                             weights are loaded
  *   w_uv    [16][128][512]    w_uv[h][d][c] = W_UV[h][d][c]
+ *   w_uk    [16][128][512]    w_uk[h][d][c] = W_UK[h][d][c], the model's own
+ *                             layout (mla_attention_layer only; may be NULL
+ *                             when no chunk request takes the multi-head path)
  *   w_o     [2048][16 * 128]  output projection
  *
  * Conventions, errors and streams are those of mla_step.h.  Workspaces are
@@ -65,6 +68,7 @@ typedef struct mla_proj_weights {
     const uint16_t *kv_gain;
     const uint16_t *w_uk_t;
     const uint16_t *w_uv;
+    const uint16_t *w_uk;
     const uint16_t *w_o;
     float rms_eps;   /* > 0 and finite (1e-6 for the served model) */
     float rope_base; /* > 1 and finite (10000) */
@@ -102,6 +106,15 @@ size_t mla_layer_workspace_bytes(const mla_batch *batch);
 /* One attention layer of the step: mla_pre_attn, mixed_step (append of the
  * new latents + attention, output rounded to bf16, which is where the value
  * up-projection rounds it anyway) and mla_post_attn, enqueued on one stream.
+ * A chunk request of c >= 256 rows at prefix p whose query-key pairs per key,
+ * c (p + c / 2) / (p + c), reach 1200 takes the multi-head form instead of
+ * the absorbed one (same result up to rounding; about 30% of the flops per
+ * query-key pair): its keys 0 .. p + c - 1 are up-projected once to per-head
+ * keys W_UK c and values W_UV c (fp16), then causal attention runs per head
+ * over 128 + 64 query / key dims and 128 value dims; the other rows run on
+ * the absorbed kernel.  The environment variables MLA_LAYER_MHA_MIN (row
+ * minimum, >= 2; set alone it drops the pairs rule) and MLA_LAYER_MHA_PAIRS
+ * (>= 0) override the two numbers.
  *   hidden    DEVICE bf16 [T][2048]
  *   kv_cache  DEVICE bf16 [num_pages][P][576], updated with the step's latents
  *   out       DEVICE [T][2048] fp32 or bf16 (out_dtype)

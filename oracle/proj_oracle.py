@@ -173,16 +173,23 @@ def attend_logical(q_abs: np.ndarray, keys: np.ndarray, prefix: int, scale: floa
     return out
 
 
-def layer_exact(q_lens, prefix_lens, hidden, W: Weights, cached: List[np.ndarray], scale: float) -> np.ndarray:
+def layer_exact(q_lens, prefix_lens, hidden, W: Weights, cached: List[np.ndarray], scale: float,
+                rows: Optional[Sequence[int]] = None) -> np.ndarray:
     """The layer in float64 with nothing rounded.  cached[r]: request r's
-    cached latents [p_r][576] (float64), in logical order."""
+    cached latents [p_r][576] (float64), in logical order.  rows: only these
+    output rows (every row's latent is still formed: later rows attend them)."""
     pos = positions(q_lens, prefix_lens)
     q_abs, lat = pre_attn(pos, hidden, W, rounded=False)
-    o = np.empty((len(pos), HEADS, LATENT))
+    want = list(range(len(pos))) if rows is None else [int(x) for x in rows]
+    where = {t: k for k, t in enumerate(want)}
+    o = np.empty((len(want), HEADS, LATENT))
     row = 0
     for r, (c, p) in enumerate(zip(q_lens, prefix_lens)):
+        c, p = int(c), int(p)
         keys = np.concatenate([np.asarray(cached[r], dtype=np.float64).reshape(p, DQK), lat[row:row + c]])
-        o[row:row + c] = attend_logical(q_abs[row:row + c], keys, p, scale)
+        for i in range(c):
+            if row + i in where:  # row i of the request sees keys 0 .. p + i
+                o[where[row + i]] = attend_logical(q_abs[row + i:row + i + 1], keys, p + i, scale)[0]
         row += c
     return post_attn(o, W, rounded=False)
 

@@ -59,6 +59,7 @@ class mla_proj_weights(ctypes.Structure):
         ("kv_gain", ctypes.c_void_p),
         ("w_uk_t", ctypes.c_void_p),
         ("w_uv", ctypes.c_void_p),
+        ("w_uk", ctypes.c_void_p),
         ("w_o", ctypes.c_void_p),
         ("rms_eps", ctypes.c_float),
         ("rope_base", ctypes.c_float),
@@ -220,7 +221,7 @@ class DeviceProjWeights:
     projection weights, from a workloads.ProjWeights or any object with the
     same fields (numpy uint16 arrays in the C ABI's layouts)."""
 
-    FIELDS = ("w_q", "w_dkv", "kv_gain", "w_uk_t", "w_uv", "w_o")
+    FIELDS = ("w_q", "w_dkv", "kv_gain", "w_uk_t", "w_uv", "w_uk", "w_o")
 
     def __init__(self, weights, device="cuda"):
         import torch

@@ -223,7 +223,7 @@ double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
 //    dec_unit_tiles; with chunk work present the units are small so that
 //    they fill the tail of the queue.
 // The device recomputes the same mapping from the device copies of the lengths.
-int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
+int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkRoute route, Plan *pl) {
     const long long P = b->page_size;
     long long cap = ((long long)(mla::kPageWindow - 1) * P) / 64 * 64;  // keys per chunk item
     if (cap < 64) cap = 64;
@@ -238,7 +238,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
             const long long nt = ceil_div_ll(p + 1, KT);
             dec.push_back(DecReq{dec_total, nt, p});
             dec_total += nt;
-        } else {
+        } else if (!route.multi_head(p, c)) {
             chunks.emplace_back(p, c);
         }
     }
@@ -404,7 +404,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, Plan *pl) {
 // The plan depends only on the host lengths, the page size and the CU count;
 // the last one is kept per thread so a steady stream of identical steps
 // plans once.
-int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
+int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute route = mla::kAbsorbAll) {
     *pl = Plan{};
     if (sh.R == 0) return MLA_OK;
     int st = MLA_OK;
@@ -413,26 +413,28 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl) {
     thread_local std::vector<int32_t> key;
     thread_local Plan cached;
     thread_local bool have = false;
-    const size_t n = 4 + 2 * (size_t)sh.R;
+    const size_t n = 6 + 2 * (size_t)sh.R;
     bool same = have && key.size() == n && key[0] == b->page_size && key[1] == ncu && key[2] == sh.R &&
-                key[3] == b->max_pages_per_req;
+                key[3] == b->max_pages_per_req && key[4] == route.min_rows && key[5] == route.pair_keys;
     if (same) {
-        same = std::memcmp(key.data() + 4, b->q_lens, sh.R * sizeof(int32_t)) == 0 &&
-               std::memcmp(key.data() + 4 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t)) == 0;
+        same = std::memcmp(key.data() + 6, b->q_lens, sh.R * sizeof(int32_t)) == 0 &&
+               std::memcmp(key.data() + 6 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t)) == 0;
     }
     if (same) {
         *pl = cached;
         return MLA_OK;
     }
-    st = make_plan_uncached(b, sh, ncu, pl);
+    st = make_plan_uncached(b, sh, ncu, route, pl);
     if (st != MLA_OK) return st;
     key.resize(n);
     key[0] = b->page_size;
     key[1] = ncu;
     key[2] = sh.R;
     key[3] = b->max_pages_per_req;
-    std::memcpy(key.data() + 4, b->q_lens, sh.R * sizeof(int32_t));
-    std::memcpy(key.data() + 4 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t));
+    key[4] = route.min_rows;
+    key[5] = route.pair_keys;
+    std::memcpy(key.data() + 6, b->q_lens, sh.R * sizeof(int32_t));
+    std::memcpy(key.data() + 6 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t));
     cached = *pl;
     have = true;
     return MLA_OK;
@@ -450,13 +452,13 @@ int set_error(int code, const char *fmt, ...) {
     return code;
 }
 
-int attn_workspace(const mla_batch *batch, size_t *bytes) {
+int attn_workspace(const mla_batch *batch, size_t *bytes, ChunkRoute route) {
     *bytes = 0;
     Shape sh;
     int st = check_batch(batch, &sh);
     if (st != MLA_OK || sh.R == 0) return st;
     Plan pl;
-    st = make_plan(batch, sh, &pl);
+    st = make_plan(batch, sh, &pl, route);
     if (st == MLA_OK) *bytes = pl.bytes;
     return st;
 }
@@ -515,7 +517,7 @@ namespace {
 // Shared by mixed_step_attn (new_latents == NULL) and mixed_step (fused append).
 int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
            float softmax_scale, void *out, int32_t out_dtype, float *lse, void *workspace, size_t workspace_bytes,
-           void *stream) {
+           void *stream, mla::ChunkRoute route = mla::kAbsorbAll) {
     Shape sh;
     int st = check_batch(batch, &sh);
     if (st != MLA_OK || sh.R == 0) return st;
@@ -531,7 +533,7 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
         return fail(MLA_ERR_INVALID_ARG, "q / kv_cache / out / workspace must be 16-byte aligned");
     if (reinterpret_cast<uintptr_t>(lse) & 3) return fail(MLA_ERR_INVALID_ARG, "lse must be 4-byte aligned");
     Plan pl;
-    st = make_plan(batch, sh, &pl);
+    st = make_plan(batch, sh, &pl, route);
     if (st != MLA_OK) return st;
     if (pl.bytes > 0 && (!workspace || workspace_bytes < pl.bytes))
         return fail(MLA_ERR_WORKSPACE, "workspace of %zu bytes at %p; this batch needs %zu", workspace_bytes,
@@ -567,6 +569,7 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
     a.merge_hsplit = pl.merge_hsplit;
     a.dec_total_tiles = pl.dec_total_tiles;
     a.out_bf16 = out_dtype == MLA_OUT_BF16 ? 1 : 0;
+    a.route = route;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = mla::launch_attention(a, s);
     if (e != hipSuccess) return hip_fail(e, "attention kernel launch");
@@ -578,6 +581,17 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
 }
 
 }  // namespace
+
+namespace mla {
+
+int attend_rows(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
+                float softmax_scale, void *out, int32_t out_dtype, void *workspace, size_t workspace_bytes, void *stream,
+                ChunkRoute route) {
+    return attend(batch, q, new_latents, kv_cache, softmax_scale, out, out_dtype, nullptr, workspace, workspace_bytes,
+                  stream, route);
+}
+
+}  // namespace mla
 
 extern "C" {
 

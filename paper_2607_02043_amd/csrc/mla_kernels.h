@@ -1,5 +1,6 @@
 // Launch-side description of the kernels of libmlastep (host <-> device).
 #pragma once
+#include "chunk_route.h"
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -51,6 +52,7 @@ struct AttnArgs {
     int32_t grid;              // persistent workgroups of the attention launch
     int32_t merge_hsplit;      // merge workgroups per split decode row (1, 4 or 8: heads split among them)
     int32_t out_bf16;
+    ChunkRoute route;          // chunk requests it sends to the multi-head path are left out of this launch
 };
 
 struct AppendArgs {

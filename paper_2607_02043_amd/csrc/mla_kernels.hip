@@ -243,8 +243,9 @@ __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn
 
 struct ChunkCount {
     int ks;
+    ChunkRoute route;
     __device__ int operator()(int p, int c) const {
-        return c > 1 ? ceil_div(c, kChunkBlockTokens) * ceil_div(p + c, ks) : 0;
+        return c > 1 && !route.multi_head(p, c) ? ceil_div(c, kChunkBlockTokens) * ceil_div(p + c, ks) : 0;
     }
 };
 
@@ -988,7 +989,7 @@ __device__ __forceinline__ void lds_dma16_sbase_imm(const void *sbase, uint32_t 
 // item again with exact = true (the exact maxima wait in LDS).
 __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages, bool exact) {
     Located lc;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return false;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk, a.route}, s_tmp, lc)) return false;
     const ChunkItem it = decode_chunk_item(a, lc);
     TRACE(1);
     const int r = it.r;
@@ -1362,7 +1363,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     // 0 merges that row over the block's splits
     const int item = (b - n_dec) / kChunkBlockTokens, j = (b - n_dec) % kChunkBlockTokens;
     Located lc;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk}, s_tmp, lc)) return;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk, a.route}, s_tmp, lc)) return;
     const ChunkItem it = decode_chunk_item(a, lc);
     if (it.ks != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr || j >= it.i1 - it.i0) return;
     if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;

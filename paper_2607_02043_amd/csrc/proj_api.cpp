@@ -182,6 +182,46 @@ int pre_attn(const mla_batch *batch, int T, const uint16_t *hidden, const mla_pr
     return launch(u, kStoreBf16, false, kHeads, s, "query absorption");
 }
 
+// o[r] = concat_h W_UV[h] attn_out[r][h] for rows r0 .. r1 - 1 (bf16 o [T][2048]).
+int uv_gemm(int r0, int r1, const void *attn_out, bool a_f32, const mla_proj_weights *w, uint16_t *o, hipStream_t s) {
+    using namespace proj;
+    if (r1 <= r0) return MLA_OK;
+    GemmArgs v{};
+    v.a = static_cast<const char *>(attn_out) + (size_t)r0 * kHeads * kLatent * (a_f32 ? 4 : 2);
+    v.lda = (long long)kHeads * kLatent;
+    v.a_bstride = kLatent;
+    v.b = w->w_uv;
+    v.b2 = w->w_uv;
+    v.ldb = kLatent;
+    v.b_bstride = (long long)kVHead * kLatent;
+    v.n_split = kVHead;
+    v.M = r1 - r0;
+    v.N = kVHead;
+    v.K = kLatent;
+    v.c = o + (size_t)r0 * kOCols;
+    v.ldc = kOCols;
+    v.c_bstride = kVHead;
+    return launch(v, kStoreBf16, a_f32, kHeads, s, "value up-projection");
+}
+
+// out = o W_o^T for T rows.
+int o_gemm(int T, const uint16_t *o, const mla_proj_weights *w, void *out, int32_t out_dtype, hipStream_t s) {
+    using namespace proj;
+    GemmArgs g{};
+    g.a = o;
+    g.lda = kOCols;
+    g.b = w->w_o;
+    g.b2 = w->w_o;
+    g.ldb = kOCols;
+    g.n_split = kHidden;
+    g.M = T;
+    g.N = kHidden;
+    g.K = kOCols;
+    g.c = out;
+    g.ldc = kHidden;
+    return launch(g, out_dtype == MLA_OUT_F32 ? kStoreF32 : kStoreBf16, false, 1, s, "output projection");
+}
+
 int post_attn(int T, const void *attn_out, int32_t attn_dtype, const mla_proj_weights *w, void *out,
               int32_t out_dtype, void *workspace, size_t workspace_bytes, hipStream_t s) {
     using namespace proj;
@@ -200,48 +240,46 @@ int post_attn(int T, const void *attn_out, int32_t attn_dtype, const mla_proj_we
         return mla::set_error(MLA_ERR_WORKSPACE, "workspace of %zu bytes at %p; %d rows need %zu", workspace_bytes,
                               workspace, T, L.total);
     uint16_t *o = reinterpret_cast<uint16_t *>(static_cast<char *>(workspace) + L.o);
-
-    GemmArgs v{};
-    v.a = attn_out;
-    v.lda = (long long)kHeads * kLatent;
-    v.a_bstride = kLatent;
-    v.b = w->w_uv;
-    v.b2 = w->w_uv;
-    v.ldb = kLatent;
-    v.b_bstride = (long long)kVHead * kLatent;
-    v.n_split = kVHead;
-    v.M = T;
-    v.N = kVHead;
-    v.K = kLatent;
-    v.c = o;
-    v.ldc = kOCols;
-    v.c_bstride = kVHead;
-    st = launch(v, kStoreBf16, attn_dtype == MLA_OUT_F32, kHeads, s, "value up-projection");
+    st = uv_gemm(0, T, attn_out, attn_dtype == MLA_OUT_F32, w, o, s);
     if (st != MLA_OK) return st;
+    return o_gemm(T, o, w, out, out_dtype, s);
+}
 
-    GemmArgs g{};
-    g.a = o;
-    g.lda = kOCols;
-    g.b = w->w_o;
-    g.b2 = w->w_o;
-    g.ldb = kOCols;
-    g.n_split = kHidden;
-    g.M = T;
-    g.N = kHidden;
-    g.K = kOCols;
-    g.c = out;
-    g.ldc = kHidden;
-    return launch(g, out_dtype == MLA_OUT_F32 ? kStoreF32 : kStoreBf16, false, 1, s, "output projection");
+// Which chunk requests take the multi-head path in the layer (up-projected
+// keys and values, 192 + 128 dims per head: about 30% of the absorbed form's
+// flops per query-key pair, for one up-projection of the request's keys).
+// Measured on MI355X, the multi-head kernel saves about 9 ps per query-key
+// pair (all 16 heads) against the absorbed one and the up-projection costs
+// about 7.7 ns per key, so it pays from about 850 pairs per key; 1200 leaves
+// room for its launches and for the short blocks of small chunks.
+// MLA_LAYER_MHA_MIN (>= 2) and MLA_LAYER_MHA_PAIRS (>= 0) override the two
+// numbers; with MLA_LAYER_MHA_MIN alone every request of that many rows
+// takes the path.
+constexpr int kMhaMinRows = 256;
+constexpr int kMhaPairsPerKey = 1200;
+
+mla::ChunkRoute mha_route() {
+    const int m = env_int("MLA_LAYER_MHA_MIN"), k = env_int("MLA_LAYER_MHA_PAIRS");
+    mla::ChunkRoute r{kMhaMinRows, kMhaPairsPerKey};
+    if (m >= 2) {
+        r.min_rows = m;
+        r.pair_keys = 0;
+    }
+    if (std::getenv("MLA_LAYER_MHA_PAIRS")) r.pair_keys = std::max(0, k);
+    return r;
 }
 
 // Layer workspace: the attention's (counters first) at offset 0, then the
 // absorbed queries, the new latents, the attention output (bf16: the value
-// up-projection reads it as bf16 in any case) and the projection workspace.
+// up-projection reads it as bf16 in any case), the per-head values o (bf16
+// [T][2048]), the up-projected keys and values of the largest multi-head
+// chunk request (fp16 [p + c][4096]) and its rope keys (fp16 [p + c][64]),
+// and the projection workspace.
 struct LayerLayout {
-    size_t attn = 0, q = 0, lat = 0, o = 0, proj = 0, total = 0;
+    size_t attn = 0, q = 0, lat = 0, olat = 0, o = 0, kv = 0, kpe = 0, proj = 0, total = 0;
 };
 
-LayerLayout layer_layout(size_t attn_bytes, long long T) {
+LayerLayout layer_layout(size_t attn_bytes, long long T, long long max_mha_keys) {
     LayerLayout l;
     l.attn = attn_bytes;
     size_t off = a256(attn_bytes);
@@ -249,11 +287,34 @@ LayerLayout layer_layout(size_t attn_bytes, long long T) {
     off = a256(off + (size_t)T * proj::kHeads * proj::kDqk * 2);
     l.lat = off;
     off = a256(off + (size_t)T * proj::kDqk * 2);
-    l.o = off;
+    l.olat = off;
     off = a256(off + (size_t)T * proj::kHeads * proj::kLatent * 2);
+    l.o = off;
+    off = a256(off + (size_t)T * proj::kOCols * 2);
+    l.kv = off;
+    off = a256(off + (size_t)max_mha_keys * 2 * proj::kOCols * 2);
+    l.kpe = off;
+    off = a256(off + (size_t)max_mha_keys * proj::kRope * 2);
     l.proj = off;
     l.total = off + proj_layout(T).total;
     return l;
+}
+
+// Sizes of a layer step: rows, the attention workspace (largest of the plans
+// with and without the multi-head requests) and the keys of the largest
+// multi-head request.
+int layer_sizes(const mla_batch *b, mla::ChunkRoute route, int *T, size_t *attn, long long *max_keys) {
+    int st = mla::batch_rows(b, T);
+    if (st != MLA_OK || *T == 0) return st;
+    *max_keys = 0;
+    for (int r = 0; r < b->num_reqs; ++r)
+        if (route.multi_head(b->prefix_lens[r], b->q_lens[r]))
+            *max_keys = std::max<long long>(*max_keys, (long long)b->prefix_lens[r] + b->q_lens[r]);
+    size_t a_all = 0, a_part = 0;
+    st = mla::attn_workspace(b, &a_all);
+    if (st == MLA_OK && *max_keys > 0) st = mla::attn_workspace(b, &a_part, route);
+    *attn = std::max(a_all, a_part);
+    return st;
 }
 
 }  // namespace
@@ -280,36 +341,118 @@ int mla_post_attn(int32_t num_rows, const void *attn_out, int32_t attn_dtype, co
 
 size_t mla_layer_workspace_bytes(const mla_batch *batch) {
     int T = 0;
-    if (mla::batch_rows(batch, &T) != MLA_OK || T == 0) return 0;
     size_t attn = 0;
-    if (mla::attn_workspace(batch, &attn) != MLA_OK) return 0;
-    return layer_layout(attn, T).total;
+    long long max_keys = 0;
+    if (layer_sizes(batch, mha_route(), &T, &attn, &max_keys) != MLA_OK || T == 0) return 0;
+    return layer_layout(attn, T, max_keys).total;
 }
 
 int mla_attention_layer(const mla_batch *batch, const uint16_t *hidden, const mla_proj_weights *w,
                         uint16_t *kv_cache, float softmax_scale, void *out, int32_t out_dtype, void *workspace,
                         size_t workspace_bytes, void *stream) {
+    using namespace proj;
+    const mla::ChunkRoute route = mha_route();
     int T = 0;
-    int st = mla::batch_rows(batch, &T);
-    if (st != MLA_OK || T == 0) return st;
     size_t attn = 0;
-    st = mla::attn_workspace(batch, &attn);
-    if (st != MLA_OK) return st;
-    const LayerLayout L = layer_layout(attn, T);
+    long long max_keys = 0;
+    int st = layer_sizes(batch, route, &T, &attn, &max_keys);
+    if (st != MLA_OK || T == 0) return st;
+    if (max_keys > 0 && (!w || !w->w_uk || misaligned(w->w_uk)))
+        return mla::set_error(MLA_ERR_INVALID_ARG, "w_uk must be non-NULL and 16-byte aligned");
+    const LayerLayout L = layer_layout(attn, T, max_keys);
     if (!workspace || misaligned(workspace) || workspace_bytes < L.total)
         return mla::set_error(MLA_ERR_WORKSPACE, "workspace of %zu bytes at %p; this batch needs %zu",
                               workspace_bytes, workspace, L.total);
     char *ws = static_cast<char *>(workspace);
     uint16_t *q = reinterpret_cast<uint16_t *>(ws + L.q);
     uint16_t *lat = reinterpret_cast<uint16_t *>(ws + L.lat);
+    uint16_t *olat = reinterpret_cast<uint16_t *>(ws + L.olat);
     uint16_t *o = reinterpret_cast<uint16_t *>(ws + L.o);
+    char *pws = ws + L.proj;
+    const size_t pws_bytes = L.total - L.proj;
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    st = pre_attn(batch, T, hidden, w, q, lat, ws + L.proj, L.total - L.proj, s);
+    st = pre_attn(batch, T, hidden, w, q, lat, pws, pws_bytes, s);
     if (st != MLA_OK) return st;
-    st = mixed_step(batch, q, lat, kv_cache, softmax_scale, o, MLA_OUT_BF16, nullptr, attn > 0 ? ws : nullptr,
-                    attn, stream);
+    if (max_keys == 0) {
+        // every row on the absorbed kernel: append and attention in one launch
+        st = mixed_step(batch, q, lat, kv_cache, softmax_scale, olat, MLA_OUT_BF16, nullptr, attn > 0 ? ws : nullptr,
+                        attn, stream);
+        if (st != MLA_OK) return st;
+        st = uv_gemm(0, T, olat, false, w, o, s);
+        if (st != MLA_OK) return st;
+        return o_gemm(T, o, w, out, out_dtype, s);
+    }
+
+    // Long chunk requests take the multi-head path; the other rows the
+    // absorbed kernel, which also appends their new latents.  The multi-head
+    // requests' latents are appended by their up-projection launch.
+    st = mla::attend_rows(batch, q, lat, kv_cache, softmax_scale, olat, MLA_OUT_BF16, attn > 0 ? ws : nullptr, attn,
+                          stream, route);
     if (st != MLA_OK) return st;
-    return post_attn(T, o, MLA_OUT_BF16, w, out, out_dtype, ws + L.proj, L.total - L.proj, s);
+    // value up-projection of the absorbed rows: the span from the first to
+    // the last row that is not in a multi-head request
+    int lo = T, hi = 0;
+    {
+        int row = 0;
+        for (int r = 0; r < batch->num_reqs; ++r) {
+            const int c = batch->q_lens[r];
+            if (!route.multi_head(batch->prefix_lens[r], c)) {
+                lo = std::min(lo, row);
+                hi = std::max(hi, row + c);
+            }
+            row += c;
+        }
+    }
+    st = uv_gemm(lo, hi, olat, false, w, o, s);
+    if (st != MLA_OK) return st;
+    const uint16_t *qn = reinterpret_cast<const uint16_t *>(pws + proj_layout(T).qn);
+    uint16_t *kvu = reinterpret_cast<uint16_t *>(ws + L.kv);
+    uint16_t *kpe = reinterpret_cast<uint16_t *>(ws + L.kpe);
+    int lg = 0;
+    while ((1 << lg) < batch->page_size) ++lg;
+    int row = 0;
+    for (int r = 0; r < batch->num_reqs; ++r) {
+        const int c = batch->q_lens[r], p = batch->prefix_lens[r];
+        if (route.multi_head(p, c)) {
+            // keys 0 .. p + c - 1 of the request: k = W_UK c, v = W_UV c (fp16)
+            GemmArgs u{};
+            u.a = kv_cache;
+            u.lda = kDqk;
+            u.a_bt = batch->block_table_dev + (size_t)r * batch->max_pages_per_req;
+            u.a_log2p = lg;
+            u.a_npages = batch->num_pages;
+            u.a_new = lat + (size_t)row * kDqk;  // the chunk's own keys: its new latents
+            u.a_new_from = p;
+            u.keys = KeyRowsJob{kv_cache, lat + (size_t)row * kDqk, u.a_bt, lg, batch->num_pages, p, p + c, kpe};
+            u.keys_wgs = (p + c + kKeyRowsPerWg - 1) / kKeyRowsPerWg;
+            u.b = w->w_uk;
+            u.b2 = w->w_uv;
+            u.ldb = kLatent;
+            u.n_split = kOCols;
+            u.M = p + c;
+            u.N = 2 * kOCols;
+            u.K = kLatent;
+            u.c = kvu;
+            u.ldc = 2 * kOCols;
+            st = launch(u, kStoreF16, false, 1, s, "key / value up-projection");
+            if (st != MLA_OK) return st;
+            MhaArgs m{};
+            m.qn = qn;
+            m.q_abs = q;
+            m.kv = kvu;
+            m.kpe = kpe;
+            m.o = o;
+            m.row0 = row;
+            m.c = c;
+            m.p = p;
+            m.scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
+            const hipError_t e = launch_mha_prefill(m, s);
+            if (e != hipSuccess)
+                return mla::set_error(MLA_ERR_HIP, "multi-head prefill launch: %s", hipGetErrorString(e));
+        }
+        row += c;
+    }
+    return o_gemm(T, o, w, out, out_dtype, s);
 }
 
 }  // extern "C"

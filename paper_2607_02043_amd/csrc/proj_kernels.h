@@ -23,6 +23,7 @@ enum Epilogue : int {
     kStoreBf16 = 0,  // C (bf16, row stride ldc)
     kStoreF32 = 1,   // C (fp32, row stride ldc)
     kQkvSplit = 2,   // first projection: nope -> qn bf16, rope -> qpe fp32, latent -> kvf fp32
+    kStoreF16 = 3,   // C (fp16, row stride ldc)
 };
 
 struct RowArgs {
@@ -39,6 +40,20 @@ struct RowArgs {
     double log2_base;         // log2 of the rope base
 };
 
+// Key rows of one chunk request for the multi-head path, run by extra
+// workgroups of its up-projection launch (8 keys each): the rope key of every
+// key 0 .. nkeys - 1 into kpe as fp16, and the new latents (keys p ..) into
+// their cache slots.
+struct KeyRowsJob {
+    uint16_t *cache;         // bf16 [pages][P][576]: keys < p are read here, keys >= p written
+    const uint16_t *lat;     // bf16 [nkeys - p][576]: the request's new latents
+    const int32_t *bt;       // block-table row of the request
+    int log2p, npages;
+    int p, nkeys;
+    uint16_t *kpe;           // fp16 [nkeys][64]
+};
+constexpr int kKeyRowsPerWg = 8;
+
 // C[z][m][n] = sum_k A[z][m][k] * B[z][n][k]: both operands K-contiguous.
 // Element strides; z = blockIdx.z.  Columns n >= n_split take their B rows
 // from b2 (row n - n_split), so two weight matrices act as one.
@@ -50,6 +65,14 @@ struct GemmArgs {
     long long ldb, b_bstride;
     int n_split;
     int M, N, K;
+    // Gathered A (non-null a_bt): row m is token m of one request in the paged
+    // cache, at a + (a_bt[m >> a_log2p] * 2^a_log2p + (m & (2^a_log2p - 1))) * lda;
+    // page ids outside [0, a_npages) read page 0.  Rows m >= a_new_from come
+    // from a_new + (m - a_new_from) * lda instead (the step's new latents).
+    const int32_t *a_bt;
+    int a_log2p, a_npages;
+    const uint16_t *a_new;
+    int a_new_from;
     void *c;
     long long ldc, c_bstride;
     // kQkvSplit outputs
@@ -61,8 +84,26 @@ struct GemmArgs {
     // overlaps the GEMM instead of taking a launch of its own.
     RowArgs rope;
     int rope_wgs;
+    KeyRowsJob keys;          // or the key rows of a multi-head chunk request
+    int keys_wgs;
 };
 
+
+// Causal attention of one chunk request in the multi-head form: per head,
+// queries (128 dims without position + 64 rope dims) against up-projected
+// keys (W_UK c, 128 dims) plus the shared rope key, values W_UV c (128 dims).
+struct MhaArgs {
+    const uint16_t *qn;      // bf16 [T][16][128]: query dims without position
+    const uint16_t *q_abs;   // bf16 [T][16][576]: dims 512..575 hold the rotated query rope dims
+    const uint16_t *kv;      // fp16 [p + c][4096]: k (h * 128 + d), then v (2048 + h * 128 + d)
+    const uint16_t *kpe;     // fp16 [p + c][64]: the rotated rope key of every key
+    uint16_t *o;             // bf16 [T][2048]: o[row][h * 128 + d]
+    int row0, c, p;          // the request's rows row0 .. row0 + c - 1 sit at positions p .. p + c - 1
+    float scale_log2;        // softmax scale * log2(e)
+};
+constexpr int kMhaWaves = 8;
+constexpr int kMhaTokens = 16 * kMhaWaves;  // query tokens per workgroup (16 per wave)
+hipError_t launch_mha_prefill(const MhaArgs &a, hipStream_t s);
 
 // Tile shape of one GEMM launch: bm x bn outputs per workgroup; `depth` > 0
 // picks the LDS ring fed by direct loads with that many stages, 0 the
@@ -76,7 +117,8 @@ struct GemmShape {
 };
 
 // The launch covers ceil(M / bm) * ceil(N / bn) tiles x batch, plus
-// g.rope_wgs workgroups of rope / norm rows (four rows each).
+// g.rope_wgs workgroups of rope / norm rows (four rows each) or g.keys_wgs of
+// key rows (kKeyRowsPerWg each).
 hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int batch, hipStream_t s);
 inline int rope_norm_wgs(int num_rows) { return (num_rows + 3) / 4; }
 

@@ -19,6 +19,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
@@ -80,6 +81,8 @@ __device__ __forceinline__ void store_tile(const GemmArgs &g, const f32x4 (&acc)
                     static_cast<uint16_t *>(g.c)[z * g.c_bstride + (long long)row * g.ldc + n] = (uint16_t)bf16_of(v);
                 } else if constexpr (EPI == kStoreF32) {
                     static_cast<float *>(g.c)[z * g.c_bstride + (long long)row * g.ldc + n] = v;
+                } else if constexpr (EPI == kStoreF16) {
+                    static_cast<_Float16 *>(g.c)[z * g.c_bstride + (long long)row * g.ldc + n] = (_Float16)v;
                 } else {
                     if (n < kQCols) {
                         const int h = n / kQkHead, j = n - h * kQkHead;
@@ -178,12 +181,38 @@ __device__ __forceinline__ void tile_of(int M, int N, int BM, int BN, int *m0, i
     *n0 = (r / gm) * BN;
 }
 
-// Workgroups past the tiles run the launch's rope / norm rows (z = 0) or
-// nothing; true when this workgroup is one of them.
+__device__ __forceinline__ void key_rows(const KeyRowsJob &j, int wg) {
+    // thread: key wg * 8 + tid / 32, 16-byte chunk tid % 32 of the 72 of a latent row
+    const int key = wg * kKeyRowsPerWg + (threadIdx.x >> 5), lane = threadIdx.x & 31;
+    if (key >= j.nkeys) return;
+    int pg = j.bt[key >> j.log2p];
+    pg = (unsigned)pg < (unsigned)j.npages ? pg : 0;
+    uint16_t *slot = j.cache + (((size_t)pg << j.log2p) + (key & ((1 << j.log2p) - 1))) * kDqk;
+    const uint16_t *src = key < j.p ? slot : j.lat + (size_t)(key - j.p) * kDqk;
+    for (int c = lane; c < kDqk / 8; c += 32) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(src + 8 * c);
+        if (key >= j.p) *reinterpret_cast<u32x4 *>(slot + 8 * c) = v;  // append of a new latent
+        if (c >= kLatent / 8) {
+            u32x4 h;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const auto f = __builtin_amdgcn_cvt_pkrtz(__uint_as_float(v[k] << 16), __uint_as_float(v[k] & 0xffff0000u));
+                h[k] = __builtin_bit_cast(uint32_t, f);
+            }
+            *reinterpret_cast<u32x4 *>(j.kpe + (size_t)key * kRope + 8 * (c - kLatent / 8)) = h;
+        }
+    }
+}
+
+// Workgroups past the tiles run the launch's side job (z = 0) or nothing;
+// true when this workgroup is one of them.
 __device__ __forceinline__ bool is_rope_wg(const GemmArgs &g, int BM, int BN) {
     const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
     if ((int)blockIdx.x < tiles) return false;
-    if (blockIdx.z == 0) rope_norm_rows(g.rope, blockIdx.x - tiles);
+    if (blockIdx.z == 0) {
+        if (g.rope_wgs > 0) rope_norm_rows(g.rope, blockIdx.x - tiles);
+        else key_rows(g.keys, blockIdx.x - tiles);
+    }
     return true;
 }
 
@@ -218,7 +247,19 @@ __global__ __launch_bounds__(256) void gemm_ring_kernel(const GemmArgs g) {
         const int kc = (s & 7) ^ ((row >> 1) & 7);
         if (row < BM) {
             const int r = min(m0 + row, g.M - 1);
-            src[i] = static_cast<const uint16_t *>(g.a) + z * g.a_bstride + (long long)r * g.lda + kc * 8;
+            long long ar = r;
+            const uint16_t *abase = static_cast<const uint16_t *>(g.a);
+            if (g.a_bt != nullptr) {
+                if (g.a_new != nullptr && r >= g.a_new_from) {
+                    abase = g.a_new;
+                    ar = r - g.a_new_from;
+                } else {
+                    int pg = g.a_bt[r >> g.a_log2p];
+                    pg = (unsigned)pg < (unsigned)g.a_npages ? pg : 0;
+                    ar = ((long long)pg << g.a_log2p) + (r & ((1 << g.a_log2p) - 1));
+                }
+            }
+            src[i] = abase + z * g.a_bstride + ar * g.lda + kc * 8;
         } else {
             const int n = min(n0 + row - BM, g.N - 1) - nbase;
             src[i] = bseg + z * g.b_bstride + (long long)n * g.ldb + kc * 8;
@@ -448,9 +489,234 @@ __global__ __launch_bounds__(256) void gemm_f32a_kernel(const GemmArgs g) {
     store_tile<EPI, MB, 2>(g, acc, m0 + wr + 4 * (lane >> 4), n0 + (wave & 1) * 32 + (lane & 15), z);
 }
 
+// ------------------------------------------------------------------------
+// Multi-head causal attention of one chunk request (see MhaArgs).  Grid
+// (ceil(c / 64), 16 heads), four waves; wave w owns tokens i0 + 16 w .. + 15.
+// Keys stream in tiles of 64 through two LDS stages, register staged one tile
+// ahead.  Four waves rather than eight: with a quarter of the chunk's blocks
+// per head the causal triangle leaves the chip unevenly loaded, and two
+// workgroups a CU hide each other's barriers.  The K tile holds 64 keys x
+// 192 fp16 dims (384 bytes a key, 16-byte chunk c at position
+// c ^ ((key >> 1) & 7) inside its group of 8), the V tile 64 keys x 128 fp16
+// dims (chunk c at c ^ (2 (key & 7))); both keep the operand reads below free
+// of bank conflicts.
+//  * S^T = K Q^T (f16 MFMA 16x16x32): lane (g, t) holds the scores of token t
+//    against keys 16 kb + 4 g + i of the tile, kb, i = 0..3.
+//  * Online softmax per token (running max and sum, accumulators rescaled);
+//    the probabilities stay in registers, already in the operand order of
+//  * O^T += V^T P^T: slot 8 g + j of a 32-key step is key 4 g + j (j < 4) or
+//    16 + 4 g + j - 4; V^T comes from transposing LDS reads in that order.
+namespace mha {
+constexpr int kKeys = 64;
+constexpr int kKRowBytes = 192 * 2;
+constexpr int kKTile = kKeys * kKRowBytes;  // 24576
+constexpr int kVTile = kKeys * 256;         // 16384
+constexpr int kStage = kKTile + kVTile;     // 40960
+
+__device__ __forceinline__ int k_off(int key, int c) { return key * kKRowBytes + ((c ^ ((key >> 1) & 7)) << 4); }
+__device__ __forceinline__ int v_off(int key, int c) { return key * 256 + ((c ^ ((key & 7) << 1)) << 4); }
+
+// 8 bf16 -> 8 fp16 (exact inside the fp16 normal range)
+__device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 w) {
+    u32x4 r;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const auto h = __builtin_amdgcn_cvt_pkrtz(__uint_as_float(w[k] << 16), __uint_as_float(w[k] & 0xffff0000u));
+        r[k] = __builtin_bit_cast(uint32_t, h);
+    }
+    return r;
+}
+
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+    typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
+}
+
+__device__ __forceinline__ u32x2 read_tr16(const char *p) {
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p));
+    return __builtin_bit_cast(u32x2, v);
+}
+
+// max / sum over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four key groups of a token)
+__device__ __forceinline__ float max4(float v) {
+    v = fmaxf(v, __shfl_xor(v, 16));
+    return fmaxf(v, __shfl_xor(v, 32));
+}
+__device__ __forceinline__ float sum4(float v) {
+    v += __shfl_xor(v, 16);
+    return v + __shfl_xor(v, 32);
+}
+
+__device__ __forceinline__ uint32_t f16x2(float a, float b) {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    const h2 v = {(_Float16)a, (_Float16)b};
+    return __builtin_bit_cast(uint32_t, v);
+}
+}  // namespace mha
+
+__global__ __launch_bounds__(64 * kMhaWaves) void mha_prefill_kernel(const MhaArgs a) {
+    using namespace mha;
+    __shared__ __attribute__((aligned(16))) char sm[2 * kStage];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, tl = lane & 15;
+    // Workgroups are dealt to the 8 XCDs round-robin: XCD x gets heads 2 x and
+    // 2 x + 1 (the keys and values of two heads stay in its L2), token blocks
+    // with the most keys first.
+    const int nblk = gridDim.x;
+    const int lin = blockIdx.x + nblk * blockIdx.y;
+    const int sl = lin >> 3;
+    const int h = 2 * (lin & 7) + sl / nblk;
+    const int i0 = (nblk - 1 - sl % nblk) * kMhaTokens;
+    const int tok = i0 + wave * 16 + tl;  // this lane's token
+    const int tokc = min(tok, a.c - 1);   // tokens past the chunk repeat its last one; never stored
+    const int lim = a.p + tokc;           // last key this token sees
+    const int nkeys = a.p + a.c;
+    const int ntiles = (a.p + min(i0 + kMhaTokens, a.c) - 1) / kKeys + 1;
+    // tiles wholly below the first key some token of this wave cannot see need no mask
+    const int wave_lim = a.p + min(i0 + wave * 16, a.c - 1);
+
+    // Q^T operands: lane (g, t) holds dims 32 s + 8 g .. + 7 of token t (s < 4: without position, s = 4, 5: rope)
+    u32x4 qf[6];
+    {
+        const uint16_t *qn = a.qn + ((size_t)(a.row0 + tokc) * 16 + h) * 128 + 8 * g;
+        const uint16_t *qr = a.q_abs + ((size_t)(a.row0 + tokc) * 16 + h) * 576 + 512 + 8 * g;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) qf[s] = bf16x8_to_f16x8(*reinterpret_cast<const u32x4 *>(qn + 32 * s));
+#pragma unroll
+        for (int s = 0; s < 2; ++s) qf[4 + s] = bf16x8_to_f16x8(*reinterpret_cast<const u32x4 *>(qr + 32 * s));
+    }
+
+    // staging per thread and tile: kKLd of the 64 x 24 K chunks (16 from the
+    // up-projected keys, 8 rope), kVLd of the 64 x 16 V chunks
+    constexpr int kThreads = 64 * kMhaWaves, kKLd = 64 * 24 / kThreads, kVLd = 64 * 16 / kThreads;
+    auto load = [&](u32x4(&r)[kKLd + kVLd], int t) {
+        const int kb = t * kKeys;
+#pragma unroll
+        for (int j = 0; j < kKLd; ++j) {
+            const int q = tid + kThreads * j, key = min(kb + q / 24, nkeys - 1), cc = q % 24;
+            const uint16_t *src = cc < 16 ? a.kv + (size_t)key * 4096 + h * 128 + cc * 8
+                                          : a.kpe + (size_t)key * 64 + (cc - 16) * 8;
+            r[j] = *reinterpret_cast<const u32x4 *>(src);
+        }
+#pragma unroll
+        for (int j = 0; j < kVLd; ++j) {
+            const int q = tid + kThreads * j, key = min(kb + (q >> 4), nkeys - 1), cc = q & 15;
+            r[kKLd + j] = *reinterpret_cast<const u32x4 *>(a.kv + (size_t)key * 4096 + 2048 + h * 128 + cc * 8);
+        }
+    };
+    auto store = [&](const u32x4(&r)[kKLd + kVLd], int buf) {
+        char *ks = sm + buf * kStage, *vs = ks + kKTile;
+#pragma unroll
+        for (int j = 0; j < kKLd; ++j) {
+            const int q = tid + kThreads * j;
+            *reinterpret_cast<u32x4 *>(ks + k_off(q / 24, q % 24)) = r[j];
+        }
+#pragma unroll
+        for (int j = 0; j < kVLd; ++j) {
+            const int q = tid + kThreads * j;
+            *reinterpret_cast<u32x4 *>(vs + v_off(q >> 4, q & 15)) = r[kKLd + j];
+        }
+    };
+
+    f32x4 acc[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) acc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    // V^T operand addresses (lane (g, t): dim 16 db + t of keys 32 m + 4 g + j and 32 m + 16 + 4 g + j)
+    const int tr_key = 4 * g + (tl >> 2);
+    const int tr_c = (tl & 3) >> 1, tr_b = 8 * (tl & 1);
+
+    auto tile = [&](int t, int buf) {
+        const char *ks = sm + buf * kStage, *vs = ks + kKTile;
+        f32x4 st[4];
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) st[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 6; ++s) {
+            u32x4 ka[4];
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) ka[kb] = *reinterpret_cast<const u32x4 *>(ks + k_off(16 * kb + tl, 4 * s + g));
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) st[kb] = mfma16(ka[kb], qf[s], st[kb]);
+        }
+        // scaled, masked scores; running max
+        const int kbase = t * kKeys + 4 * g;
+        const bool need_mask = t * kKeys + kKeys - 1 > wave_lim;
+        float x[16];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            float v = st[e >> 2][e & 3] * a.scale_log2;
+            if (need_mask && kbase + 16 * (e >> 2) + (e & 3) > lim) v = -INFINITY;
+            x[e] = v;
+            mx = fmaxf(mx, v);
+        }
+        mx = max4(mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
+        m_run = m_new;
+        float ps = 0.f;
+        float pe[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            pe[e] = __builtin_amdgcn_exp2f(x[e] - m_new);
+            ps += pe[e];
+        }
+        l_run = l_run * alpha + ps;
+        u32x4 pb[2];
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+            pb[m] = u32x4{f16x2(pe[8 * m + 0], pe[8 * m + 1]), f16x2(pe[8 * m + 2], pe[8 * m + 3]),
+                          f16x2(pe[8 * m + 4], pe[8 * m + 5]), f16x2(pe[8 * m + 6], pe[8 * m + 7])};
+#pragma unroll
+        for (int db = 0; db < 8; ++db) acc[db] = acc[db] * alpha;
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+#pragma unroll
+            for (int db = 0; db < 8; ++db) {
+                const int k1 = 32 * m + tr_key, k2 = k1 + 16;
+                const u32x2 lo = read_tr16(vs + v_off(k1, 2 * db + tr_c) + tr_b);
+                const u32x2 hi = read_tr16(vs + v_off(k2, 2 * db + tr_c) + tr_b);
+                acc[db] = mfma16(u32x4{lo[0], lo[1], hi[0], hi[1]}, pb[m], acc[db]);
+            }
+        }
+    };
+
+    // Tile t + 1 loads into registers while tile t is scored; the load of
+    // the tile past the last one re-reads it (in bounds, never stored), so the
+    // loads stay unconditional and the register set is never merged at a
+    // branch join (a copy of a register still being loaded waits for every
+    // load in flight).
+    u32x4 r[kKLd + kVLd];
+    load(r, 0);
+    store(r, 0);
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        load(r, min(t + 1, ntiles - 1));
+        tile(t, t & 1);
+        if (t + 1 < ntiles) store(r, (t + 1) & 1);
+        __syncthreads();
+    }
+    const float l = sum4(l_run);
+    if (tok < a.c) {
+        const float inv = 1.f / l;
+        uint16_t *dst = a.o + (size_t)(a.row0 + tok) * 2048 + h * 128 + 4 * g;
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const f32x4 v = acc[db] * inv;
+            *reinterpret_cast<u32x2 *>(dst + 16 * db) = u32x2{pack2(v[0], v[1]), pack2(v[2], v[3])};
+        }
+    }
+}
+
 template <int BM, int BN, int D>
 hipError_t launch_ring(const GemmArgs &g, int epi, dim3 grid, hipStream_t s) {
-    if (epi == kStoreBf16) gemm_ring_kernel<BM, BN, D, kStoreBf16><<<grid, 256, 0, s>>>(g);
+    if (epi == kStoreF16) gemm_ring_kernel<BM, BN, D, kStoreF16><<<grid, 256, 0, s>>>(g);
+    else if (epi == kStoreBf16) gemm_ring_kernel<BM, BN, D, kStoreBf16><<<grid, 256, 0, s>>>(g);
     else if (epi == kStoreF32) gemm_ring_kernel<BM, BN, D, kStoreF32><<<grid, 256, 0, s>>>(g);
     else if (epi == kQkvSplit) gemm_ring_kernel<BM, BN, D, kQkvSplit><<<grid, 256, 0, s>>>(g);
     else return hipErrorInvalidValue;
@@ -477,15 +743,28 @@ hipError_t launch_f32a(const GemmArgs &g, int epi, dim3 grid, hipStream_t s) {
 
 }  // namespace
 
+hipError_t launch_mha_prefill(const MhaArgs &a, hipStream_t s) {
+    if (a.c <= 0) return hipSuccess;
+    if (a.p < 0) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((a.c + kMhaTokens - 1) / kMhaTokens), 16);
+    mha_prefill_kernel<<<grid, 64 * kMhaWaves, 0, s>>>(a);
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmArgs &g, const GemmShape &t, bool a_f32, int batch, hipStream_t s) {
     if (g.M <= 0 || batch <= 0) return hipSuccess;
     if (g.K % kBK != 0 || g.K <= 0 || g.N <= 0) return hipErrorInvalidValue;
     const int bn = a_f32 ? kBN : t.bn;
-    const long long tiles = (long long)((g.M + t.bm - 1) / t.bm) * ((g.N + bn - 1) / bn) + g.rope_wgs;
-    if (tiles > 0x7FFFFFFF || g.rope_wgs < 0) return hipErrorInvalidValue;
+    const long long tiles = (long long)((g.M + t.bm - 1) / t.bm) * ((g.N + bn - 1) / bn) + g.rope_wgs + g.keys_wgs;
+    if (tiles > 0x7FFFFFFF || g.rope_wgs < 0 || g.keys_wgs < 0 || (g.rope_wgs > 0 && g.keys_wgs > 0))
+        return hipErrorInvalidValue;
     const dim3 grid((unsigned)tiles, 1, (unsigned)batch);
+    if (a_f32 || t.depth == 0) {
+        // gathered rows and fp16 output exist in the LDS-ring kernel only
+        if (g.a_bt != nullptr || t.epi == kStoreF16) return hipErrorInvalidValue;
+    }
     if (a_f32) {
-        if (g.rope_wgs != 0) return hipErrorInvalidValue;
+        if (g.rope_wgs != 0 || g.keys_wgs != 0) return hipErrorInvalidValue;
         if (g.N % kBN != 0) return hipErrorInvalidValue;
         switch (t.bm) {
             case 32: return launch_f32a<32>(g, t.epi, grid, s);

@@ -297,8 +297,9 @@ class ProjWeights:
     w_q: np.ndarray      # [16 * 192][2048]
     w_dkv: np.ndarray    # [576][2048]
     kv_gain: np.ndarray  # [512]
-    w_uk_t: np.ndarray   # [16][512][128]
+    w_uk_t: np.ndarray   # [16][512][128]: w_uk transposed per head
     w_uv: np.ndarray     # [16][128][512]
+    w_uk: np.ndarray     # [16][128][512]
     w_o: np.ndarray      # [2048][16 * 128]
     rms_eps: float = 1e-6
     rope_base: float = 10000.0
@@ -311,12 +312,14 @@ def make_proj_weights(seed: int = 0, layer: int = 0) -> ProjWeights:
         return random_bf16(n, sc, seed, layer, _STREAM_W + k, offset).reshape(shape)
 
     qk = QK_NOPE + QK_ROPE
+    w_uk = draw(3, (NUM_HEADS, QK_NOPE, D_LATENT), QK_NOPE)
     return ProjWeights(
         w_q=draw(0, (NUM_HEADS * qk, HIDDEN), HIDDEN),
         w_dkv=draw(1, (D_QK, HIDDEN), HIDDEN),
         kv_gain=draw(2, (D_LATENT,), 1, offset=1.0, scale=0.1),
-        w_uk_t=draw(3, (NUM_HEADS, D_LATENT, QK_NOPE), QK_NOPE),
+        w_uk_t=np.ascontiguousarray(w_uk.transpose(0, 2, 1)),
         w_uv=draw(4, (NUM_HEADS, V_HEAD, D_LATENT), D_LATENT),
+        w_uk=w_uk,
         w_o=draw(5, (HIDDEN, NUM_HEADS * V_HEAD), NUM_HEADS * V_HEAD),
     )
 

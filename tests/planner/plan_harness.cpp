@@ -48,7 +48,7 @@ int main() {
         double us = 0.0;
         if (st == MLA_OK && sh.R > 0) {
             const auto t0 = std::chrono::steady_clock::now();
-            st = make_plan_uncached(&b, sh, ncu, &pl);
+            st = make_plan_uncached(&b, sh, ncu, mla::kAbsorbAll, &pl);
             us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
         }
         if (st != MLA_OK) {

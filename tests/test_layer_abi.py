@@ -28,8 +28,8 @@ def test_layer_header_symbols_are_exported():
 
 
 def _weights(**kw):
-    w = mla.mla_proj_weights(w_q=FAKE, w_dkv=FAKE, kv_gain=FAKE, w_uk_t=FAKE, w_uv=FAKE, w_o=FAKE, rms_eps=1e-6,
-                             rope_base=10000.0)
+    w = mla.mla_proj_weights(w_q=FAKE, w_dkv=FAKE, kv_gain=FAKE, w_uk_t=FAKE, w_uv=FAKE, w_uk=FAKE, w_o=FAKE,
+                             rms_eps=1e-6, rope_base=10000.0)
     for k, v in kw.items():
         setattr(w, k, v)
     return w
