@@ -559,7 +559,7 @@ __device__ __forceinline__ uint32_t f16x2(float a, float b) {
 
 __global__ __launch_bounds__(64 * kMhaWaves) void mha_prefill_kernel(const MhaArgs a) {
     using namespace mha;
-    __shared__ __attribute__((aligned(16))) char sm[2 * kStage];
+    __shared__ __attribute__((aligned(16))) char sm[3 * kStage];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, tl = lane & 15;
     // Workgroups are dealt to the 8 XCDs round-robin: XCD x gets heads 2 x and
@@ -630,8 +630,10 @@ __global__ __launch_bounds__(64 * kMhaWaves) void mha_prefill_kernel(const MhaAr
     const int tr_key = 4 * g + (tl >> 2);
     const int tr_c = (tl & 3) >> 1, tr_b = 8 * (tl & 1);
 
-    auto tile = [&](int t, int buf) {
-        const char *ks = sm + buf * kStage, *vs = ks + kKTile;
+    u32x4 pb[2];  // probabilities of the last scored tile, operand order of P V
+    float alpha;  // and the factor that rescales the accumulators before it
+    auto score = [&](int t, int buf) {
+        const char *ks = sm + buf * kStage;
         f32x4 st[4];
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) st[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -657,7 +659,7 @@ __global__ __launch_bounds__(64 * kMhaWaves) void mha_prefill_kernel(const MhaAr
         }
         mx = max4(mx);
         const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
+        alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile (m_run = -inf)
         m_run = m_new;
         float ps = 0.f;
         float pe[16];
@@ -667,11 +669,13 @@ __global__ __launch_bounds__(64 * kMhaWaves) void mha_prefill_kernel(const MhaAr
             ps += pe[e];
         }
         l_run = l_run * alpha + ps;
-        u32x4 pb[2];
 #pragma unroll
         for (int m = 0; m < 2; ++m)
             pb[m] = u32x4{f16x2(pe[8 * m + 0], pe[8 * m + 1]), f16x2(pe[8 * m + 2], pe[8 * m + 3]),
                           f16x2(pe[8 * m + 4], pe[8 * m + 5]), f16x2(pe[8 * m + 6], pe[8 * m + 7])};
+    };
+    auto pv = [&](int buf) {
+        const char *vs = sm + buf * kStage + kKTile;
 #pragma unroll
         for (int db = 0; db < 8; ++db) acc[db] = acc[db] * alpha;
 #pragma unroll
@@ -686,21 +690,37 @@ __global__ __launch_bounds__(64 * kMhaWaves) void mha_prefill_kernel(const MhaAr
         }
     };
 
-    // Tile t + 1 loads into registers while tile t is scored; the load of
+    // Tile t + 1 loads into registers while tile t is processed; the load of
     // the tile past the last one re-reads it (in bounds, never stored), so the
     // loads stay unconditional and the register set is never merged at a
     // branch join (a copy of a register still being loaded waits for every
-    // load in flight).
+    // load in flight).  The second half of the waves runs P V one tile
+    // behind its scores: each SIMD holds one wave of each half, so one
+    // wave's softmax overlaps the other's MFMAs instead of both waiting at
+    // the same point between barriers.  Three LDS stages: tile t - 1 stays
+    // readable while tile t + 1 is stored.
+    const bool lag = wave >= kMhaWaves / 2;
     u32x4 r[kKLd + kVLd];
     load(r, 0);
     store(r, 0);
     __syncthreads();
+    int b_prev = 2, b_cur = 0;
     for (int t = 0; t < ntiles; ++t) {
+        const int b_next = b_cur == 2 ? 0 : b_cur + 1;
         load(r, min(t + 1, ntiles - 1));
-        tile(t, t & 1);
-        if (t + 1 < ntiles) store(r, (t + 1) & 1);
+        if (!lag) {
+            score(t, b_cur);
+            pv(b_cur);
+        } else {
+            if (t > 0) pv(b_prev);
+            score(t, b_cur);
+        }
+        if (t + 1 < ntiles) store(r, b_next);
         __syncthreads();
+        b_prev = b_cur;
+        b_cur = b_next;
     }
+    if (lag) pv(b_prev);
     const float l = sum4(l_run);
     if (tok < a.c) {
         const float inv = 1.f / l;
