@@ -20,6 +20,13 @@ hipError_t launch_combine(const AttnArgs &, hipStream_t) { return hipSuccess; }
 }  // namespace mla
 
 int main() {
+    // PLAN_ROUTE="min_rows pair_keys": leave the chunk requests that this
+    // route sends to the multi-head path out of the plan
+    mla::ChunkRoute route = mla::kAbsorbAll;
+    if (const char *e = std::getenv("PLAN_ROUTE")) {
+        std::istringstream r(e);
+        r >> route.min_rows >> route.pair_keys;
+    }
     std::string line;
     while (std::getline(std::cin, line)) {
         std::istringstream in(line);
@@ -48,7 +55,7 @@ int main() {
         double us = 0.0;
         if (st == MLA_OK && sh.R > 0) {
             const auto t0 = std::chrono::steady_clock::now();
-            st = make_plan_uncached(&b, sh, ncu, mla::kAbsorbAll, &pl);
+            st = make_plan_uncached(&b, sh, ncu, route, &pl);
             us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
         }
         if (st != MLA_OK) {

@@ -32,10 +32,14 @@ def harness(tmp_path_factory):
     return exe
 
 
-def plan(exe, batches):
+def plan(exe, batches, route=None):
     text = "".join(f"{ncu} {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n"
                    for ncu, P, q, p in batches)
-    out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True).stdout.splitlines()
+    env = dict(os.environ)
+    if route is not None:
+        env["PLAN_ROUTE"] = f"{route[0]} {route[1]}"
+    out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True,
+                         env=env).stdout.splitlines()
     assert len(out) == len(batches)
     res = []
     for line in out:
@@ -81,9 +85,16 @@ def unit_limits(dec, U, P):
     return worst_seg, worst_pages
 
 
-def check_plan(batch, d):
+def multi_head(route, p, c):
+    """The layer's route of a chunk request (c rows at prefix p) to the
+    multi-head path: at least min_rows rows and c (p + c/2) / (p + c) query-key
+    pairs per key reaching pair_keys."""
+    return route is not None and c >= route[0] and c * (2 * p + c) >= 2 * route[1] * (p + c)
+
+
+def check_plan(batch, d, route=None):
     ncu, P, q, p = batch
-    chunks = [(pi, qi) for qi, pi in zip(q, p) if qi > 1]
+    chunks = [(pi, qi) for qi, pi in zip(q, p) if qi > 1 and not multi_head(route, pi, qi)]
     dec, first = [], 0
     for qi, pi in zip(q, p):
         if qi == 1:
@@ -154,3 +165,23 @@ def test_single_request_extremes(harness):
              (256, 64, [4096], [1 << 16]), (1, 64, [1, 1, 300], [5, 70, 1000])]
     for b, d in zip(cases, plan(harness, cases)):
         check_plan(b, d)
+
+
+@pytest.mark.parametrize("route", [(256, 1200), (2, 100), (2, 0)])
+def test_plan_leaves_out_routed_chunks(harness, route):
+    """Chunk requests that the layer sends to the multi-head path get no work
+    items; the rest of the plan is that of the remaining requests."""
+    rng = np.random.default_rng(7)
+    batches = [random_batch(rng, int(rng.choice([80, 256]))) for _ in range(40)]
+    batches.append((256, 64, [1] * 128 + [2048], list(rng.integers(0, 4096, 128)) + [6144]))
+    batches.append((256, 64, [1500], [0]))  # the only request leaves: nothing to plan
+    res = plan(harness, batches, route)
+    for b, d in zip(batches, res):
+        assert not isinstance(d, tuple), (b[:2], d)
+        ncu, P, q, p = b
+        if all(qi > 1 and multi_head(route, pi, qi) for qi, pi in zip(q, p)):
+            assert d["n_chunk_items"] == 0 and d["n_dec_items"] == 0 and d["grid"] == 0, d
+            continue
+        check_plan(b, d, route)
+    # the benchmark's 2048-row chunk over 6144 keys leaves on every route here
+    assert res[-2]["n_chunk_items"] == 0 and res[-2]["n_dec_items"] > 0
