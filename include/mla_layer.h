@@ -107,7 +107,7 @@ size_t mla_layer_workspace_bytes(const mla_batch *batch);
  * new latents + attention, output rounded to bf16, which is where the value
  * up-projection rounds it anyway) and mla_post_attn, enqueued on one stream.
  * A chunk request of c >= 256 rows at prefix p whose query-key pairs per key,
- * c (p + c / 2) / (p + c), reach 1200 takes the multi-head form instead of
+ * c (p + c / 2) / (p + c), reach 950 takes the multi-head form instead of
  * the absorbed one (same result up to rounding; about 30% of the flops per
  * query-key pair): its keys 0 .. p + c - 1 are up-projected once to per-head
  * keys W_UK c and values W_UV c (fp16), then causal attention runs per head

@@ -248,15 +248,17 @@ int post_attn(int T, const void *attn_out, int32_t attn_dtype, const mla_proj_we
 // Which chunk requests take the multi-head path in the layer (up-projected
 // keys and values, 192 + 128 dims per head: about 30% of the absorbed form's
 // flops per query-key pair, for one up-projection of the request's keys).
-// Measured on MI355X, the multi-head kernel saves about 9 ps per query-key
-// pair (all 16 heads) against the absorbed one and the up-projection costs
-// about 7.7 ns per key, so it pays from about 850 pairs per key; 1200 leaves
-// room for its launches and for the short blocks of small chunks.
+// Measured on MI355X, the multi-head kernel saves about 14 ps per query-key
+// pair (all 16 heads) against the absorbed one on a full grid and the
+// up-projection costs about 7.6 ns per key, so it pays from about 550 pairs
+// per key; chunks of fewer than 2048 rows fill only part of the chip with its
+// 128-token blocks, and a sweep over the benchmark workloads put the measured
+// break-even between 896 (slower) and 967 (faster) pairs per key.
 // MLA_LAYER_MHA_MIN (>= 2) and MLA_LAYER_MHA_PAIRS (>= 0) override the two
 // numbers; with MLA_LAYER_MHA_MIN alone every request of that many rows
 // takes the path.
 constexpr int kMhaMinRows = 256;
-constexpr int kMhaPairsPerKey = 1200;
+constexpr int kMhaPairsPerKey = 950;
 
 mla::ChunkRoute mha_route() {
     const int m = env_int("MLA_LAYER_MHA_MIN"), k = env_int("MLA_LAYER_MHA_PAIRS");

@@ -336,8 +336,9 @@ def test_layer_mixed_routing(weights, monkeypatch):
 @pytest.mark.parametrize("route", ["default", "multi_head"])
 def test_layer_four_chunks_full_size_sampled_rows(route, weights, monkeypatch):
     """One layer of the 27-layer workload: 64 decode rows and four 1024-token
-    chunks at prefixes 0 / 1024 / 3072 / 8192 (absorbed by default: too few
-    pairs per key; with the row minimum alone, all four multi-head)."""
+    chunks at prefixes 0 / 1024 / 3072 / 8192 (by default the one at 8192
+    goes multi-head, the others have too few pairs per key; with the row
+    minimum alone, all four)."""
     if route == "multi_head":
         monkeypatch.setenv("MLA_LAYER_MHA_MIN", "256")
     wl = W.config(5)
