@@ -2,11 +2,20 @@
 """Benchmark of one decode-node mixed step (latent append + mixed-step
 attention) on one MI355X, through the C ABI.
 
-Default workload: one layer, 32 decode requests with lognormal contexts
-(median 1024, sigma 1.0, clipped to [16, 8192]) plus one 512-token prefill
-chunk at prefix 0, page size 64 (the paper's scenario of section 3.2: a
-decode batch with a chunked prefill injected).  `--config N` picks another
-workload (1..5; `--chunk C` sets workload 4's chunk length).
+Headline (default): the full-depth step, 27 layers back to back on one stream,
+each with its own paged latent cache; per layer 64 decode requests (lognormal
+contexts, median 4096, sigma 1.0, clipped to 32768) plus the chunks of four
+deflected prompts, 1024 tokens each at prefixes 0 / 1024 / 3072 / 8192, page
+size 64 (the paper's mixed step: section 2.3, section 4.3.1 Eq. 4; the model of
+section 6).  `--config N` picks another workload (1..5; `--chunk C` sets
+workload 4's chunk length).
+
+The same JSON line also carries sub-records (unless --no-sub): workload 2
+(32 decodes + a 512-token chunk), workload 3 (128 decodes + a 2048-token
+chunk over a 6144-token prefix), the step-latency curve over the prefill
+chunk length C = 0 .. 4096 at the fixed 256-request decode batch of
+workload 4, and plan-inclusive steps (decode lengths grow by one token every
+step, so the host plans every step).
 
 Timing: W untimed warm-up steps, then K timed steps bracketed by
 torch.cuda.synchronize().  All inputs are resident in HBM before timing
@@ -15,8 +24,8 @@ independent copies of its buffers (pool, queries, new latents, outputs) that
 the rotating working set is >= 1 GiB, four times the 256 MB last-level
 (Infinity) cache, so bytes really come from HBM.
 
-Printed: one JSON line (metric, value = us/step, roofline of the dominant
-kernel from HIP events on its stream, CPU-oracle baseline on rank 0).
+Printed: one JSON line (metric, value = us/step, roofline of the mixed_step
+call from HIP events on its stream, CPU-oracle baseline on rank 0).
 """
 import argparse
 import json
@@ -35,6 +44,8 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16/fp16 MFMA
 ROTATE_TARGET_BYTES = 1 << 30
 METRIC = "mixed-step MLA attention µs/step; TB/s & TFLOP/s as % of combined roofline"
+DEFAULT_CONFIG = 5
+CPU_SAMPLE_PAIRS = 4_000_000  # query-key pairs of the oracle sample (10-30 s of host work in all)
 
 
 def log(msg):
@@ -75,50 +86,79 @@ def profiled_traffic(config_idx):
 def algorithmic_work(batch, out_bytes_per_elem=4):
     """Bytes and flops the method must move / compute for one layer.
 
-    attention: every row's keys are read once (1152 B per cached or new latent
-    of each request), queries read once (16 x 576 bf16 per row), outputs
-    written once (16 x 512 per row), lse written (16 fp32 per row), block-table
-    entries read once.  append: new latents read once and written once.
-    flops: 2 x 16 x (576 + 512) per (query token, visible key) pair.
+    Fused step (append + attention): every cached key read once (1152 B per
+    cached latent), every new latent read once and written once into its
+    page, queries read once (16 x 576 bf16 per row), outputs written once
+    (16 x 512 per row), block-table entries read once, plus the two length
+    words of each request.  The attention call alone (append done before)
+    reads the new latents from the cache instead: 1152 B per key, cached or
+    new, and writes none.  flops: 2 x 16 x (576 + 512) per (query token,
+    visible key) pair.  lse and softmax work are not counted.
     """
     p = batch.prefix_lens.astype(np.int64)
     c = batch.q_lens.astype(np.int64)
     T = int(c.sum())
     keys = int((p + c).sum())
     pages = int(np.ceil((p + c) / batch.page_size).sum())
-    attn_bytes = 1152 * keys + 18432 * T + 16 * 512 * out_bytes_per_elem * T + 64 * T + 4 * pages + 8 * batch.num_reqs
-    append_bytes = 2 * 1152 * T + 8 * batch.num_reqs
+    common = 18432 * T + 16 * 512 * out_bytes_per_elem * T + 4 * pages + 8 * batch.num_reqs
+    step_bytes = 1152 * int(p.sum()) + 2 * 1152 * T + common
+    attn_bytes = 1152 * keys + common
     pairs = int((c * p + c * (c + 1) // 2).sum())
     flops = 34816 * pairs
-    return {"attn_bytes": attn_bytes, "append_bytes": append_bytes, "step_bytes": attn_bytes + append_bytes,
-            "flops": flops, "pairs": pairs, "rows": T, "keys": keys}
+    return {"attn_bytes": attn_bytes, "step_bytes": step_bytes, "flops": flops, "pairs": pairs, "rows": T,
+            "keys": keys}
+
+
+def ideal_time_us(step_bytes, step_flops):
+    return max(step_bytes / (HBM_PEAK_GBS * 1e9), step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6
+
+
+def bound_of(step_bytes, step_flops):
+    return "hbm" if step_bytes / HBM_PEAK_GBS >= step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e3) else "mfma"
+
+
+def summary(wl, m, two_call=False):
+    """Step figures of one measured workload (all layers of a step)."""
+    work, L = m["work"], wl.num_layers
+    step_bytes = (work["attn_bytes"] if two_call else work["step_bytes"]) * L
+    step_flops = work["flops"] * L
+    ideal = ideal_time_us(step_bytes, step_flops)
+    us = m["us_per_step"]
+    return {"workload": wl.name, "us_per_step": round(us, 3), "ideal_us": round(ideal, 3),
+            "roofline_frac": round(ideal / us, 4), "bound": bound_of(step_bytes, step_flops),
+            "TB_per_s": round(step_bytes / (us * 1e-6) / 1e12, 3),
+            "TFLOP_per_s": round(step_flops / (us * 1e-6) / 1e12, 2),
+            "call_us": {"mean": round(m["attn_us"], 3), "p10": round(m["p10"], 3), "p50": round(m["p50"], 3),
+                        "p90": round(m["p90"], 3)}}
 
 
 # -------------------------------------------------------------------- bench
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=DEFAULT_CONFIG)
     ap.add_argument("--chunk", type=int, default=2048, help="prefill chunk length of workload 4")
     ap.add_argument("--out-dtype", choices=["f32", "bf16"], default="f32")
     ap.add_argument("--no-rotate", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sub", action="store_true",
+                    help="only the selected workload (no sub-records for workloads 2, 3, the workload-4 curve "
+                         "and the plan-inclusive steps)")
     ap.add_argument("--two-call", action="store_true",
                     help="time append_latent_kv + mixed_step_attn instead of the fused mixed_step")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one device copy of this many MiB (counter calibration)")
-    ap.add_argument("--sweep", action="store_true",
-                    help="also report step latency vs prefill chunk length on workload 4 (C = 0 .. 4096)")
     ap.add_argument("--layer", action="store_true",
                     help="time the whole attention layer (projections + append + attention, mla_attention_layer) "
                          "instead of the mixed step alone")
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1 "
-                                   "(each decode node is an independent one-GPU unit)"}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only (--gpus 1): every decode node of the "
+                                   "paper's deployment is an independent one-GPU unit, and this build uses one "
+                                   f"GPU; --gpus {args.gpus} is not supported"}))
         sys.exit(2)
 
     import torch
@@ -136,26 +176,28 @@ def main():
     m = measure(args, wl, args.steps, args.warmup, calib=args.calib_copy_mib)
     work, b, L = m["work"], wl.batch, wl.num_layers
     out_bf16 = args.out_dtype == "bf16"
-    us_per_step, attn_us = m["us_per_step"], m["attn_us"]
+    us_per_step, call_us = m["us_per_step"], m["attn_us"]
+    head = summary(wl, m, args.two_call)
 
-    # the timed call: the fused step (append + attention), or the attention call alone
+    # roofline of the timed call (per layer): the fused step (attention_kernel
+    # with the append, plus the split merge when the batch has split rows), or
+    # the attention call alone
     call_bytes = work["attn_bytes"] if args.two_call else work["step_bytes"]
-    attn_gbs = call_bytes / (attn_us * 1e-6) / 1e9
-    attn_tflops = work["flops"] / (attn_us * 1e-6) / 1e12
-    step_bytes = work["step_bytes"] * L
-    step_flops = work["flops"] * L
-    ideal_us = ideal_time_us(step_bytes, step_flops)
-    bound = "hbm" if step_bytes / HBM_PEAK_GBS >= step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e3) else "mfma"
+    bound = bound_of(call_bytes, work["flops"])
     if bound == "hbm":
-        roof = {"bound": "hbm", "achieved": round(attn_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(attn_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+        ach = call_bytes / (call_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4)}
     else:
-        roof = {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(attn_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+        ach = work["flops"] / (call_us * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4)}
     roof["traffic"] = profiled_traffic(args.config) if not (out_bf16 or args.two_call) else None
-    roof["kernel"] = ("mixed_step_attn (attention_kernel + combine_kernel)" if args.two_call
-                      else "mixed_step (attention_kernel with the fused append + combine_kernel)")
-    roof["per_launch_us"] = round(attn_us, 3)
+    roof["kernel"] = ("mixed_step_attn call (attention_kernel + combine_kernel)" if args.two_call
+                      else "mixed_step call (attention_kernel with the fused append, + combine_kernel when rows "
+                           "are split)")
+    roof["per_launch_us"] = round(call_us, 3)
+    roof["launches_per_step"] = L
     roof["algorithmic_bytes"] = call_bytes
     roof["algorithmic_flops"] = work["flops"]
 
@@ -176,29 +218,37 @@ def main():
                    "rows": work["rows"], "decode_rows": wl.num_decode, "chunks": [list(x) for x in wl.chunks],
                    "out_dtype": args.out_dtype, "rotating_sets": m["n_rot"], "parallelism": "single GPU",
                    "entry": "append_latent_kv + mixed_step_attn" if args.two_call else "mixed_step"},
-        "step": {"ideal_us": round(ideal_us, 3), "roofline_frac": round(ideal_us / us_per_step, 4),
-                 "bound": bound, "TB_per_s": round(step_bytes / (us_per_step * 1e-6) / 1e12, 3),
-                 "TFLOP_per_s": round(step_flops / (us_per_step * 1e-6) / 1e12, 2),
-                 "algorithmic_bytes": step_bytes, "algorithmic_flops": step_flops,
-                 "attention_call_us": {"mean": round(attn_us, 3), "p10": round(m["p10"], 3),
-                                       "p50": round(m["p50"], 3), "p90": round(m["p90"], 3)}},
+        "step": {"ideal_us": head["ideal_us"], "roofline_frac": head["roofline_frac"], "bound": head["bound"],
+                 "TB_per_s": head["TB_per_s"], "TFLOP_per_s": head["TFLOP_per_s"],
+                 "algorithmic_bytes": call_bytes * L, "algorithmic_flops": work["flops"] * L,
+                 "call_us": head["call_us"]},
         "roofline": roof,
     }
 
-    if args.sweep:
+    if not args.no_sub:
+        sub = {}
+        n_sub, w_sub = max(10, args.steps), max(3, args.warmup)
+        for idx in (2, 3):
+            if idx == args.config:
+                continue
+            wi = W.config(idx)
+            sub[f"workload_{idx}"] = summary(wi, measure(args, wi, n_sub, w_sub))
+            del wi
         # step latency vs prefill chunk length at the fixed decode batch of
         # workload 4 (the paper's chi counts decode + prefill tokens: 256 + C)
         curve = []
         for c in W.CHUNK_SWEEP:
             wc = W.config(4, chunk=c)
-            mc = measure(args, wc, max(10, args.steps // 4), max(3, args.warmup // 4))
-            wk = mc["work"]
-            ideal_c = ideal_time_us(wk["step_bytes"], wk["flops"])
-            curve.append({"chunk": c, "chi": wc.num_decode + c, "us_per_step": round(mc["us_per_step"], 2),
-                          "ideal_us": round(ideal_c, 2), "roofline_frac": round(ideal_c / mc["us_per_step"], 4)})
-            log(f"[bench] sweep C={c}: {mc['us_per_step']:.1f} us/step (ideal {ideal_c:.1f})")
-        result["curve"] = {"workload": "256 decode (uniform 512..16384) + C-token chunk at prefix 0, page 64",
-                           "points": curve}
+            s = summary(wc, measure(args, wc, n_sub, w_sub))
+            curve.append({"chunk": c, "chi": wc.num_decode + c, "us_per_step": s["us_per_step"],
+                          "ideal_us": s["ideal_us"], "roofline_frac": s["roofline_frac"], "bound": s["bound"]})
+            log(f"[bench] curve C={c}: {s['us_per_step']:.1f} us/step (ideal {s['ideal_us']:.1f})")
+            del wc
+        sub["workload_4_curve"] = {"workload": "256 decode (uniform 512..16384) + C-token chunk at prefix 0, "
+                                               "page 64", "points": curve}
+        sub["plan_inclusive"] = [plan_inclusive(args, W.config(idx), n_sub, w_sub) for idx in (2, args.config)
+                                 if idx in (2, 3, 5)]
+        result["sub"] = sub
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.config)
@@ -349,14 +399,11 @@ def layer_bench(args, wl):
     }
 
 
-def ideal_time_us(step_bytes, step_flops):
-    return max(step_bytes / (HBM_PEAK_GBS * 1e9), step_flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6
-
-
-def measure(args, wl, steps, warmup, calib=0):
+def measure(args, wl, steps, warmup, calib=0, batches=None):
     """Upload one workload (rotating buffer sets), time `steps` whole steps
     after `warmup` untimed ones, then the same steps again with HIP events
-    around each attention call on its stream."""
+    around each attention call on its stream.  `batches`: one
+    DeviceBatch per step (warm-up steps first) instead of the workload's own."""
     import torch
 
     import paper_2607_02043_amd as mla
@@ -369,8 +416,9 @@ def measure(args, wl, steps, warmup, calib=0):
     L = wl.num_layers
     log(f"[bench] workload: {wl.name}; rows={work['rows']} keys={work['keys']} pairs={work['pairs']}")
 
-    db = mla.DeviceBatch.from_batch(b, device=dev)
-    ws = mla.workspace_for(db, device=dev)
+    dbs = batches if batches is not None else [mla.DeviceBatch.from_batch(b, device=dev)]
+    ws_bytes = max(mla.mixed_step_workspace_bytes(d) for d in dbs)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes > 0 else None
 
     def up(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
@@ -402,6 +450,7 @@ def measure(args, wl, steps, warmup, calib=0):
     scale = W.SOFTMAX_SCALE
 
     def step(k, ev=None):
+        db = dbs[k % len(dbs)]
         for j, d in enumerate(rotations[k % n_rot]):
             if args.two_call:
                 mla.append_latent_kv(db, d["new"], d["pool"], stream)
@@ -431,7 +480,7 @@ def measure(args, wl, steps, warmup, calib=0):
     # timed region: whole steps
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    for k in range(steps):
+    for k in range(warmup, warmup + steps):
         step(k)
     torch.cuda.synchronize()
     t_total = time.perf_counter() - t_start
@@ -442,7 +491,7 @@ def measure(args, wl, steps, warmup, calib=0):
            for _ in range(steps)]
     torch.cuda.synchronize()
     for k in range(steps):
-        step(k, evs[k])
+        step(warmup + k, evs[k])
     torch.cuda.synchronize()
     attn_ms = [e0.elapsed_time(e1) for row in evs for e0, e1 in row]
     attn_us = float(np.mean(attn_ms)) * 1e3
@@ -453,6 +502,44 @@ def measure(args, wl, steps, warmup, calib=0):
     torch.cuda.empty_cache()
     return {"work": work, "us_per_step": us_per_step, "attn_us": attn_us, "p10": p10, "p50": p50, "p90": p90,
             "n_rot": n_rot}
+
+
+def plan_inclusive(args, wl, steps, warmup):
+    """Steps whose decode lengths grow by one token per step, as in serving:
+    every step is a new batch, so the host plans every step (a plan is reused
+    only across the layers of one step).  Step k of n uses decode prefixes
+    p - (n - 1) + k (clipped at 0), where p are the workload's, so every
+    appended slot lies inside the workload's block table and pool.  Reported:
+    the wall time per step of the whole loop (host checks, planning and
+    launches overlap the GPU work of the steps before) and the host time of
+    the checks and the planning alone, per new batch."""
+    import torch
+
+    import paper_2607_02043_amd as mla
+
+    dev = torch.device("cuda:0")
+    b = wl.batch
+    n = steps + warmup
+    dec = b.q_lens == 1
+    batches = []
+    for k in range(n):
+        p = b.prefix_lens.astype(np.int64).copy()
+        p[dec] = np.maximum(0, p[dec] - (n - 1) + k)
+        batches.append(mla.DeviceBatch(b.q_lens, p.astype(np.int32), b.block_table, b.page_size, b.num_pages,
+                                       device=dev))
+    reps = []
+    for _ in range(5):  # every call meets a new batch: the plan cache never hits
+        t = time.perf_counter()
+        for db in batches:
+            mla.mixed_step_workspace_bytes(db)
+        reps.append((time.perf_counter() - t) / n * 1e6)
+    m = measure(args, wl, steps, warmup, batches=batches)
+    s = summary(wl, m)
+    s["workload"] = wl.name + "; decode lengths +1 per step"
+    s["host_plan_us"] = {"median": round(float(np.median(reps)), 2), "min": round(float(np.min(reps)), 2)}
+    log(f"[bench] plan-inclusive {wl.name[:40]}: {s['us_per_step']:.1f} us/step, host plan "
+        f"{s['host_plan_us']['median']:.1f} us")
+    return s
 
 
 def cpu_baseline(wl, cfg, layer=False):
@@ -467,19 +554,19 @@ def cpu_baseline(wl, cfg, layer=False):
     li = wl.layer(0)
     work = algorithmic_work(b)
     total_pairs = work["pairs"]
-    if total_pairs <= 400_000:
+    if total_pairs <= CPU_SAMPLE_PAIRS:
         rows = None
         sample = "one full layer step (append + every row)"
         frac = 1.0
     else:
-        # a seeded sample of rows whose pairs add up to about 400k (a few seconds of fp64 work)
+        # a seeded sample of rows whose pairs add up to about 4M (several seconds of fp64 work per run)
         rng = np.random.default_rng(0)
         order = rng.permutation(b.num_rows)
         cu = b.cu_q
         req_of = np.searchsorted(cu, np.arange(b.num_rows), side="right") - 1
         pairs_of = b.prefix_lens[req_of].astype(np.int64) + (np.arange(b.num_rows) - cu[req_of]) + 1
         csum = np.cumsum(pairs_of[order])
-        n = int(np.searchsorted(csum, 400_000)) + 1
+        n = int(np.searchsorted(csum, CPU_SAMPLE_PAIRS)) + 1
         rows = np.sort(order[:n])
         frac = float(pairs_of[rows].sum()) / total_pairs
         sample = f"{len(rows)} seeded random rows ({frac * 100:.2f}% of one layer's query-key pairs), scaled up"

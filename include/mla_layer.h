@@ -103,18 +103,37 @@ int mla_post_attn(int32_t num_rows, const void *attn_out, int32_t attn_dtype, co
  * before the workspace is first used (see mixed_step_workspace_bytes). */
 size_t mla_layer_workspace_bytes(const mla_batch *batch);
 
+/* Tuning overrides, process-wide (for tuning and tests; every later call on
+ * any thread sees them).  value -1 restores the library's own choice.
+ *   MLA_TUNE_GEMM_BM / _BN / _DEPTH  GEMM tile rows, columns, LDS stages (a
+ *       shape that is not instantiated fails the launch with MLA_ERR_HIP);
+ *   MLA_TUNE_MHA_MIN_ROWS (>= 2)  chunk requests of at least this many rows
+ *       take the layer's multi-head path (off by default);
+ *   MLA_TUNE_MHA_PAIRS (>= 0)  and only those whose query-key pairs per key,
+ *       c (p + c / 2) / (p + c), reach this many.
+ * The first values come from the environment variables MLA_GEMM_BM,
+ * MLA_GEMM_BN, MLA_GEMM_D, MLA_LAYER_MHA_MIN and MLA_LAYER_MHA_PAIRS, read
+ * once.  Errors: MLA_ERR_INVALID_ARG (unknown knob, value < -1). */
+typedef enum {
+    MLA_TUNE_GEMM_BM = 0,
+    MLA_TUNE_GEMM_BN = 1,
+    MLA_TUNE_GEMM_DEPTH = 2,
+    MLA_TUNE_MHA_MIN_ROWS = 3,
+    MLA_TUNE_MHA_PAIRS = 4,
+    MLA_TUNE_COUNT = 5
+} mla_tune_knob;
+int mla_layer_tune(int32_t knob, int32_t value);
+
 /* One attention layer of the step: mla_pre_attn, mixed_step (append of the
  * new latents + attention, output rounded to bf16, which is where the value
  * up-projection rounds it anyway) and mla_post_attn, enqueued on one stream.
- * A chunk request of c >= 256 rows at prefix p whose query-key pairs per key,
- * c (p + c / 2) / (p + c), reach 950 takes the multi-head form instead of
- * the absorbed one (same result up to rounding; about 30% of the flops per
- * query-key pair): its keys 0 .. p + c - 1 are up-projected once to per-head
- * keys W_UK c and values W_UV c (fp16), then causal attention runs per head
- * over 128 + 64 query / key dims and 128 value dims; the other rows run on
- * the absorbed kernel.  The environment variables MLA_LAYER_MHA_MIN (row
- * minimum, >= 2; set alone it drops the pairs rule) and MLA_LAYER_MHA_PAIRS
- * (>= 0) override the two numbers.
+ * Optionally (MLA_TUNE_MHA_MIN_ROWS) a long chunk request takes the
+ * multi-head form instead of the absorbed one (same result up to rounding;
+ * about 30% of the flops per query-key pair): its keys 0 .. p + c - 1 are
+ * up-projected once to per-head keys W_UK c and values W_UV c, stored in
+ * fp16 (|values| must stay below 65504), then causal attention runs per head
+ * over 128 + 64 query / key dims and 128 value dims with fp16 probabilities;
+ * the other rows run on the absorbed kernel.
  *   hidden    DEVICE bf16 [T][2048]
  *   kv_cache  DEVICE bf16 [num_pages][P][576], updated with the step's latents
  *   out       DEVICE [T][2048] fp32 or bf16 (out_dtype)

@@ -43,8 +43,23 @@
  *     prefix_lens).  Block-table entries are not read on the host; kernels
  *     guard every page id (an id outside [0, num_pages) is never dereferenced:
  *     append skips that slot, attention reads page 0 in its place) so a bad
- *     table gives wrong numbers, not a memory fault.
- *   - Two requests must not map the same written slot (undefined result).
+ *     table gives wrong numbers, not a memory fault, and raises the device
+ *     flag MLA_FLAG_BAD_PAGE (see mla_device_flags).
+ *   - Two requests must not map the same written slot, nor may a request
+ *     read a slot another request writes in the same step (undefined result).
+ *   - Check mode (mla_debug_set(MLA_DEBUG_CHECK, 1), or MLASTEP_CHECK=1 in the
+ *     environment when the library first runs): before launching, every entry
+ *     point synchronises the stream and checks on the host that the device
+ *     lengths equal the host ones, that every block-table entry a request uses
+ *     lies in [0, num_pages) and that no written slot is aliased as above
+ *     (MLA_ERR_INVALID_ARG); after launching it synchronises again and turns
+ *     the device flags into MLA_ERR_INVALID_ARG (bad page) or MLA_ERR_HIP
+ *     (an expired wait).  For debugging: it makes every call synchronous.
+ *   - Chunk rows (c_r > 1) carry the value dims through fp16 for their
+ *     probability x value products: value dims of magnitude up to 65504 are
+ *     exact, larger ones are clamped to +-65504 (wrong results); magnitudes
+ *     below 2^-14 keep the fp16 subnormal spacing of 2^-24.  Decode rows keep
+ *     bf16 values as they are.
  *   - Reentrant; concurrent calls on different streams need distinct
  *     workspaces.
  */
@@ -58,7 +73,7 @@
 extern "C" {
 #endif
 
-#define MLA_ABI_VERSION 2
+#define MLA_ABI_VERSION 3
 #define MLA_NUM_HEADS 16
 #define MLA_D_QK 576 /* latent width: 512 compressed + 64 rope dims */
 #define MLA_D_V 512  /* value width: the first 512 latent dims */
@@ -88,6 +103,26 @@ typedef struct mla_batch {
 
 /* ABI version of the loaded library (MLA_ABI_VERSION it was built with). */
 int mla_abi_version(void);
+
+/* Device-side error flags (sticky, per device, raised by any call of this
+ * library on the current device since they were last cleared). */
+#define MLA_FLAG_BAD_PAGE 1     /* a block-table entry outside [0, num_pages) was met */
+#define MLA_FLAG_WAIT_EXPIRED 2 /* a bounded wait inside a kernel gave up: that call's results are undefined */
+
+/* Synchronises `stream`, then stores the current device's flags in *flags
+ * and clears them if `clear` is non-zero.  Errors: MLA_ERR_INVALID_ARG (flags
+ * NULL), MLA_ERR_HIP. */
+int mla_device_flags(int32_t clear, int32_t *flags, void *stream);
+
+/* Debug settings, process-wide:
+ *   MLA_DEBUG_CHECK       0 / 1: check mode (see Conventions); the first value
+ *                         comes from the environment variable MLASTEP_CHECK;
+ *   MLA_DEBUG_SPIN_LIMIT  sleeps a bounded wait inside a kernel takes before
+ *                         it gives up (-1: the default, 65536); for tests of
+ *                         the flag only: a small limit gives wrong results.
+ * Errors: MLA_ERR_INVALID_ARG (unknown knob, bad value). */
+typedef enum { MLA_DEBUG_CHECK = 0, MLA_DEBUG_SPIN_LIMIT = 1, MLA_DEBUG_COUNT = 2 } mla_debug_knob;
+int mla_debug_set(int32_t knob, int32_t value);
 
 /* Message of the last non-OK return on this thread ("" if none). */
 const char *mla_last_error(void);

@@ -31,6 +31,16 @@ the same arithmetic in float64, but each value that the GPU path stores in
 bf16 is rounded to bf16 (nearest, ties to even) at that point: q[..][:128]
 before the absorption, q_abs, latent, the attention output before W_UV, o,
 and the result when a bf16 result is asked for.
+
+The multi-head form of a chunk request (`layer_multihead`) has storage points
+of its own, rounded the same way in the rounded mode: the per-head keys
+W_UK[h] c and values W_UV[h] c of every visible latent c are stored in fp16
+(round to nearest even; the rope key c[512:] is a bf16 value, exact in
+fp16), the query is the bf16 q[..][:128] with the bf16 rope part of q_abs,
+and the per-head output o is stored in bf16 before W_o.  The softmax
+probabilities, which the GPU also holds in fp16 against a running maximum,
+are not rounded here: their rounding depends on the order in which keys
+arrive, which is not part of the definition.
 """
 from __future__ import annotations
 
@@ -252,3 +262,42 @@ def logical_cache(batch, pool_bits) -> List[np.ndarray]:
         rows = [pool[batch.block_table[r][j // batch.page_size], j % batch.page_size] for j in range(p)]
         out.append(np.array(rows, dtype=np.float64).reshape(p, DQK))
     return out
+
+
+def round_f16(x) -> np.ndarray:
+    """float64 values of x rounded once to IEEE half (nearest, ties to even)."""
+    return np.asarray(x, dtype=np.float64).astype(np.float16).astype(np.float64)
+
+
+def layer_multihead(batch, hidden_bits, W: Weights, pool_bits, scale: float, multi_head, rows=None):
+    """The layer in the rounded mode where chunk requests with
+    multi_head(p, c) true take the multi-head form (storage points in the
+    module doc) and every other row the absorbed form (`layer`).  Returns
+    out [T or len(rows)][2048] (float64)."""
+    ref, pool_after, q_bits, lat_bits = layer(batch, hidden_bits, W, pool_bits, scale, rows=None)
+    pos = positions(batch.q_lens, batch.prefix_lens)
+    x = bf16_value(hidden_bits)
+    q_nope = through_bf16((x @ W.w_q.T).reshape(-1, HEADS, QK)[:, :, :NOPE])  # [T][16][128]
+    q_rope = bf16_value(q_bits)[:, :, LATENT:]  # [T][16][64], the rope part of q_abs
+    pool = bf16_value(pool_after)
+    w_uk = np.transpose(W.w_uk_t, (0, 2, 1))  # [16][128][512] = W_UK[h][d][c]
+    row = 0
+    for r in range(batch.num_reqs):
+        c, p = int(batch.q_lens[r]), int(batch.prefix_lens[r])
+        if c > 1 and multi_head(p, c):
+            n = p + c
+            lat = np.array([pool[batch.block_table[r][j // batch.page_size], j % batch.page_size] for j in range(n)])
+            o = np.empty((c, HEADS, VHEAD))
+            for h in range(HEADS):
+                k_nope = round_f16(lat[:, :LATENT] @ w_uk[h].T)  # [n][128]
+                vals = round_f16(lat[:, :LATENT] @ W.w_uv[h].T)  # [n][128]
+                k_rope = lat[:, LATENT:]  # bf16 values, exact in fp16
+                for i in range(c):
+                    t = row + i
+                    s = scale * (k_nope[:p + i + 1] @ q_nope[t, h] + k_rope[:p + i + 1] @ q_rope[t, h])
+                    w = np.exp(s - s.max())
+                    o[i, h] = (w @ vals[:p + i + 1]) / w.sum()
+            o = through_bf16(o.reshape(c, HEADS * VHEAD))
+            ref[row:row + c] = o @ W.w_o.T
+        row += c
+    return ref if rows is None else ref[np.asarray(rows)]

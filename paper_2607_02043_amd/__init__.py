@@ -24,11 +24,17 @@ MLA_OUT_F32 = 0
 MLA_OUT_BF16 = 1
 NUM_HEADS, D_QK, D_V = 16, 576, 512
 
-EXPORTED = ("mla_abi_version", "mla_last_error", "mixed_step_workspace_bytes", "append_latent_kv",
-            "mixed_step_attn", "mixed_step")
+EXPORTED = ("mla_abi_version", "mla_last_error", "mla_device_flags", "mla_debug_set", "mixed_step_workspace_bytes",
+            "append_latent_kv", "mixed_step_attn", "mixed_step")
+MLA_FLAG_BAD_PAGE = 1
+MLA_FLAG_WAIT_EXPIRED = 2
+MLA_DEBUG_CHECK = 0
+MLA_DEBUG_SPIN_LIMIT = 1
 # include/mla_layer.h
 EXPORTED_LAYER = ("mla_proj_workspace_bytes", "mla_pre_attn", "mla_post_attn", "mla_layer_workspace_bytes",
-                  "mla_attention_layer")
+                  "mla_attention_layer", "mla_layer_tune")
+# mla_layer_tune knobs (include/mla_layer.h)
+TUNE_GEMM_BM, TUNE_GEMM_BN, TUNE_GEMM_DEPTH, TUNE_MHA_MIN_ROWS, TUNE_MHA_PAIRS = range(5)
 HIDDEN = 2048
 
 
@@ -92,6 +98,10 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_size_t, ctypes.c_void_p]
         L.mixed_step.restype = ctypes.c_int
         vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.mla_device_flags.argtypes = [i32, ctypes.POINTER(ctypes.c_int32), vp]
+        L.mla_device_flags.restype = ctypes.c_int
+        L.mla_debug_set.argtypes = [i32, i32]
+        L.mla_debug_set.restype = ctypes.c_int
         wp = ctypes.POINTER(mla_proj_weights)
         L.mla_proj_workspace_bytes.argtypes = [i32]
         L.mla_proj_workspace_bytes.restype = sz
@@ -104,6 +114,8 @@ def lib() -> ctypes.CDLL:
         L.mla_attention_layer.argtypes = [ctypes.POINTER(mla_batch), vp, wp, vp, ctypes.c_float, vp, i32, vp, sz,
                                           vp]
         L.mla_attention_layer.restype = ctypes.c_int
+        L.mla_layer_tune.argtypes = [i32, i32]
+        L.mla_layer_tune.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -162,6 +174,19 @@ class DeviceBatch:
 
 def abi_version() -> int:
     return int(lib().mla_abi_version())
+
+
+def device_flags(clear: bool = True, stream=None) -> int:
+    """The current device's sticky kernel error flags (MLA_FLAG_*), after
+    synchronising `stream`; cleared unless clear is False."""
+    f = ctypes.c_int32(0)
+    _check(lib().mla_device_flags(1 if clear else 0, ctypes.byref(f), _stream(stream)))
+    return int(f.value)
+
+
+def debug_set(knob: int, value: int) -> None:
+    """Process-wide debug setting (MLA_DEBUG_CHECK: 0/1; MLA_DEBUG_SPIN_LIMIT: >= 0, -1 = default)."""
+    _check(lib().mla_debug_set(int(knob), int(value)))
 
 
 def mixed_step_workspace_bytes(batch: DeviceBatch) -> int:
@@ -276,3 +301,26 @@ def layer_workspace_for(batch: DeviceBatch, device="cuda"):
     import torch
     n = mla_layer_workspace_bytes(batch)
     return torch.zeros(n, dtype=torch.uint8, device=device) if n > 0 else None
+
+
+def layer_tune(knob: int, value: int) -> None:
+    """Process-wide tuning override of the layer (mla_layer_tune); -1 restores the default."""
+    _check(lib().mla_layer_tune(int(knob), int(value)))
+
+
+class tuned:
+    """Context manager: set layer tuning knobs ({knob: value}) and restore
+    the library defaults (-1) on exit."""
+
+    def __init__(self, settings):
+        self.settings = dict(settings)
+
+    def __enter__(self):
+        for k, v in self.settings.items():
+            layer_tune(k, v)
+        return self
+
+    def __exit__(self, *exc):
+        for k in self.settings:
+            layer_tune(k, -1)
+        return False

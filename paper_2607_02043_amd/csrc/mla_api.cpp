@@ -10,6 +10,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -55,6 +56,22 @@ int cu_count(int *status) {
     }
     return cache[dev];
 }
+
+// Debug settings (mla_debug_set): check mode, first value from the
+// environment variable MLASTEP_CHECK (read once), and the spin limit of the
+// kernels' bounded waits.
+std::atomic<int> &debug_value(int knob) {
+    static std::atomic<int> v[MLA_DEBUG_COUNT] = {};
+    static std::once_flag once;
+    std::call_once(once, [] {
+        const char *e = std::getenv("MLASTEP_CHECK");
+        v[MLA_DEBUG_CHECK].store(e && std::atoi(e) != 0 ? 1 : 0);
+        v[MLA_DEBUG_SPIN_LIMIT].store(mla::kSpinLimit);
+    });
+    return v[knob];
+}
+
+bool check_mode() { return debug_value(MLA_DEBUG_CHECK).load(std::memory_order_relaxed) != 0; }
 
 int ilog2_exact(int v) {
     int l = 0;
@@ -440,6 +457,79 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute rou
     return MLA_OK;
 }
 
+// Check mode, before a launch: the device copies of the lengths equal the
+// host ones, every block-table entry a request uses lies in the pool, and no
+// slot a request writes is written or read by another request (or twice by
+// one).  Synchronises the stream first (the device arrays may be produced on
+// it).
+int check_device_batch(const mla_batch *b, const Shape &sh, hipStream_t s) {
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "check mode: hipStreamSynchronize");
+    const size_t R = sh.R, mp = b->max_pages_per_req;
+    std::vector<int32_t> cu(R + 1), pre(R), bt(R * mp);
+    if ((e = hipMemcpy(cu.data(), b->cu_q_dev, (R + 1) * 4, hipMemcpyDeviceToHost)) != hipSuccess ||
+        (e = hipMemcpy(pre.data(), b->prefix_lens_dev, R * 4, hipMemcpyDeviceToHost)) != hipSuccess ||
+        (e = hipMemcpy(bt.data(), b->block_table_dev, R * mp * 4, hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(e, "check mode: reading the device batch arrays");
+    long long acc = 0;
+    for (size_t r = 0; r <= R; ++r) {
+        if (cu[r] != acc)
+            return fail(MLA_ERR_INVALID_ARG, "check mode: cu_q_dev[%zu] = %d, the host q_lens give %lld", r, cu[r], acc);
+        if (r < R) {
+            if (pre[r] != b->prefix_lens[r])
+                return fail(MLA_ERR_INVALID_ARG, "check mode: prefix_lens_dev[%zu] = %d, host prefix_lens %d", r, pre[r],
+                            b->prefix_lens[r]);
+            acc += b->q_lens[r];
+        }
+    }
+    const long long P = b->page_size;
+    for (size_t r = 0; r < R; ++r) {
+        const long long n = ceil_div_ll((long long)b->prefix_lens[r] + b->q_lens[r], P);
+        for (long long j = 0; j < n; ++j) {
+            const int32_t id = bt[r * mp + j];
+            if (id < 0 || id >= b->num_pages)
+                return fail(MLA_ERR_INVALID_ARG,
+                            "check mode: request %zu, logical page %lld: block-table entry %d outside [0, %d)", r, j, id,
+                            b->num_pages);
+        }
+    }
+    const long long slots = (long long)b->num_pages * P;
+    if (slots <= (1LL << 28)) {
+        std::vector<int32_t> writer(slots, -1);
+        for (size_t r = 0; r < R; ++r)
+            for (long long t = b->prefix_lens[r]; t < (long long)b->prefix_lens[r] + b->q_lens[r]; ++t) {
+                const long long sl = (long long)bt[r * mp + t / P] * P + t % P;
+                if (writer[sl] >= 0)
+                    return fail(MLA_ERR_INVALID_ARG, "check mode: slot %lld is written by requests %d and %zu", sl,
+                                writer[sl], r);
+                writer[sl] = (int32_t)r;
+            }
+        for (size_t r = 0; r < R; ++r)
+            for (long long t = 0; t < b->prefix_lens[r]; ++t) {
+                const long long sl = (long long)bt[r * mp + t / P] * P + t % P;
+                if (writer[sl] >= 0)
+                    return fail(MLA_ERR_INVALID_ARG,
+                                "check mode: request %zu reads key %lld from slot %lld, which request %d writes", r, t,
+                                sl, writer[sl]);
+            }
+    }
+    return MLA_OK;
+}
+
+// Check mode, after a launch: wait for the stream and turn the kernels' error
+// flags into a status.
+int check_after_launch(hipStream_t s, const char *what) {
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, what);
+    int flags = 0;
+    if ((e = mla::read_flags(&flags, true)) != hipSuccess) return hip_fail(e, "check mode: reading the device flags");
+    if (flags & mla::kFlagWaitExpired)
+        return fail(MLA_ERR_HIP, "check mode: %s: a bounded wait inside a kernel expired; results are undefined", what);
+    if (flags & mla::kFlagBadPage)
+        return fail(MLA_ERR_INVALID_ARG, "check mode: %s: a kernel met a block-table entry outside the pool", what);
+    return MLA_OK;
+}
+
 }  // namespace
 
 namespace mla {
@@ -505,8 +595,33 @@ int append_latent_kv(const mla_batch *batch, const uint16_t *new_latents, uint16
     a.log2_page = sh.log2_page;
     a.max_pages = batch->max_pages_per_req;
     a.num_pages = batch->num_pages;
-    hipError_t e = mla::launch_append(a, static_cast<hipStream_t>(stream));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool chk = check_mode();
+    if (chk && (st = check_device_batch(batch, sh, s)) != MLA_OK) return st;
+    hipError_t e = mla::launch_append(a, s);
     if (e != hipSuccess) return hip_fail(e, "append kernel launch");
+    return chk ? check_after_launch(s, "append_latent_kv") : MLA_OK;
+}
+
+int mla_device_flags(int32_t clear, int32_t *flags, void *stream) {
+    g_err[0] = '\0';
+    if (!flags) return fail(MLA_ERR_INVALID_ARG, "flags is NULL");
+    *flags = 0;
+    hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    int f = 0;
+    if ((e = mla::read_flags(&f, clear != 0)) != hipSuccess) return hip_fail(e, "reading the device flags");
+    *flags = f;
+    return MLA_OK;
+}
+
+int mla_debug_set(int32_t knob, int32_t value) {
+    g_err[0] = '\0';
+    if (knob < 0 || knob >= MLA_DEBUG_COUNT) return fail(MLA_ERR_INVALID_ARG, "unknown debug knob %d", knob);
+    if (knob == MLA_DEBUG_CHECK && value != 0 && value != 1)
+        return fail(MLA_ERR_INVALID_ARG, "check mode must be 0 or 1, not %d", value);
+    if (knob == MLA_DEBUG_SPIN_LIMIT && value < -1) return fail(MLA_ERR_INVALID_ARG, "spin limit %d < -1", value);
+    debug_value(knob).store(knob == MLA_DEBUG_SPIN_LIMIT && value == -1 ? mla::kSpinLimit : value);
     return MLA_OK;
 }
 
@@ -569,15 +684,18 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
     a.merge_hsplit = pl.merge_hsplit;
     a.dec_total_tiles = pl.dec_total_tiles;
     a.out_bf16 = out_dtype == MLA_OUT_BF16 ? 1 : 0;
+    a.spin_limit = debug_value(MLA_DEBUG_SPIN_LIMIT).load(std::memory_order_relaxed);
     a.route = route;
     const hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool chk = check_mode();
+    if (chk && (st = check_device_batch(batch, sh, s)) != MLA_OK) return st;
     hipError_t e = mla::launch_attention(a, s);
     if (e != hipSuccess) return hip_fail(e, "attention kernel launch");
     if (pl.chunk_split || pl.dec_split) {
         e = mla::launch_combine(a, s);
         if (e != hipSuccess) return hip_fail(e, "merge kernel launch");
     }
-    return MLA_OK;
+    return chk ? check_after_launch(s, new_latents ? "mixed_step" : "mixed_step_attn") : MLA_OK;
 }
 
 }  // namespace

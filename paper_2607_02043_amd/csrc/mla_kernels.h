@@ -18,6 +18,9 @@ constexpr int kChunkBlockTokens = 8;                        // tokens per chunk 
 constexpr int kPartialFloats = kHeads * kDv;                // one row's partial output
 constexpr int kPartialStats = kHeads * 2;                   // one row's (max, sum) per head
 constexpr int kMaxDecSegments = 64;                         // requests one decode workgroup may touch
+constexpr int kFlagBadPage = 1;       // a block-table entry outside [0, num_pages) was met (MLA_FLAG_BAD_PAGE)
+constexpr int kFlagWaitExpired = 2;   // a bounded wait inside a kernel gave up (MLA_FLAG_WAIT_EXPIRED)
+constexpr int kSpinLimit = 1 << 16;   // sleeps of a bounded wait before it gives up
 
 struct AttnArgs {
     const uint16_t *q;
@@ -52,6 +55,7 @@ struct AttnArgs {
     int32_t grid;              // persistent workgroups of the attention launch
     int32_t merge_hsplit;      // merge workgroups per split decode row (1, 4 or 8: heads split among them)
     int32_t out_bf16;
+    int32_t spin_limit;        // sleeps of a bounded wait before it gives up (kSpinLimit)
     ChunkRoute route;          // chunk requests it sends to the multi-head path are left out of this launch
 };
 
@@ -70,6 +74,8 @@ struct AppendArgs {
 };
 
 hipError_t launch_append(const AppendArgs &a, hipStream_t s);
+// Reads the device's sticky kernel error flags (kFlag*), and clears them if asked.
+hipError_t read_flags(int *flags, bool clear);
 hipError_t launch_attention(const AttnArgs &a, hipStream_t s);
 hipError_t launch_combine(const AttnArgs &a, hipStream_t s);
 

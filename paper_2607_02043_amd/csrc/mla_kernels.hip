@@ -100,6 +100,15 @@ __shared__ int s_trace_item;
 
 constexpr float kLn2 = 0.69314718055994530942f;
 
+// Sticky error flags of the kernels on this device (MLA_FLAG_* of
+// mla_step.h): raised on the rare error paths only, read and cleared by the
+// host (mla_device_flags).
+__device__ int g_flags;
+
+__device__ __forceinline__ void raise_flag(int f) {
+    __hip_atomic_fetch_or(&g_flags, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------- helpers
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
@@ -280,7 +289,9 @@ __device__ __forceinline__ void load_page_window(const AttnArgs &a, int r, int l
     for (int i = threadIdx.x; i < n; i += blockDim.x) {
         const int lp = lp0 + i;
         int pg = lp < a.max_pages ? row[lp] : 0;
-        s_pages[i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
+        const bool ok = (unsigned)pg < (unsigned)a.num_pages;
+        if (!ok) raise_flag(kFlagBadPage);
+        s_pages[i] = ok ? pg : 0;
     }
 }
 
@@ -352,7 +363,10 @@ __device__ __forceinline__ void append_rows(const AttnArgs &a, int r, int key0, 
         const int key = key0 + i;
         const int lp = key >> a.log2_page;
         const int page = lp < a.max_pages ? btr[lp] : -1;
-        if ((unsigned)page >= (unsigned)a.num_pages) continue;
+        if ((unsigned)page >= (unsigned)a.num_pages) {
+            raise_flag(kFlagBadPage);
+            continue;
+        }
         const u32x4 v = *reinterpret_cast<const u32x4 *>(a.new_kv + (size_t)(row0 + i) * kDqk + c * 8);
         *reinterpret_cast<u32x4 *>(a.kv_out + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kDqk +
                                    c * 8) = v;
@@ -367,7 +381,10 @@ __device__ __forceinline__ void append_rows_group(const AttnArgs &a, int r, int 
         const int key = key0 + i;
         const int lp = key >> a.log2_page;
         const int page = lp < a.max_pages ? btr[lp] : -1;
-        if ((unsigned)page >= (unsigned)a.num_pages) continue;
+        if ((unsigned)page >= (unsigned)a.num_pages) {
+            raise_flag(kFlagBadPage);
+            continue;
+        }
         const u32x4 v = *reinterpret_cast<const u32x4 *>(a.new_kv + (size_t)(row0 + i) * kDqk + c * 8);
         *reinterpret_cast<u32x4 *>(a.kv_out + ((size_t)page * a.page_size + (key & (a.page_size - 1))) * kDqk +
                                    c * 8) = v;
@@ -632,17 +649,20 @@ __device__ __forceinline__ int item_tid() {
 // counter in LDS; epoch (wave-uniform) counts the group's barriers so far.
 // Each wave first waits for its own LDS accesses, so what it wrote before the
 // barrier is visible to the group after it.  The wait is bounded (far beyond
-// any real skew), so a broken count can only give wrong results, not a hang.
-__device__ __forceinline__ void group_barrier(int *ctr, int &epoch) {
+// any real skew): a broken count cannot hang the kernel; an expired wait
+// raises kFlagWaitExpired (that call's results are then undefined).
+__device__ __forceinline__ void group_barrier(int *ctr, int &epoch, int spin_limit) {
     ++epoch;
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     const int target = 4 * epoch;
-    for (int spin = 0; spin < (1 << 16); ++spin) {
+    int spin = 0;
+    for (; spin < spin_limit; ++spin) {
         const int seen = __builtin_amdgcn_readfirstlane(__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP));
         if (seen >= target) break;
         __builtin_amdgcn_s_sleep(1);
     }
+    if (spin == spin_limit && (threadIdx.x & 63) == 0) raise_flag(kFlagWaitExpired);
     asm volatile("" ::: "memory");
 }
 
@@ -691,7 +711,9 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
         for (int i = gtid; i < n && sg.pw + i < kPageWindow; i += kThreads) {
             const int lp = sg.lp0 + i;
             const int pg = lp < a.max_pages ? btr[lp] : 0;
-            s_pages[sg.pw + i] = ((unsigned)pg < (unsigned)a.num_pages) ? pg : 0;
+            const bool ok = (unsigned)pg < (unsigned)a.num_pages;
+            if (!ok) raise_flag(kFlagBadPage);
+            s_pages[sg.pw + i] = ok ? pg : 0;
         }
     }
     if (a.new_kv != nullptr) {  // fused append: the group holding a request's last tile writes its latent
@@ -732,7 +754,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
     for (int u = 0; u < n_units; ++u) {
         TRACE_TILE(u, 10);
         wait_dma_all();                // unit u (the only one in flight)
-        group_barrier(gbar, epoch);    // unit u landed; slot (u + 1) % 2 is free
+        group_barrier(gbar, epoch, a.spin_limit);    // unit u landed; slot (u + 1) % 2 is free
         bool tile_unit = false;
         DecSeg sg{};
         const char *slot = smem + grp * kDecGroupBytes + (u % kDecRing) * kDecTileBytes;
@@ -766,7 +788,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
             }
         }
         if (!tile_unit) continue;
-        group_barrier(gbar, epoch);  // partial score blocks complete
+        group_barrier(gbar, epoch, a.spin_limit);  // partial score blocks complete
         TRACE_TILE(u, 12);
         const int kbase = cons.t * kDecKeys;
         // full scores of this lane's head: x[kt][i] = key 16 kt + 4 g + i (kt = 0, 1)
@@ -1443,7 +1465,11 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < kAppendRowsPerWave; ++k) {
-        if (k >= nrows || (unsigned)page[k] >= (unsigned)a.num_pages) continue;
+        if (k >= nrows) continue;
+        if ((unsigned)page[k] >= (unsigned)a.num_pages) {
+            raise_flag(kFlagBadPage);
+            continue;
+        }
         u32x4 *dst = reinterpret_cast<u32x4 *>(a.kv + ((size_t)page[k] * a.page_size + slot_in_page[k]) * kDqk);
         dst[lane] = va[k];
         if (lane < kChunksPerRow - 64) dst[64 + lane] = vb[k];
@@ -1457,6 +1483,13 @@ extern "C" int mla_trace_read(void *dst, size_t bytes) {
     return (int)hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_trace), bytes, 0, hipMemcpyDeviceToHost);
 }
 #endif
+
+hipError_t read_flags(int *flags, bool clear) {
+    hipError_t e = hipMemcpyFromSymbol(flags, HIP_SYMBOL(g_flags), sizeof(int), 0, hipMemcpyDeviceToHost);
+    if (e != hipSuccess || !clear || *flags == 0) return e;
+    const int zero = 0;
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_flags), &zero, sizeof(int), 0, hipMemcpyHostToDevice);
+}
 
 hipError_t launch_append(const AppendArgs &a, hipStream_t s) {
     const int rows_per_block = 4 * kAppendRowsPerWave;

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
+#include <atomic>
 
 #include "api_util.h"
 #include "proj_kernels.h"
@@ -40,10 +41,36 @@ ProjLayout proj_layout(long long T) {
     return l;
 }
 
-int env_int(const char *name) {
+// Tuning overrides (mla_layer_tune), process-wide.  Their first values come
+// from the environment, read once: MLA_GEMM_BM / MLA_GEMM_BN / MLA_GEMM_D and
+// MLA_LAYER_MHA_MIN / MLA_LAYER_MHA_PAIRS (see mla_layer.h).  -1 = the
+// library's own choice.
+struct Tuning {
+    std::atomic<int> v[MLA_TUNE_COUNT];
+};
+
+int env_or(const char *name, int dflt) {
     const char *e = std::getenv(name);
-    return e ? std::atoi(e) : 0;
+    return e ? std::atoi(e) : dflt;
 }
+
+Tuning &tuning() {
+    static Tuning *t = [] {
+        Tuning *n = new Tuning;
+        const int bm = env_or("MLA_GEMM_BM", 0), bn = env_or("MLA_GEMM_BN", 0);
+        n->v[MLA_TUNE_GEMM_BM].store(bm > 0 ? bm : -1);
+        n->v[MLA_TUNE_GEMM_BN].store(bn > 0 ? bn : -1);
+        n->v[MLA_TUNE_GEMM_DEPTH].store(std::getenv("MLA_GEMM_D") ? std::max(0, env_or("MLA_GEMM_D", 0)) : -1);
+        const int m = env_or("MLA_LAYER_MHA_MIN", 0);
+        n->v[MLA_TUNE_MHA_MIN_ROWS].store(m >= 2 ? m : -1);
+        n->v[MLA_TUNE_MHA_PAIRS].store(std::getenv("MLA_LAYER_MHA_PAIRS") ? std::max(0, env_or("MLA_LAYER_MHA_PAIRS", 0))
+                                                                        : -1);
+        return n;
+    }();
+    return *t;
+}
+
+int tuned(int knob) { return tuning().v[knob].load(std::memory_order_relaxed); }
 
 int cu_count() {
     int ncu = 256, dev = 0, v = 0;
@@ -80,10 +107,10 @@ proj::GemmShape pick_shape(long long M, int N, int batch, int epi, bool a_f32) {
         t.bn = proj::kBN;
         t.bm = std::min(t.bm, 128);
     }
-    if (int v = env_int("MLA_GEMM_BM")) t.bm = v;
+    if (int v = tuned(MLA_TUNE_GEMM_BM); v > 0) t.bm = v;
     if (!a_f32)
-        if (int v = env_int("MLA_GEMM_BN")) t.bn = v;
-    if (const char *e = std::getenv("MLA_GEMM_D")) t.depth = std::atoi(e);
+        if (int v = tuned(MLA_TUNE_GEMM_BN); v > 0) t.bn = v;
+    if (int v = tuned(MLA_TUNE_GEMM_DEPTH); v >= 0) t.depth = v;
     return t;
 }
 
@@ -248,26 +275,18 @@ int post_attn(int T, const void *attn_out, int32_t attn_dtype, const mla_proj_we
 // Which chunk requests take the multi-head path in the layer (up-projected
 // keys and values, 192 + 128 dims per head: about 30% of the absorbed form's
 // flops per query-key pair, for one up-projection of the request's keys).
-// Measured on MI355X, the multi-head kernel saves about 14 ps per query-key
-// pair (all 16 heads) against the absorbed one on a full grid and the
-// up-projection costs about 7.6 ns per key, so it pays from about 550 pairs
-// per key; chunks of fewer than 2048 rows fill only part of the chip with its
-// 128-token blocks, and a sweep over the benchmark workloads put the measured
-// break-even between 896 (slower) and 967 (faster) pairs per key.
-// MLA_LAYER_MHA_MIN (>= 2) and MLA_LAYER_MHA_PAIRS (>= 0) override the two
-// numbers; with MLA_LAYER_MHA_MIN alone every request of that many rows
-// takes the path.
-constexpr int kMhaMinRows = 256;
-constexpr int kMhaPairsPerKey = 950;
-
+// By default none do: every row runs on the absorbed kernel.  The route is
+// opt-in (mla_layer_tune): a row minimum alone sends every chunk request of
+// that many rows; with a pairs-per-key bar too, only requests whose query-key
+// pairs per key, c (p + c / 2) / (p + c), reach it (the up-projection costs a
+// fixed time per key, the multi-head form saves a fixed time per pair).
 mla::ChunkRoute mha_route() {
-    const int m = env_int("MLA_LAYER_MHA_MIN"), k = env_int("MLA_LAYER_MHA_PAIRS");
-    mla::ChunkRoute r{kMhaMinRows, kMhaPairsPerKey};
+    const int m = tuned(MLA_TUNE_MHA_MIN_ROWS), k = tuned(MLA_TUNE_MHA_PAIRS);
+    mla::ChunkRoute r = mla::kAbsorbAll;
     if (m >= 2) {
         r.min_rows = m;
-        r.pair_keys = 0;
+        r.pair_keys = k >= 0 ? k : 0;
     }
-    if (std::getenv("MLA_LAYER_MHA_PAIRS")) r.pair_keys = std::max(0, k);
     return r;
 }
 
@@ -339,6 +358,14 @@ int mla_post_attn(int32_t num_rows, const void *attn_out, int32_t attn_dtype, co
     mla::set_error(MLA_OK, "");
     return post_attn(num_rows, attn_out, attn_dtype, w, out, out_dtype, workspace, workspace_bytes,
                      static_cast<hipStream_t>(stream));
+}
+
+int mla_layer_tune(int32_t knob, int32_t value) {
+    mla::set_error(MLA_OK, "");
+    if (knob < 0 || knob >= MLA_TUNE_COUNT) return mla::set_error(MLA_ERR_INVALID_ARG, "unknown tuning knob %d", knob);
+    if (value < -1) return mla::set_error(MLA_ERR_INVALID_ARG, "tuning value %d < -1", value);
+    tuning().v[knob].store(value);
+    return MLA_OK;
 }
 
 size_t mla_layer_workspace_bytes(const mla_batch *batch) {

@@ -185,13 +185,18 @@ __device__ __forceinline__ void key_rows(const KeyRowsJob &j, int wg) {
     // thread: key wg * 8 + tid / 32, 16-byte chunk tid % 32 of the 72 of a latent row
     const int key = wg * kKeyRowsPerWg + (threadIdx.x >> 5), lane = threadIdx.x & 31;
     if (key >= j.nkeys) return;
-    int pg = j.bt[key >> j.log2p];
-    pg = (unsigned)pg < (unsigned)j.npages ? pg : 0;
+    // A page id outside the pool: a prefix key is read from page 0 instead
+    // (wrong numbers, no fault); a new latent is not written anywhere, as in
+    // the other append paths.
+    const int pg_raw = j.bt[key >> j.log2p];
+    const bool pg_ok = (unsigned)pg_raw < (unsigned)j.npages;
+    const int pg = pg_ok ? pg_raw : 0;
     uint16_t *slot = j.cache + (((size_t)pg << j.log2p) + (key & ((1 << j.log2p) - 1))) * kDqk;
     const uint16_t *src = key < j.p ? slot : j.lat + (size_t)(key - j.p) * kDqk;
+    const bool write = key >= j.p && pg_ok;
     for (int c = lane; c < kDqk / 8; c += 32) {
         const u32x4 v = *reinterpret_cast<const u32x4 *>(src + 8 * c);
-        if (key >= j.p) *reinterpret_cast<u32x4 *>(slot + 8 * c) = v;  // append of a new latent
+        if (write) *reinterpret_cast<u32x4 *>(slot + 8 * c) = v;  // append of a new latent
         if (c >= kLatent / 8) {
             u32x4 h;
 #pragma unroll

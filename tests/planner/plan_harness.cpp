@@ -1,12 +1,30 @@
 // Host-only harness around the library's work planner (the translation unit
-// is included as is; the three launch functions are stubbed because nothing is
-// launched here).  Input on stdin, one batch per line:
+// is included as is; the launch functions are stubbed because nothing is
+// launched here, and the device queries answer for a 256-CU device).  Input on
+// stdin, one batch per line:
 //   ncu page_size R q_0 p_0 q_1 p_1 ...
 // Output, one line per batch:
 //   ok ks n_chunk_items n_dec_items unit_tiles dec_total grid merge_hsplit chunk_split dec_split bytes
 //      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us
 // or "err <status> <message>".
+// A line "ws <bytes> page_size R q_0 p_0 ..." instead calls the real
+// mixed_step_attn entry point with fake device pointers and a workspace of
+// <bytes> bytes and prints "rc <status> <needed bytes> <message>".
+#include <hip/hip_runtime.h>
+
+static hipError_t harness_get_device(int *d) {
+    *d = 0;
+    return hipSuccess;
+}
+static hipError_t harness_get_attribute(int *v, hipDeviceAttribute_t, int) {
+    *v = 256;
+    return hipSuccess;
+}
+#define hipGetDevice harness_get_device
+#define hipDeviceGetAttribute harness_get_attribute
 #include "../../paper_2607_02043_amd/csrc/mla_api.cpp"
+#undef hipGetDevice
+#undef hipDeviceGetAttribute
 
 #include <chrono>
 #include <iostream>
@@ -17,6 +35,10 @@ namespace mla {
 hipError_t launch_append(const AppendArgs &, hipStream_t) { return hipSuccess; }
 hipError_t launch_attention(const AttnArgs &, hipStream_t) { return hipSuccess; }
 hipError_t launch_combine(const AttnArgs &, hipStream_t) { return hipSuccess; }
+hipError_t read_flags(int *flags, bool) {
+    *flags = 0;
+    return hipSuccess;
+}
 }  // namespace mla
 
 int main() {
@@ -29,6 +51,36 @@ int main() {
     }
     std::string line;
     while (std::getline(std::cin, line)) {
+        if (line.rfind("ws ", 0) == 0) {
+            std::istringstream in(line.substr(3));
+            long long bytes = 0;
+            int P = 0, R = 0;
+            in >> bytes >> P >> R;
+            std::vector<int32_t> q(R), p(R);
+            long long maxk = 1;
+            for (int i = 0; i < R; ++i) {
+                in >> q[i] >> p[i];
+                maxk = std::max<long long>(maxk, (long long)q[i] + p[i]);
+            }
+            static const int32_t fake = 0;
+            mla_batch b{};
+            b.num_reqs = R;
+            b.page_size = P;
+            b.num_pages = 1 << 20;
+            b.max_pages_per_req = (int)((maxk + P - 1) / P);
+            b.q_lens = q.data();
+            b.prefix_lens = p.data();
+            b.cu_q_dev = &fake;
+            b.prefix_lens_dev = &fake;
+            b.block_table_dev = &fake;
+            alignas(16) static char fake_dev[16];
+            const size_t need = mixed_step_workspace_bytes(&b);
+            const int rc = mixed_step_attn(&b, reinterpret_cast<const uint16_t *>(fake_dev),
+                                           reinterpret_cast<const uint16_t *>(fake_dev), 0.07f, fake_dev, MLA_OUT_F32,
+                                           nullptr, bytes > 0 ? fake_dev : nullptr, (size_t)bytes, nullptr);
+            std::cout << "rc " << rc << " " << need << " " << mla_last_error() << "\n";
+            continue;
+        }
         std::istringstream in(line);
         int ncu = 0, P = 0, R = 0;
         if (!(in >> ncu >> P >> R)) continue;

@@ -136,3 +136,14 @@ def test_error_message_is_cleared_by_a_good_call():
     assert _err() != ""
     assert _attn(_HostBatch([], [])) == mla.MLA_OK
     assert _err() == ""
+
+
+def test_debug_settings_are_checked_on_the_host():
+    L = mla.lib()
+    assert L.mla_debug_set(7, 1) == mla.MLA_ERR_INVALID_ARG
+    assert "knob" in _err()
+    assert L.mla_debug_set(mla.MLA_DEBUG_CHECK, 2) == mla.MLA_ERR_INVALID_ARG
+    assert L.mla_debug_set(mla.MLA_DEBUG_SPIN_LIMIT, -5) == mla.MLA_ERR_INVALID_ARG
+    assert L.mla_debug_set(mla.MLA_DEBUG_SPIN_LIMIT, -1) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_CHECK, 0) == mla.MLA_OK
+    assert L.mla_device_flags(1, None, None) == mla.MLA_ERR_INVALID_ARG

@@ -16,14 +16,15 @@ boundary), and fp32 results keep a mean relative error <= 2^-10 against the
 oracle's rounded mode.  The whole layer keeps the attention output's bars
 (max-abs 1e-2 at unit scale, mean relative error 2e-3).
 Layers whose chunks take the multi-head path (up-projected fp16 keys and
-values) round at other points than the oracle's absorbed rounded mode; they are
-checked against the exact layer within 1.5 times the error of that rounded
-mode (the floor the ABI's bf16 queries, latents and attention output set).
-Every instantiated GEMM tile shape is exercised through the tuning variables
-MLA_GEMM_BM / MLA_GEMM_BN / MLA_GEMM_D.
+values) are checked against the oracle's multi-head rounded mode, which rounds
+at that path's own storage points, at the same bars (max-abs 1e-2 at unit
+scale, mean relative error 2e-3).  A second, looser guard compares them with
+the exact layer: within 1.5 times the absorbed rounded mode's own distance
+from it, a sanity bound only (the two forms round at different points, so
+neither error bounds the other).
+Every instantiated GEMM tile shape is exercised through the tuning knobs
+(mla_layer_tune).
 """
-import os
-
 import numpy as np
 import pytest
 
@@ -48,23 +49,30 @@ def weights():
 # tuning variables; None keeps the library's own choice.
 SHAPES = [None, (32, 64, 6), (64, 64, 4), (128, 64, 3), (32, 128, 4), (64, 128, 3), (128, 128, 2), (128, 128, 3),
           (32, 128, 0), (64, 128, 0), (128, 128, 0), (128, 256, 0), (256, 128, 0)]
-_VARS = ("MLA_GEMM_BM", "MLA_GEMM_BN", "MLA_GEMM_D")
+_KNOBS = (mla.TUNE_GEMM_BM, mla.TUNE_GEMM_BN, mla.TUNE_GEMM_DEPTH)
 
 
 @pytest.fixture
 def gemm_shape(request):
-    old = {k: os.environ.get(k) for k in _VARS}
-    for k in _VARS:
-        os.environ.pop(k, None)
-    if request.param is not None:
-        for k, v in zip(_VARS, request.param):
-            os.environ[k] = str(v)
-    yield request.param
-    for k, v in old.items():
-        if v is None:
-            os.environ.pop(k, None)
-        else:
-            os.environ[k] = v
+    settings = {k: -1 for k in _KNOBS} if request.param is None else dict(zip(_KNOBS, request.param))
+    with mla.tuned(settings):
+        yield request.param
+
+
+@pytest.fixture
+def mha_route():
+    """Sets the layer's multi-head route for one test: mha_route(min_rows, pairs=-1)."""
+    keys = (mla.TUNE_MHA_MIN_ROWS, mla.TUNE_MHA_PAIRS)
+    for k in keys:
+        mla.layer_tune(k, -1)
+
+    def set_route(min_rows, pairs=-1):
+        mla.layer_tune(mla.TUNE_MHA_MIN_ROWS, min_rows)
+        mla.layer_tune(mla.TUNE_MHA_PAIRS, pairs)
+
+    yield set_route
+    for k in keys:
+        mla.layer_tune(k, -1)
 
 
 def _ulp_bf16(x):
@@ -210,7 +218,20 @@ def test_post_attn_parity(attn_bf16, out_bf16, gemm_shape, weights):
     check_f32(got, ref, "out vs rounded oracle", mean_rel=2.0 ** -10 if not out_bf16 else 2.0 ** -8)
 
 
-def _layer_case(prefix, qlen, page, seed, weights, rows=None, out_bf16=False, exact=False):
+def _route_fn(route):
+    """The multi-head route (min_rows, pairs) as the oracle's predicate (None: every row absorbed)."""
+    if route is None:
+        return None
+    m, k = route
+    k = max(k, 0)
+    return lambda p, c: c >= m and c * (2 * p + c) >= 2 * k * (p + c)
+
+
+def _layer_case(prefix, qlen, page, seed, weights, rows=None, out_bf16=False, exact=False, route=None):
+    """One mla_attention_layer call against the oracle's rounded mode (the
+    multi-head rounded mode for the requests `route` sends there).  Returns
+    (got, ref, pool after (GPU), pool after (oracle), batch[, exact layer][,
+    the step's latents from mla_pre_attn on the GPU])."""
     import torch
     wb, wo, dw = weights
     wl = W.custom(prefix, qlen, page_size=page, seed=seed)
@@ -225,14 +246,42 @@ def _layer_case(prefix, qlen, page, seed, weights, rows=None, out_bf16=False, ex
     mla.mla_attention_layer(db, to_dev(hidden), dw, pool, SCALE, out, ws)
     torch.cuda.synchronize()
     ref, pool_ref, _, _ = PO.layer(b, hidden, wo, li.pool, SCALE, out_bf16=out_bf16, rows=rows)
+    if route is not None:
+        ref = PO.layer_multihead(b, hidden, wo, li.pool, SCALE, _route_fn(route), rows=rows)
     got = out.float().cpu().numpy().astype(np.float64)
     if rows is not None:
         got = got[np.asarray(rows)]
+    res = [got, ref, from_dev_u16(pool), pool_ref, b]
     if exact:
-        ex = PO.layer_exact(b.q_lens, b.prefix_lens, PO.bf16_value(hidden), wo, PO.logical_cache(b, li.pool), SCALE,
-                            rows=rows)
-        return got, ref, from_dev_u16(pool), pool_ref, b, ex
-    return got, ref, from_dev_u16(pool), pool_ref, b
+        res.append(PO.layer_exact(b.q_lens, b.prefix_lens, PO.bf16_value(hidden), wo, PO.logical_cache(b, li.pool),
+                                  SCALE, rows=rows))
+    if route is not None:
+        _, lat_gpu = _run_pre(b, hidden, dw)
+        res.append(lat_gpu)
+    return tuple(res)
+
+
+def _written(b, shape):
+    w = np.zeros(shape, dtype=bool)
+    for r in range(b.num_reqs):
+        for t in range(int(b.prefix_lens[r]), int(b.prefix_lens[r] + b.q_lens[r])):
+            w[b.block_table[r][t // b.page_size], t % b.page_size] = True
+    return w
+
+
+def _check_pool_bits(b, pool_gpu, pool_before, lat_gpu):
+    """The step writes exactly its own slots, each with the latent that
+    mla_pre_attn computes for that row (bit for bit); every other slot keeps
+    its bits."""
+    written = _written(b, pool_gpu.shape[:2])
+    assert np.array_equal(pool_gpu[~written], pool_before[~written]), "a slot outside the step changed"
+    row = 0
+    for r in range(b.num_reqs):
+        for i in range(int(b.q_lens[r])):
+            t = int(b.prefix_lens[r]) + i
+            slot = pool_gpu[b.block_table[r][t // b.page_size], t % b.page_size]
+            assert np.array_equal(slot, lat_gpu[row + i]), f"request {r} slot {t}: not the step's latent"
+        row += int(b.q_lens[r])
 
 
 LAYER_CASES = {
@@ -249,10 +298,7 @@ def test_layer_parity(case, weights):
     got, ref, pool_gpu, pool_ref, b = _layer_case(prefix, qlen, page, 41, weights)
     check_f32(got, ref, "layer out", max_abs=1e-2 * max(1.0, float(np.sqrt(np.mean(ref ** 2)))), mean_rel=2e-3)
     # slots the step did not write are untouched; written slots hold the step's latents to one bf16 step
-    written = np.zeros(pool_ref.shape[:2], dtype=bool)
-    for r in range(b.num_reqs):
-        for t in range(int(b.prefix_lens[r]), int(b.prefix_lens[r] + b.q_lens[r])):
-            written[b.block_table[r][t // b.page_size], t % b.page_size] = True
+    written = _written(b, pool_ref.shape[:2])
     assert np.array_equal(pool_gpu[~written], pool_ref[~written])
     gw, rw = PO.bf16_value(pool_gpu[written]), PO.bf16_value(pool_ref[written])
     assert (np.abs(gw - rw) <= 2 * _ulp_bf16(rw) + 1e-3).all()
@@ -266,23 +312,34 @@ def test_layer_bf16_out(weights):
     assert (np.abs(got - ref) <= lim).all()
 
 
-def test_layer_full_size_sampled_rows(weights):
+@pytest.mark.parametrize("route", ["default", "multi_head"])
+def test_layer_full_size_sampled_rows(route, weights, mha_route):
     """128 decode rows with lognormal contexts plus a 2048-token chunk over a
-    6144-token prefix (T = 2176; the chunk takes the multi-head path by default): sampled
-    rows against the exact layer."""
+    6144-token prefix (T = 2176), the chunk on the absorbed kernel (default)
+    or the multi-head path: sampled rows against the rounded oracle."""
+    r = None
+    if route == "multi_head":
+        r = (256, 0)
+        mha_route(256)
     wl = W.config(3)
     b = wl.batch
     rows = sample_rows(b, n_decode=24, seed=3)
-    log(f"[gpu] attention layer at full size: T={b.num_rows}, {len(rows)} sampled rows")
-    got, ref, *_, ex = _layer_case(list(b.prefix_lens), list(b.q_lens), b.page_size, wl.seed, weights, rows=rows,
-                                   exact=True)
-    check_vs_exact(got, ex, ref, "layer out (sampled)")
+    log(f"[gpu] attention layer at full size ({route}): T={b.num_rows}, {len(rows)} sampled rows")
+    res = _layer_case(list(b.prefix_lens), list(b.q_lens), b.page_size, wl.seed, weights, rows=rows, exact=True,
+                      route=r)
+    got, ref, ex = res[0], res[1], res[5]
+    if r is None:
+        check_f32(got, ref, "layer out (sampled)", max_abs=1e-2 * max(1.0, float(np.sqrt(np.mean(ref ** 2)))),
+                  mean_rel=2e-3)
+    else:
+        _check_mha(got, ref, ex, "layer out (sampled)")
 
 
-# Chunk requests of many rows take the multi-head path in the layer (keys and
-# values up-projected per head, fp16); MLA_LAYER_MHA_MIN = 2 sends every chunk
-# request there.  The oracle is the same layer: the two forms are equal up to
-# rounding.
+# Chunk requests of many rows can take the multi-head path in the layer (keys
+# and values up-projected per head, fp16; opt-in through the layer's tuning
+# knobs).  The oracle is the same layer in its multi-head rounded mode (fp16
+# keys and values, bf16 query parts and per-head output at the GPU path's
+# storage points), at the attention bars; the exact layer is a second guard.
 MHA_CASES = {
     "chunk_only_prefix0": ([0], [150], 64),
     "decode_chunk_decode_page16": ([300, 40, 1000], [1, 97, 1], 16),
@@ -292,59 +349,78 @@ MHA_CASES = {
 }
 
 
+def _check_mha(got, ref, ex, what):
+    check_f32(got, ref, what + " vs multi-head rounded oracle",
+              max_abs=1e-2 * max(1.0, float(np.sqrt(np.mean(ref ** 2)))), mean_rel=2e-3)
+    check_vs_exact(got, ex, ref, what)
+
+
 @pytest.mark.parametrize("case", sorted(MHA_CASES))
-def test_layer_multihead_path_parity(case, weights, monkeypatch):
-    monkeypatch.setenv("MLA_LAYER_MHA_MIN", "2")
+def test_layer_multihead_path_parity(case, weights, mha_route):
+    mha_route(2)
     prefix, qlen, page = MHA_CASES[case]
     log(f"[gpu] attention layer, multi-head chunks {case}: prefix={prefix} q_lens={qlen} page={page}")
-    got, ref, pool_gpu, pool_ref, b, ex = _layer_case(prefix, qlen, page, 47, weights, exact=True)
-    check_vs_exact(got, ex, ref, "layer out")
-    written = np.zeros(pool_ref.shape[:2], dtype=bool)
-    for r in range(b.num_reqs):
-        for t in range(int(b.prefix_lens[r]), int(b.prefix_lens[r] + b.q_lens[r])):
-            written[b.block_table[r][t // b.page_size], t % b.page_size] = True
-    assert np.array_equal(pool_gpu[~written], pool_ref[~written])
+    wl = W.custom(prefix, qlen, page_size=page, seed=47)
+    got, ref, pool_gpu, pool_ref, b, ex, lat = _layer_case(prefix, qlen, page, 47, weights, exact=True, route=(2, 0))
+    _check_mha(got, ref, ex, "layer out")
+    _check_pool_bits(b, pool_gpu, wl.layer(0).pool, lat)
 
 
-def test_layer_multihead_default_route(weights):
-    """By default a chunk request takes the multi-head path when it has at
-    least 256 rows and enough query-key pairs per key to repay the
-    up-projection: a 1536-row chunk over a 4096-token prefix does, the decode
-    rows around it do not.  Sampled rows against the exact layer."""
+def test_layer_multihead_pairs_route(weights, mha_route):
+    """With a pairs-per-key bar, a 1536-row chunk over a 4096-token prefix
+    takes the multi-head path and the decode rows around it do not.  Sampled
+    rows."""
+    mha_route(256, 950)
     prefix, qlen = [50, 4096, 3000], [1, 1536, 1]
     wl = W.custom(prefix, qlen, page_size=64, seed=49)
     rows = sample_rows(wl.batch, n_decode=2, seed=49)
-    got, ref, *_, ex = _layer_case(prefix, qlen, 64, 49, weights, rows=rows, exact=True)
-    check_vs_exact(got, ex, ref, "layer out (sampled)")
+    got, ref, pool_gpu, pool_ref, b, ex, lat = _layer_case(prefix, qlen, 64, 49, weights, rows=rows, exact=True,
+                                                           route=(256, 950))
+    _check_mha(got, ref, ex, "layer out (sampled)")
+    _check_pool_bits(b, pool_gpu, wl.layer(0).pool, lat)
 
 
-def test_layer_mixed_routing(weights, monkeypatch):
+def test_layer_default_route_is_absorbed(weights):
+    """By default every row runs on the absorbed kernel: the same long chunk
+    matches the absorbed rounded oracle at the attention bars."""
+    prefix, qlen = [50, 4096, 3000], [1, 1536, 1]
+    wl = W.custom(prefix, qlen, page_size=64, seed=49)
+    rows = sample_rows(wl.batch, n_decode=2, seed=49)
+    got, ref, *_ = _layer_case(prefix, qlen, 64, 49, weights, rows=rows)
+    check_f32(got, ref, "layer out (sampled)", max_abs=1e-2 * max(1.0, float(np.sqrt(np.mean(ref ** 2)))),
+              mean_rel=2e-3)
+
+
+def test_layer_mixed_routing(weights, mha_route):
     """One chunk request on each path in the same step: with 100 pairs per key
     required, the 120-row chunk over 2000 keys goes multi-head and the 150-row
     chunk at prefix 0 stays on the absorbed kernel."""
-    monkeypatch.setenv("MLA_LAYER_MHA_MIN", "2")
-    monkeypatch.setenv("MLA_LAYER_MHA_PAIRS", "100")
-    got, ref, pool_gpu, pool_ref, b, ex = _layer_case([2000, 7, 0], [120, 1, 150], 64, 51, weights, exact=True)
-    check_vs_exact(got, ex, ref, "layer out")
-    written = np.zeros(pool_ref.shape[:2], dtype=bool)
-    for r in range(b.num_reqs):
-        for t in range(int(b.prefix_lens[r]), int(b.prefix_lens[r] + b.q_lens[r])):
-            written[b.block_table[r][t // b.page_size], t % b.page_size] = True
-    assert np.array_equal(pool_gpu[~written], pool_ref[~written])
+    mha_route(2, 100)
+    wl = W.custom([2000, 7, 0], [120, 1, 150], page_size=64, seed=51)
+    got, ref, pool_gpu, pool_ref, b, ex, lat = _layer_case([2000, 7, 0], [120, 1, 150], 64, 51, weights, exact=True,
+                                                           route=(2, 100))
+    _check_mha(got, ref, ex, "layer out")
+    _check_pool_bits(b, pool_gpu, wl.layer(0).pool, lat)
 
 
 @pytest.mark.parametrize("route", ["default", "multi_head"])
-def test_layer_four_chunks_full_size_sampled_rows(route, weights, monkeypatch):
+def test_layer_four_chunks_full_size_sampled_rows(route, weights, mha_route):
     """One layer of the 27-layer workload: 64 decode rows and four 1024-token
-    chunks at prefixes 0 / 1024 / 3072 / 8192 (by default the one at 8192
-    goes multi-head, the others have too few pairs per key; with the row
-    minimum alone, all four)."""
+    chunks at prefixes 0 / 1024 / 3072 / 8192 (by default every row on the
+    absorbed kernel; with a 256-row minimum, all four chunks multi-head)."""
+    r = None
     if route == "multi_head":
-        monkeypatch.setenv("MLA_LAYER_MHA_MIN", "256")
+        r = (256, 0)
+        mha_route(256)
     wl = W.config(5)
     b = wl.batch
     rows = sample_rows(b, n_decode=16, seed=5)
-    log(f"[gpu] attention layer, four chunks at full size: T={b.num_rows}, {len(rows)} sampled rows")
-    got, ref, *_, ex = _layer_case(list(b.prefix_lens), list(b.q_lens), b.page_size, wl.seed, weights, rows=rows,
-                                   exact=True)
-    check_vs_exact(got, ex, ref, "layer out (sampled)")
+    log(f"[gpu] attention layer, four chunks at full size ({route}): T={b.num_rows}, {len(rows)} sampled rows")
+    res = _layer_case(list(b.prefix_lens), list(b.q_lens), b.page_size, wl.seed, weights, rows=rows, exact=True,
+                      route=r)
+    got, ref, ex = res[0], res[1], res[5]
+    if r is None:
+        check_f32(got, ref, "layer out (sampled)", max_abs=1e-2 * max(1.0, float(np.sqrt(np.mean(ref ** 2)))),
+                  mean_rel=2e-3)
+    else:
+        _check_mha(got, ref, ex, "layer out (sampled)")

@@ -185,3 +185,23 @@ def test_plan_leaves_out_routed_chunks(harness, route):
         check_plan(b, d, route)
     # the benchmark's 2048-row chunk over 6144 keys leaves on every route here
     assert res[-2]["n_chunk_items"] == 0 and res[-2]["n_dec_items"] > 0
+
+
+def test_workspace_too_small_is_rejected(harness):
+    """The real mixed_step_attn entry point (launches stubbed) rejects a
+    workspace below what the batch needs with MLA_ERR_WORKSPACE before
+    launching anything, and accepts the exact size."""
+    q = [1] * 40 + [700]
+    p = [int(x) for x in np.random.default_rng(2).integers(100, 9000, 40)] + [3000]
+    line = " ".join(f"{a} {b}" for a, b in zip(q, p))
+    out = subprocess.run([harness], input=f"ws 0 64 {len(q)} {line}\n", capture_output=True, text=True,
+                         check=True).stdout.split()
+    assert out[0] == "rc"
+    need = int(out[2])
+    assert need > 256
+    assert int(out[1]) == -3  # MLA_ERR_WORKSPACE
+    text = "".join(f"ws {n} 64 {len(q)} {line}\n" for n in (need - 16, need))
+    lines = subprocess.run([harness], input=text, capture_output=True, text=True, check=True).stdout.splitlines()
+    small, exact = lines[0].split(), lines[1].split()
+    assert int(small[1]) == -3 and "needs" in lines[0]
+    assert int(exact[1]) == 0

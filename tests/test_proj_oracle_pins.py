@@ -150,3 +150,34 @@ def test_rounded_mode_stays_within_bf16_rounding(weights):
     pos = PO.positions(b.q_lens, b.prefix_lens)
     _, lat_exact = PO.pre_attn(pos, PO.bf16_value(hidden), weights, rounded=False)
     assert np.array_equal(lat_bits, PO.round_bf16(lat_exact))
+
+
+def test_multihead_rounded_mode_pins(weights):
+    """The multi-head rounded mode: with no request routed it is the absorbed
+    rounded mode exactly; with every chunk routed, it stays within fp16 / bf16
+    rounding of the exact layer computed the plain multi-head way
+    (layer_unabsorbed: explicit per-head keys and values, one head at a time)
+    and differs from the absorbed rounded mode only by rounding.  fp16
+    rounding matches numpy's IEEE half conversion on hand-worked ties."""
+    assert PO.round_f16(1.0 + 2.0 ** -11) == 1.0            # tie to even (down)
+    assert PO.round_f16(1.0 + 3 * 2.0 ** -11) == 1.0 + 2.0 ** -9  # tie to even (up)
+    assert PO.round_f16(2.0 ** -24) == 2.0 ** -24           # smallest subnormal
+    assert PO.round_f16(65504.0) == 65504.0
+    wl = W.custom([37, 0, 5, 20], [1, 9, 3, 6], page_size=16, seed=9)
+    b = wl.batch
+    li = wl.layer(0)
+    hidden = W.random_hidden(b.num_rows, seed=9)
+    absorbed, *_ = PO.layer(b, hidden, weights, li.pool, SCALE)
+    none = PO.layer_multihead(b, hidden, weights, li.pool, SCALE, lambda p, c: False)
+    assert np.array_equal(none, absorbed)
+    mh = PO.layer_multihead(b, hidden, weights, li.pool, SCALE, lambda p, c: c >= 2)
+    ref = PO.layer_unabsorbed(b.q_lens, b.prefix_lens, PO.bf16_value(hidden), weights, PO.logical_cache(b, li.pool),
+                              SCALE)
+    rel = np.sqrt(np.mean((mh - ref) ** 2) / np.mean(ref ** 2))
+    assert 0 < rel < 2.0 ** -6
+    # the decode rows (c = 1) are the absorbed ones; the chunk rows differ by rounding only
+    dec = np.concatenate([np.arange(int(b.cu_q[r]), int(b.cu_q[r + 1])) for r in range(b.num_reqs)
+                          if b.q_lens[r] == 1])
+    assert np.array_equal(mh[dec], absorbed[dec])
+    d = np.abs(mh - absorbed)
+    assert 0 < d.max() < 2.0 ** -5 * np.abs(ref).max()
