@@ -181,6 +181,24 @@ int mixed_step(const mla_batch *batch, const uint16_t *q, const uint16_t *new_la
                float softmax_scale, void *out, int32_t out_dtype, float *lse, void *workspace,
                size_t workspace_bytes, void *stream);
 
+/* mixed_step without a workspace argument, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation.  Same arguments, contract and results (bit for bit)
+ * as mixed_step; it allocates nothing and calls no allocating routine.  Its
+ * workspace is a library-owned device buffer of MLA_NOALLOC_SCRATCH_BYTES per
+ * device, set up on the first call on each device (make that call outside
+ * graph capture); it lives until the process ends.
+ *   - Every call on one device shares that buffer: calls that overlap in time
+ *     on one device (several streams or threads) race and give undefined
+ *     results.  Serialise them, or use mixed_step with distinct workspaces.
+ *   - A batch whose plan needs more scratch than MLA_NOALLOC_SCRATCH_BYTES
+ *     (mixed_step_workspace_bytes tells) is rejected with MLA_ERR_WORKSPACE
+ *     before anything is enqueued.
+ * Errors: as mixed_step. */
+#define MLA_NOALLOC_SCRATCH_BYTES (128u << 20)
+int mixed_step_noalloc(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
+                       float softmax_scale, void *out, int32_t out_dtype, float *lse, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,8 @@ MLA_OUT_BF16 = 1
 NUM_HEADS, D_QK, D_V = 16, 576, 512
 
 EXPORTED = ("mla_abi_version", "mla_last_error", "mla_device_flags", "mla_debug_set", "mixed_step_workspace_bytes",
-            "append_latent_kv", "mixed_step_attn", "mixed_step")
+            "append_latent_kv", "mixed_step_attn", "mixed_step", "mixed_step_noalloc")
+NOALLOC_SCRATCH_BYTES = 128 << 20
 MLA_FLAG_BAD_PAGE = 1
 MLA_FLAG_WAIT_EXPIRED = 2
 MLA_DEBUG_CHECK = 0
@@ -97,6 +98,10 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_float, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_size_t, ctypes.c_void_p]
         L.mixed_step.restype = ctypes.c_int
+        L.mixed_step_noalloc.argtypes = [ctypes.POINTER(mla_batch), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_float, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                         ctypes.c_void_p]
+        L.mixed_step_noalloc.restype = ctypes.c_int
         vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
         L.mla_device_flags.argtypes = [i32, ctypes.POINTER(ctypes.c_int32), vp]
         L.mla_device_flags.restype = ctypes.c_int
@@ -227,6 +232,14 @@ def mixed_step(batch: DeviceBatch, q, new_latents, kv_cache, softmax_scale: floa
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().mixed_step(ctypes.byref(batch.c), _ptr(q), _ptr(new_latents), _ptr(kv_cache), float(softmax_scale),
                             _ptr(out), mode, _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def mixed_step_noalloc(batch: DeviceBatch, q, new_latents, kv_cache, softmax_scale: float, out, lse=None,
+                       stream=None) -> None:
+    """mixed_step on the library's own per-device scratch (no workspace argument)."""
+    mode = _out_mode(out)
+    _check(lib().mixed_step_noalloc(ctypes.byref(batch.c), _ptr(q), _ptr(new_latents), _ptr(kv_cache),
+                                    float(softmax_scale), _ptr(out), mode, _ptr(lse), _stream(stream)))
 
 
 def workspace_for(batch: DeviceBatch, device="cuda"):

@@ -720,6 +720,24 @@ int mixed_step_attn(const mla_batch *batch, const uint16_t *q, const uint16_t *k
                   workspace_bytes, stream);
 }
 
+static_assert(MLA_NOALLOC_SCRATCH_BYTES == mla::kNoAllocScratchBytes, "scratch size of the header and the library");
+
+int mixed_step_noalloc(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
+                       float softmax_scale, void *out, int32_t out_dtype, float *lse, void *stream) {
+    g_err[0] = '\0';
+    if (batch && batch->num_reqs > 0 && !new_latents) return fail(MLA_ERR_INVALID_ARG, "new_latents is NULL");
+    void *ws = nullptr;
+    const hipError_t e = mla::noalloc_scratch(&ws);
+    if (e != hipSuccess) return hip_fail(e, "no-allocation scratch set-up");
+    const int st = attend(batch, q, new_latents, kv_cache, softmax_scale, out, out_dtype, lse, ws,
+                          mla::kNoAllocScratchBytes, stream);
+    if (st == MLA_ERR_WORKSPACE)
+        return fail(MLA_ERR_WORKSPACE, "mixed_step_noalloc: this batch needs %zu bytes of scratch, more than the %zu "
+                    "bytes the no-allocation entry point holds; use mixed_step with a workspace",
+                    mixed_step_workspace_bytes(batch), mla::kNoAllocScratchBytes);
+    return st;
+}
+
 int mixed_step(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latents, uint16_t *kv_cache,
                float softmax_scale, void *out, int32_t out_dtype, float *lse, void *workspace,
                size_t workspace_bytes, void *stream) {

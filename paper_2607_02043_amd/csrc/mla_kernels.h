@@ -21,6 +21,8 @@ constexpr int kMaxDecSegments = 64;                         // requests one deco
 constexpr int kFlagBadPage = 1;       // a block-table entry outside [0, num_pages) was met (MLA_FLAG_BAD_PAGE)
 constexpr int kFlagWaitExpired = 2;   // a bounded wait inside a kernel gave up (MLA_FLAG_WAIT_EXPIRED)
 constexpr int kSpinLimit = 1 << 16;   // sleeps of a bounded wait before it gives up
+constexpr size_t kNoAllocScratchBytes = size_t(128) << 20;  // scratch of mixed_step_noalloc, per device
+constexpr int kMaxDevices = 64;
 
 struct AttnArgs {
     const uint16_t *q;
@@ -76,6 +78,9 @@ struct AppendArgs {
 hipError_t launch_append(const AppendArgs &a, hipStream_t s);
 // Reads the device's sticky kernel error flags (kFlag*), and clears them if asked.
 hipError_t read_flags(int *flags, bool clear);
+// Device address of the current device's no-allocation scratch
+// (kNoAllocScratchBytes bytes, counters zero on first use); set up once per device.
+hipError_t noalloc_scratch(void **ptr);
 hipError_t launch_attention(const AttnArgs &a, hipStream_t s);
 hipError_t launch_combine(const AttnArgs &a, hipStream_t s);
 

@@ -23,6 +23,16 @@
 #include <limits.h>
 #include <math.h>
 
+#include <mutex>
+
+// Scratch of the no-allocation entry point (mixed_step_noalloc): the
+// attention workspace (work-queue counters, then split partials) for callers
+// that cannot allocate.  Each device holds its own copy until the process
+// ends; host code reaches it only through the address that
+// hipGetSymbolAddress returns on that device (noalloc_scratch below).
+static __device__ __align__(256) unsigned char scratch[mla::kNoAllocScratchBytes];
+
+
 namespace mla {
 namespace {
 
@@ -1483,6 +1493,29 @@ extern "C" int mla_trace_read(void *dst, size_t bytes) {
     return (int)hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_trace), bytes, 0, hipMemcpyDeviceToHost);
 }
 #endif
+
+hipError_t noalloc_scratch(void **ptr) {
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (addr[dev] == nullptr) {
+        // once per device, with that device current: its copy's address, and
+        // the work-queue counters cleared (every completed call leaves them zero)
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        static const unsigned char zeros[256] = {};
+        e = hipMemcpy(p, zeros, sizeof zeros, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 hipError_t read_flags(int *flags, bool clear) {
     hipError_t e = hipMemcpyFromSymbol(flags, HIP_SYMBOL(g_flags), sizeof(int), 0, hipMemcpyDeviceToHost);

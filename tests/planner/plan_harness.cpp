@@ -9,7 +9,8 @@
 // or "err <status> <message>".
 // A line "ws <bytes> page_size R q_0 p_0 ..." instead calls the real
 // mixed_step_attn entry point with fake device pointers and a workspace of
-// <bytes> bytes and prints "rc <status> <needed bytes> <message>".
+// <bytes> bytes and prints "rc <status> <needed bytes> <message>"; "na 0 ..."
+// calls mixed_step_noalloc the same way (its scratch stubbed by a fake address).
 #include <hip/hip_runtime.h>
 
 static hipError_t harness_get_device(int *d) {
@@ -39,6 +40,11 @@ hipError_t read_flags(int *flags, bool) {
     *flags = 0;
     return hipSuccess;
 }
+hipError_t noalloc_scratch(void **ptr) {
+    alignas(256) static char fake[256];
+    *ptr = fake;
+    return hipSuccess;
+}
 }  // namespace mla
 
 int main() {
@@ -51,7 +57,8 @@ int main() {
     }
     std::string line;
     while (std::getline(std::cin, line)) {
-        if (line.rfind("ws ", 0) == 0) {
+        const bool noalloc = line.rfind("na ", 0) == 0;
+        if (line.rfind("ws ", 0) == 0 || noalloc) {
             std::istringstream in(line.substr(3));
             long long bytes = 0;
             int P = 0, R = 0;
@@ -75,9 +82,11 @@ int main() {
             b.block_table_dev = &fake;
             alignas(16) static char fake_dev[16];
             const size_t need = mixed_step_workspace_bytes(&b);
-            const int rc = mixed_step_attn(&b, reinterpret_cast<const uint16_t *>(fake_dev),
-                                           reinterpret_cast<const uint16_t *>(fake_dev), 0.07f, fake_dev, MLA_OUT_F32,
-                                           nullptr, bytes > 0 ? fake_dev : nullptr, (size_t)bytes, nullptr);
+            const uint16_t *fq = reinterpret_cast<const uint16_t *>(fake_dev);
+            const int rc = noalloc ? mixed_step_noalloc(&b, fq, fq, reinterpret_cast<uint16_t *>(fake_dev), 0.07f,
+                                                        fake_dev, MLA_OUT_F32, nullptr, nullptr)
+                                   : mixed_step_attn(&b, fq, fq, 0.07f, fake_dev, MLA_OUT_F32, nullptr,
+                                                     bytes > 0 ? fake_dev : nullptr, (size_t)bytes, nullptr);
             std::cout << "rc " << rc << " " << need << " " << mla_last_error() << "\n";
             continue;
         }

@@ -205,3 +205,15 @@ def test_workspace_too_small_is_rejected(harness):
     small, exact = lines[0].split(), lines[1].split()
     assert int(small[1]) == -3 and "needs" in lines[0]
     assert int(exact[1]) == 0
+
+
+def test_noalloc_entry_rejects_batches_beyond_its_scratch(harness):
+    """mixed_step_noalloc plans like mixed_step; a batch whose workspace
+    exceeds the library's fixed scratch (128 MiB) is rejected with
+    MLA_ERR_WORKSPACE and a message naming the limit, before any launch."""
+    big = "na 0 64 1 8192 57344\n"
+    small = "na 0 64 2 1 500 64 0\n"
+    lines = subprocess.run([harness], input=big + small, capture_output=True, text=True, check=True).stdout.splitlines()
+    b, s = lines[0].split(), lines[1].split()
+    assert int(b[2]) > 128 << 20 and int(b[1]) == -3 and "no-allocation" in lines[0]
+    assert int(s[2]) <= 128 << 20 and int(s[1]) == 0
