@@ -119,9 +119,19 @@ int mla_device_flags(int32_t clear, int32_t *flags, void *stream);
  *                         comes from the environment variable MLASTEP_CHECK;
  *   MLA_DEBUG_SPIN_LIMIT  sleeps a bounded wait inside a kernel takes before
  *                         it gives up (-1: the default, 65536); for tests of
- *                         the flag only: a small limit gives wrong results.
+ *                         the flag only: a small limit gives wrong results;
+ *   MLA_DEBUG_CHUNK_KEYS  force the work plan's chunk key split (each block of
+ *                         8 query tokens is cut into ceil((p + c) / value) key
+ *                         ranges; a multiple of 64, capped by what one work
+ *                         item may hold); 0 or -1: the planner's choice.  For
+ *                         tuning and tests: results stay within rounding.
  * Errors: MLA_ERR_INVALID_ARG (unknown knob, bad value). */
-typedef enum { MLA_DEBUG_CHECK = 0, MLA_DEBUG_SPIN_LIMIT = 1, MLA_DEBUG_COUNT = 2 } mla_debug_knob;
+typedef enum {
+    MLA_DEBUG_CHECK = 0,
+    MLA_DEBUG_SPIN_LIMIT = 1,
+    MLA_DEBUG_CHUNK_KEYS = 2,
+    MLA_DEBUG_COUNT = 3
+} mla_debug_knob;
 int mla_debug_set(int32_t knob, int32_t value);
 
 /* Message of the last non-OK return on this thread ("" if none). */

@@ -67,6 +67,7 @@ std::atomic<int> &debug_value(int knob) {
         const char *e = std::getenv("MLASTEP_CHECK");
         v[MLA_DEBUG_CHECK].store(e && std::atoi(e) != 0 ? 1 : 0);
         v[MLA_DEBUG_SPIN_LIMIT].store(mla::kSpinLimit);
+        v[MLA_DEBUG_CHUNK_KEYS].store(0);
     });
     return v[knob];
 }
@@ -124,7 +125,7 @@ int check_batch(const mla_batch *b, Shape *sh) {
 struct Plan {
     int ks_chunk = 0, n_chunk_items = 0;
     int n_dec_units = 0, dec_unit_tiles = 0, dec_total_tiles = 0, grid = 0, merge_hsplit = 1;
-    bool chunk_split = false, dec_split = false;
+    bool chunk_split = false, dec_split = false, chunk_rev = false;
     size_t off_chunk_o = 0, off_chunk_ml = 0, off_dec_o = 0, off_dec_ml = 0, bytes = 0;
 };
 
@@ -136,7 +137,7 @@ constexpr double kChunkItemUs = 14.0;  // chunk item: lookup, queries, ring fill
 constexpr double kEmptyItemUs = 1.5;   // a chunk item past its block's causal limit
 constexpr double kDecTileUs = 3.5;     // one decode tile of a unit (the two units of an item run side by side)
 constexpr double kDecUnitUs = 5.5;     // decode item start-up
-constexpr double kMergeGBs = 2000.0;   // partial rows written and merged, whole chip
+constexpr double kMergeGBs = 4000.0;   // partial rows written and merged, whole chip
 constexpr int kCounterBytes = 256;     // work-queue counters at the start of the workspace
 
 struct DecReq {
@@ -145,10 +146,14 @@ struct DecReq {
 
 // Does a decode unit of S tiles respect the kernel's limits (segments and
 // page-window entries per unit)?
-bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long S, int page_size) {
-    // a unit of S tiles touches at most S requests and, per request, at most
-    // its keys / page_size + 2 pages
-    if (S <= mla::kMaxDecSegments && S * mla::kKeysPerTile / page_size + 2 * S <= mla::kPageWindow) return true;
+bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long S, int page_size,
+                    long long min_tiles) {
+    // a unit of S tiles touches at most S / min_tiles + 2 requests (min_tiles:
+    // the shortest request's tiles) and, per request, at most its keys /
+    // page_size + 2 pages
+    const long long segs = std::min(S, S / std::max(1LL, min_tiles) + 2);
+    if (segs <= mla::kMaxDecSegments && S * mla::kKeysPerTile / page_size + 2 * segs <= mla::kPageWindow) return true;
+    const int lg = __builtin_ctz((unsigned)page_size);  // page_size is a power of two
     size_t k = 0;
     for (long long R0 = 0; R0 < total; R0 += S) {
         const long long R1 = std::min(R0 + S, total);
@@ -159,7 +164,7 @@ bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long 
             const long long t1 = std::min(R1 - reqs[j].first_tile, reqs[j].tiles);
             const long long k0 = t0 * mla::kKeysPerTile;
             const long long klast = std::min(t1 * mla::kKeysPerTile, reqs[j].p + 1) - 1;
-            pages += klast / page_size - k0 / page_size + 1;
+            pages += (klast >> lg) - (k0 >> lg) + 1;
             ++segs;
         }
         if (segs > mla::kMaxDecSegments || pages > mla::kPageWindow) return false;
@@ -233,13 +238,18 @@ double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
 }
 
 // Work layout of one call.
-//  * chunk requests -> items of (6 tokens) x (ks_chunk keys), largest blocks
-//    first; ks_chunk is picked by simulating the work queue for a few
-//    candidate splits, counting the cost of the partials a split leaves.
+//  * chunk requests -> items of (8 tokens) x (a range of keys): every block
+//    of 8 query tokens is cut into nks = ceil((p + c) / ks_chunk) equal key
+//    ranges (multiples of 64 keys), longest rows first; ks_chunk is picked
+//    from a closed-form estimate of the finishing time (work spread over the
+//    CUs plus half the largest item) plus the merge of the partials a split
+//    leaves.  Chunk requests are numbered from the last to the first when the
+//    last one has the larger items, so that large items start first.
 //  * decode requests -> one list of 32-key tiles cut into units of
-//    dec_unit_tiles; with chunk work present the units are small so that
-//    they fill the tail of the queue.
-// The device recomputes the same mapping from the device copies of the lengths.
+//    dec_unit_tiles; the units fill the tail after the chunk items.
+// The device recomputes the same mapping from the device copies of the
+// lengths.  Cost: a closed form per request and candidate key split, then a
+// queue simulation of the best one or two.
 int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkRoute route, Plan *pl) {
     const long long P = b->page_size;
     long long cap = ((long long)(mla::kPageWindow - 1) * P) / 64 * 64;  // keys per chunk item
@@ -247,7 +257,8 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     const int BM = mla::kChunkBlockTokens, KT = mla::kKeysPerTile;
 
     std::vector<DecReq> dec;
-    std::vector<std::pair<long long, long long>> chunks;  // (p, c) of each chunk request, queue order
+    std::vector<std::pair<long long, long long>> chunks;  // (p, c) of each chunk request, request order
+    dec.reserve(sh.R);
     long long dec_total = 0;
     for (int r = 0; r < sh.R; ++r) {
         const long long c = b->q_lens[r], p = b->prefix_lens[r];
@@ -260,10 +271,67 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         }
     }
     if (dec_total > (1LL << 30)) return fail(MLA_ERR_INVALID_ARG, "too many decode keys in the step");
+    long long min_tiles = 1LL << 40;
+    for (const DecReq &d : dec) min_tiles = std::min(min_tiles, d.tiles);
     const int G = std::max(1, ncu);
     const double row_bytes = (double)mla::kPartialFloats * 4.0;
 
-    // Candidate decode unit sizes (tiles); each must respect the kernel's
+    // Chunk work for a key split ks: total cost, largest item, items, and
+    // the partial rows (written, read back, the merged row written).  Per
+    // request in closed form: the blocks' causal limits p + 8 (rb + 1) form
+    // an arithmetic sequence (the last block ends at p + c).
+    struct ChunkEst {
+        double total = 0.0, max_item = 0.0, merge_us = 0.0;
+        long long items = 0;
+    };
+    auto chunk_est = [&](long long ks) {
+        ChunkEst e;
+        double split_rows = 0.0;
+        for (const auto &pc : chunks) {
+            const long long p = pc.first, c = pc.second;
+            const long long nrb = ceil_div_ll(c, BM), nks = ceil_div_ll(p + c, ks);
+            // sum over blocks of their tiles: limits p + 8, p + 16, .., p + c
+            const double keys = (double)nrb * (double)p + 4.0 * (double)(nrb - 1) * (double)nrb + (double)c;
+            const double tiles = keys / KT + 0.5 * (double)nrb * (double)nks;  // + rounding of each range
+            e.total += tiles * kChunkTileUs + (double)(nrb * nks) * kChunkItemUs;
+            const long long kp = ceil_div_ll(ceil_div_ll(p + c, nks), 64) * 64;
+            e.max_item = std::max(e.max_item, kChunkItemUs + kChunkTileUs * (double)ceil_div_ll(kp, KT));
+            if (nks > 1) {
+                // rows of the blocks whose keys span more than one range
+                const double first_split = std::max(0.0, (double)(ks - p) / BM);  // blocks within ks keys
+                split_rows += (double)(nks + 1) * std::max(0.0, (double)c - first_split * BM);
+            }
+            e.items += nrb * nks;
+        }
+        e.merge_us = split_rows * row_bytes / (kMergeGBs * 1e3);
+        return e;
+    };
+    // Chunk items of key split ks in device queue order (requests forward or
+    // from the last, blocks longest first, nks ranges per block; an empty
+    // range still takes a queue slot), as costs.
+    auto chunk_items = [&](long long ks, bool rev, std::vector<double> &items) {
+        items.clear();
+        for (size_t i = 0; i < chunks.size(); ++i) {
+            const auto &pc = chunks[rev ? chunks.size() - 1 - i : i];
+            const long long p = pc.first, c = pc.second;
+            const long long nrb = ceil_div_ll(c, BM), nks = ceil_div_ll(p + c, ks);
+            for (long long rb = nrb - 1; rb >= 0; --rb) {
+                const long long klim = p + std::min(c, (rb + 1) * BM);
+                const long long kp = ceil_div_ll(ceil_div_ll(klim, ceil_div_ll(klim, ks)), 64) * 64;
+                for (long long j = 0; j < nks; ++j) {
+                    const long long keys = std::min(kp, klim - j * kp);
+                    items.push_back(keys > 0 ? kChunkItemUs + kChunkTileUs * (double)ceil_div_ll(keys, KT)
+                                             : kEmptyItemUs);
+                }
+            }
+        }
+    };
+    // large items first: number the chunk requests from the last one when
+    // its items are the larger ones
+    const bool rev = chunks.size() > 1 && chunks.back().first + chunks.back().second >
+                                              chunks.front().first + chunks.front().second;
+
+    // Decode units: the candidate sizes (tiles) that respect the kernel's
     // per-unit segment and page-window limits.
     std::vector<long long> units;
     if (dec_total > 0) {
@@ -271,98 +339,81 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                                    ceil_div_ll(dec_total, G)};
         for (long long U : cands) {
             U = std::max(1LL, std::min(U, dec_total));
-            while (U > 1 && !dec_share_fits(dec, dec_total, U, (int)P)) U = std::max(1LL, U * 3 / 4);
-            if (!dec_share_fits(dec, dec_total, U, (int)P)) continue;
+            bool fits;
+            while (!(fits = dec_share_fits(dec, dec_total, U, (int)P, min_tiles)) && U > 1) U = std::max(1LL, U * 3 / 4);
+            if (!fits) continue;
             if (std::find(units.begin(), units.end(), U) == units.end()) units.push_back(U);
         }
         if (units.empty())
             return fail(MLA_ERR_UNSUPPORTED, "decode work does not fit the per-unit segment / page limits");
     }
-    // Finishing time of the decode units (equal cost u) poured onto the loads
-    // left by the chunk items, plus the merge of the requests they split.
+    // Finishing time of the decode units (equal cost u) poured onto the
+    // workgroup loads left by the chunk items, plus the merge of the requests
+    // they split.
     auto with_decode = [&](const std::vector<LoadRun> &loads, long long U) {
         const long long n = ceil_div_ll(ceil_div_ll(dec_total, U), 2);  // work items: pairs of units
         const double u = kDecUnitUs + kDecTileUs * (double)U;
         long long split_parts = 0;
+        const uint32_t u32 = (uint32_t)U;  // tile indices stay below 2^30
         for (const DecReq &d : dec) {
-            const long long parts = (d.first_tile + d.tiles - 1) / U - d.first_tile / U + 1;
+            const uint32_t f = (uint32_t)d.first_tile, l = (uint32_t)(d.first_tile + d.tiles - 1);
+            const uint32_t parts = l / u32 - f / u32 + 1;
             if (parts > 1) split_parts += parts + 1;
         }
         return fill_units(loads, n, u) + (double)split_parts * row_bytes / (kMergeGBs * 1e3);
     };
 
-    // Chunk key split (keys per item).  Items in device queue order: request
-    // by request, blocks largest first, ceil((p + c) / ks) key splits per
-    // block (a split past a block's causal limit is an empty item, still taken
-    // off the queue).
+    // Key split: the closed-form estimate keeps the best candidate (and the
+    // runner-up when within 10%), whose queue is then simulated (with the
+    // decode units after it).
     long long ks_best = cap, U_best = units.empty() ? 1 : units.back();
+    const long long ks_forced = debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed);
     {
-        // first pass: each key split with a cheap estimate of the decode fill;
-        // second pass: the exact fill for the two best splits
         struct Cand {
             long long ks;
-            double merge_us, est;
-            std::vector<LoadRun> loads;
+            double est, merge_us;
         };
         std::vector<Cand> cands;
-        std::vector<double> items;
-        for (long long ks = 64;; ks *= 2) {
-            const long long k = std::min(ks, cap);
-            items.clear();
-            long long split_rows = 0;
-            bool too_many = false;
-            for (const auto &pc : chunks) {
-                const long long p = pc.first, c = pc.second;
-                const long long nrb = ceil_div_ll(c, BM), nks = ceil_div_ll(p + c, k);
-                if ((long long)items.size() + nrb * nks > 4LL * G) {
-                    too_many = true;
-                    break;
+        // the decode work fills the CUs after the chunk items: about
+        // kDecTileUs / 2 per tile (the two units of an item run side by side)
+        const double dec_work = 0.5 * kDecTileUs * (double)dec_total;
+        if (!chunks.empty() && ks_forced > 0) {
+            cands.push_back(Cand{std::min(ks_forced, cap), 0.0, chunk_est(std::min(ks_forced, cap)).merge_us});
+        } else if (!chunks.empty()) {
+            for (long long ks = 64;; ks *= 2) {
+                const long long k = std::min(ks, cap);
+                const ChunkEst e = chunk_est(k);
+                if (e.items <= 8LL * G || k >= cap) {
+                    const double tail = e.items <= G ? 0.0 : 0.5 * e.total / (double)e.items;
+                    cands.push_back(
+                        Cand{k, std::max(e.max_item, (e.total + dec_work) / G + tail) + e.merge_us, e.merge_us});
                 }
-                for (long long rb = nrb - 1; rb >= 0; --rb) {
-                    const long long keys = p + std::min(c, (rb + 1) * BM);
-                    const long long ns = ceil_div_ll(keys, k);
-                    for (long long j = 0; j < nks; ++j)
-                        items.push_back(j < ns ? kChunkItemUs + kChunkTileUs * (double)ceil_div_ll(
-                                                                                 std::min(k, keys - j * k), KT)
-                                               : kEmptyItemUs);
-                    // partial rows are written, read back and the final row written by the merge
-                    if (ns > 1) split_rows += (ns + 1) * std::min<long long>(BM, c - rb * BM);
-                }
+                if (k >= cap) break;
             }
-            if (!too_many) {
-                Cand cd{k, (double)split_rows * row_bytes / (kMergeGBs * 1e3), 0.0, load_runs(simulate_chunks(items, G))};
-                double mx = 0.0, sum = 0.0;
-                for (const LoadRun &r : cd.loads) {
-                    mx = std::max(mx, r.load);
-                    sum += r.load * (double)r.count;
-                }
-                double est = mx;
-                if (dec_total > 0) {
-                    est = 1e300;
-                    for (long long U : units) {
-                        const double u = kDecUnitUs + kDecTileUs * (double)U;
-                        est = std::min(est, std::max(mx, (sum + (double)ceil_div_ll(ceil_div_ll(dec_total, U), 2) * u) /
-                                                                 G));
-                    }
-                }
-                cd.est = est + cd.merge_us;
-                cands.push_back(std::move(cd));
-            }
-            if (k >= cap || chunks.empty()) break;
+            std::sort(cands.begin(), cands.end(), [](const Cand &x, const Cand &y) { return x.est < y.est; });
+            // the runner-up is simulated too only when the estimates are close
+            cands.resize(cands.size() > 1 && cands[1].est <= 1.1 * cands[0].est ? 2 : 1);
+        } else {
+            cands.push_back(Cand{cap, 0.0, 0.0});
         }
-        std::sort(cands.begin(), cands.end(), [](const Cand &x, const Cand &y) { return x.est < y.est; });
         double best = 1e300;
-        for (size_t i = 0; i < cands.size() && i < 2; ++i) {
-            const Cand &cd = cands[i];
+        std::vector<double> items;
+        for (const Cand &cd : cands) {
+            std::vector<LoadRun> loads{LoadRun{0.0, (long long)G}};
+            if (!chunks.empty()) {
+                chunk_items(cd.ks, rev, items);
+                loads = load_runs(simulate_chunks(items, G));
+            }
             if (dec_total == 0) {
-                if (cd.est < best) {
-                    best = cd.est;
+                const double t = loads.back().load + cd.merge_us;
+                if (t < best) {
+                    best = t;
                     ks_best = cd.ks;
                 }
                 continue;
             }
             for (long long U : units) {
-                const double t = with_decode(cd.loads, U) + cd.merge_us;
+                const double t = with_decode(loads, U) + cd.merge_us;
                 if (t < best) {
                     best = t;
                     ks_best = cd.ks;
@@ -377,9 +428,10 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     for (const auto &pc : chunks) {
         const long long p = pc.first, c = pc.second;
         nci += ceil_div_ll(c, BM) * ceil_div_ll(p + c, ks_best);
-        if (p + c > ks_best) pl->chunk_split = true;
+        if (ceil_div_ll(p + c, ks_best) > 1) pl->chunk_split = true;
     }
     if (nci > (1LL << 27)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
+    pl->chunk_rev = rev;
     pl->ks_chunk = (int)ks_best;
     pl->n_chunk_items = (int)nci;
     pl->n_dec_units = (int)ceil_div_ll(n_units, 2);  // a work item is a pair of units, one per wave group
@@ -411,10 +463,11 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     static const bool log_plan = std::getenv("MLA_PLAN_LOG") != nullptr;
     if (log_plan)
         std::fprintf(stderr,
-                     "[mla plan] R=%d CUs=%d chunk items=%d (ks=%d keys, split=%d) decode units=%d x %d tiles "
-                     "(total %lld, split=%d, merge x%d) grid=%d workspace=%zu B\n",
-                     sh.R, ncu, pl->n_chunk_items, pl->ks_chunk, (int)pl->chunk_split, pl->n_dec_units,
-                     pl->dec_unit_tiles, dec_total, (int)pl->dec_split, pl->merge_hsplit, pl->grid, pl->bytes);
+                     "[mla plan] R=%d CUs=%d chunk items=%d (ks=%d keys, split=%d, rev=%d) decode units=%d x %d "
+                     "tiles (total %lld, split=%d, merge x%d) grid=%d workspace=%zu B\n",
+                     sh.R, ncu, pl->n_chunk_items, pl->ks_chunk, (int)pl->chunk_split, (int)pl->chunk_rev,
+                     pl->n_dec_units, pl->dec_unit_tiles, dec_total, (int)pl->dec_split, pl->merge_hsplit, pl->grid,
+                     pl->bytes);
     return MLA_OK;
 }
 
@@ -430,12 +483,14 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute rou
     thread_local std::vector<int32_t> key;
     thread_local Plan cached;
     thread_local bool have = false;
-    const size_t n = 6 + 2 * (size_t)sh.R;
+    const size_t n = 7 + 2 * (size_t)sh.R;
+    const int forced = debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed);
     bool same = have && key.size() == n && key[0] == b->page_size && key[1] == ncu && key[2] == sh.R &&
-                key[3] == b->max_pages_per_req && key[4] == route.min_rows && key[5] == route.pair_keys;
+                key[3] == b->max_pages_per_req && key[4] == route.min_rows && key[5] == route.pair_keys &&
+                key[6] == forced;
     if (same) {
-        same = std::memcmp(key.data() + 6, b->q_lens, sh.R * sizeof(int32_t)) == 0 &&
-               std::memcmp(key.data() + 6 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t)) == 0;
+        same = std::memcmp(key.data() + 7, b->q_lens, sh.R * sizeof(int32_t)) == 0 &&
+               std::memcmp(key.data() + 7 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t)) == 0;
     }
     if (same) {
         *pl = cached;
@@ -450,8 +505,9 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute rou
     key[3] = b->max_pages_per_req;
     key[4] = route.min_rows;
     key[5] = route.pair_keys;
-    std::memcpy(key.data() + 6, b->q_lens, sh.R * sizeof(int32_t));
-    std::memcpy(key.data() + 6 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t));
+    key[6] = forced;
+    std::memcpy(key.data() + 7, b->q_lens, sh.R * sizeof(int32_t));
+    std::memcpy(key.data() + 7 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t));
     cached = *pl;
     have = true;
     return MLA_OK;
@@ -621,7 +677,9 @@ int mla_debug_set(int32_t knob, int32_t value) {
     if (knob == MLA_DEBUG_CHECK && value != 0 && value != 1)
         return fail(MLA_ERR_INVALID_ARG, "check mode must be 0 or 1, not %d", value);
     if (knob == MLA_DEBUG_SPIN_LIMIT && value < -1) return fail(MLA_ERR_INVALID_ARG, "spin limit %d < -1", value);
-    debug_value(knob).store(knob == MLA_DEBUG_SPIN_LIMIT && value == -1 ? mla::kSpinLimit : value);
+    if (knob == MLA_DEBUG_CHUNK_KEYS && (value < -1 || value % 64 != 0) && value != -1)
+        return fail(MLA_ERR_INVALID_ARG, "chunk key split %d is not a non-negative multiple of 64", value);
+    debug_value(knob).store(value != -1 ? value : knob == MLA_DEBUG_SPIN_LIMIT ? mla::kSpinLimit : 0);
     return MLA_OK;
 }
 
@@ -677,6 +735,7 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
     a.num_pages = batch->num_pages;
     a.scale_log2 = (float)((double)softmax_scale * 1.4426950408889634);
     a.ks_chunk = pl.ks_chunk;
+    a.chunk_rev = pl.chunk_rev ? 1 : 0;
     a.n_chunk_items = pl.n_chunk_items;
     a.n_dec_units = pl.n_dec_units;
     a.dec_unit_tiles = pl.dec_unit_tiles;

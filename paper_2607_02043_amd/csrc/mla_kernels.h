@@ -48,7 +48,8 @@ struct AttnArgs {
     int32_t max_pages;
     int32_t num_pages;
     float scale_log2;     // softmax scale * log2(e)
-    int32_t ks_chunk;          // keys per chunk work item (a multiple of 64)
+    int32_t ks_chunk;          // chunk blocks are cut into ceil((p + c) / ks_chunk) key ranges (a multiple of 64)
+    int32_t chunk_rev;         // chunk items numbered from the last request to the first
     int32_t n_chunk_items;     // work items 0 .. n_chunk_items - 1
     int32_t n_dec_units;       // then the decode items: pairs of units (slices of the flattened decode
                                // tile list), one unit per wave group

@@ -203,6 +203,7 @@ __device__ __forceinline__ u32x2 lds_read_tr16(const char *p) {
 struct ReqLens {
     const int32_t *cu_q;
     const int32_t *prefix;
+    bool rev;  // number the items from the last request to the first
 };
 
 struct Located {
@@ -217,9 +218,9 @@ __device__ bool locate_item(int target, int num_reqs, const ReqLens &rl, CountFn
     if (tid == 0) s_tmp[8] = -1;
     int running = 0;
     for (int base = 0; base < num_reqs; base += nthr) {
-        const int r = base + tid;
+        const int r = rl.rev ? num_reqs - 1 - (base + tid) : base + tid;
         int cnt = 0, p = 0, row0 = 0, c = 0;
-        if (r < num_reqs) {
+        if (base + tid < num_reqs) {
             row0 = rl.cu_q[r];
             c = rl.cu_q[r + 1] - row0;
             p = rl.prefix[r];
@@ -272,6 +273,12 @@ struct ChunkItem {
     int r, p, c, row0, i0, i1, k0, k1, ks, nks_eff;
 };
 
+// Item `local` of a chunk request: every block of 8 query tokens (the
+// longest rows first) takes nks = ceil((p + c) / ks_chunk) queue slots.  The
+// block's keys (0 .. p + i1 - 1, its causal limit klim) are cut into
+// ceil(klim / ks_chunk) ranges of equal length, rounded up to a multiple of
+// 64 keys (at most ks_chunk); the remaining slots are empty items.  A block
+// whose keys fit one range writes its rows directly.
 __device__ __forceinline__ ChunkItem decode_chunk_item(const AttnArgs &a, const Located &lc) {
     ChunkItem it;
     it.r = lc.r;
@@ -285,9 +292,10 @@ __device__ __forceinline__ ChunkItem decode_chunk_item(const AttnArgs &a, const 
     it.i0 = rb * kChunkBlockTokens;
     it.i1 = min(it.i0 + kChunkBlockTokens, it.c);
     const int klim = it.p + it.i1;
-    it.nks_eff = ceil_div(klim, a.ks_chunk);
-    it.k0 = it.ks * a.ks_chunk;
-    it.k1 = min(klim, it.k0 + a.ks_chunk);
+    const int kp = ceil_div(ceil_div(klim, ceil_div(klim, a.ks_chunk)), 64) * 64;  // keys per range (<= ks_chunk)
+    it.nks_eff = ceil_div(klim, kp);
+    it.k0 = it.ks * kp;
+    it.k1 = min(klim, it.k0 + kp);
     return it;
 }
 
@@ -1021,7 +1029,7 @@ __device__ __forceinline__ void lds_dma16_sbase_imm(const void *sbase, uint32_t 
 // item again with exact = true (the exact maxima wait in LDS).
 __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, int *s_pages, bool exact) {
     Located lc;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk, a.route}, s_tmp, lc)) return false;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix, a.chunk_rev != 0}, ChunkCount{a.ks_chunk, a.route}, s_tmp, lc)) return false;
     const ChunkItem it = decode_chunk_item(a, lc);
     TRACE(1);
     const int r = it.r;
@@ -1395,7 +1403,7 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(AttnArgs a) {
     // 0 merges that row over the block's splits
     const int item = (b - n_dec) / kChunkBlockTokens, j = (b - n_dec) % kChunkBlockTokens;
     Located lc;
-    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix}, ChunkCount{a.ks_chunk, a.route}, s_tmp, lc)) return;
+    if (!locate_item(item, a.num_reqs, ReqLens{a.cu_q, a.prefix, a.chunk_rev != 0}, ChunkCount{a.ks_chunk, a.route}, s_tmp, lc)) return;
     const ChunkItem it = decode_chunk_item(a, lc);
     if (it.ks != 0 || it.nks_eff <= 1 || a.ws_chunk_o == nullptr || j >= it.i1 - it.i0) return;
     if (it.p < 0 || it.row0 < 0 || it.row0 + it.i1 > a.num_rows) return;

@@ -3,6 +3,7 @@
 // launched here, and the device queries answer for a 256-CU device).  Input on
 // stdin, one batch per line:
 //   ncu page_size R q_0 p_0 q_1 p_1 ...
+// (PLAN_ROUTE and PLAN_CHUNK_KEYS in the environment: see main)
 // Output, one line per batch:
 //   ok ks n_chunk_items n_dec_items unit_tiles dec_total grid merge_hsplit chunk_split dec_split bytes
 //      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us
@@ -55,6 +56,8 @@ int main() {
         std::istringstream r(e);
         r >> route.min_rows >> route.pair_keys;
     }
+    // PLAN_CHUNK_KEYS=k: the forced chunk key split of the debug knob
+    if (const char *e = std::getenv("PLAN_CHUNK_KEYS")) mla_debug_set(MLA_DEBUG_CHUNK_KEYS, std::atoi(e));
     std::string line;
     while (std::getline(std::cin, line)) {
         const bool noalloc = line.rfind("na ", 0) == 0;

@@ -146,4 +146,8 @@ def test_debug_settings_are_checked_on_the_host():
     assert L.mla_debug_set(mla.MLA_DEBUG_SPIN_LIMIT, -5) == mla.MLA_ERR_INVALID_ARG
     assert L.mla_debug_set(mla.MLA_DEBUG_SPIN_LIMIT, -1) == mla.MLA_OK
     assert L.mla_debug_set(mla.MLA_DEBUG_CHECK, 0) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 100) == mla.MLA_ERR_INVALID_ARG
+    assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, -64) == mla.MLA_ERR_INVALID_ARG
+    assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 128) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, -1) == mla.MLA_OK
     assert L.mla_device_flags(1, None, None) == mla.MLA_ERR_INVALID_ARG

@@ -237,3 +237,17 @@ def test_chunk_value_range():
     assert d_big.max() <= 65280 * 2.0 ** -10, "large value dims lost precision (clamped?)"
     assert d_tiny.max() <= 2.0 ** -22, "fp16-subnormal value dims lost more than the subnormal spacing"
     assert_close(out[..., 64:], out_ref[..., 64:], g.lse_np(), lse_ref, what="value range, other dims")
+
+
+@pytest.mark.parametrize("keys", [64, 192, 1024])
+def test_forced_chunk_key_splits(keys):
+    """Every block of 8 chunk tokens cut into many key ranges (equal 64-aligned
+    ranges, the last ones shorter or empty), merged by the split combine: the
+    result must not depend on the split.  Page 16 and ragged chunk tails."""
+    wl = W.custom([5000, 15, 0, 1300, 333], [37, 1, 70, 9, 1], page_size=16, seed=keys, name=f"split{keys}")
+    log(f"[gpu] forced chunk key split {keys}")
+    mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, keys)
+    try:
+        _compare_all_rows(wl, wl.layer(0))
+    finally:
+        mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)

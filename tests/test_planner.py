@@ -32,12 +32,14 @@ def harness(tmp_path_factory):
     return exe
 
 
-def plan(exe, batches, route=None):
+def plan(exe, batches, route=None, chunk_keys=None):
     text = "".join(f"{ncu} {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n"
                    for ncu, P, q, p in batches)
     env = dict(os.environ)
     if route is not None:
         env["PLAN_ROUTE"] = f"{route[0]} {route[1]}"
+    if chunk_keys is not None:
+        env["PLAN_CHUNK_KEYS"] = str(chunk_keys)
     out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True,
                          env=env).stdout.splitlines()
     assert len(out) == len(batches)
@@ -217,3 +219,16 @@ def test_noalloc_entry_rejects_batches_beyond_its_scratch(harness):
     b, s = lines[0].split(), lines[1].split()
     assert int(b[2]) > 128 << 20 and int(b[1]) == -3 and "no-allocation" in lines[0]
     assert int(s[2]) <= 128 << 20 and int(s[1]) == 0
+
+
+@pytest.mark.parametrize("keys", [64, 320, 4096])
+def test_forced_chunk_key_split(harness, keys):
+    """The debug knob fixes the chunk key split (capped by the page window);
+    the plan still respects every kernel limit."""
+    rng = np.random.default_rng(keys)
+    batches = [random_batch(rng, 256) for _ in range(40)]
+    for batch, d in zip(batches, plan(harness, batches, chunk_keys=keys)):
+        check_plan(batch, d)
+        ncu, P, q, p = batch
+        if any(qi > 1 for qi in q):
+            assert d["ks"] == min(keys, max(64, (PAGE_WINDOW - 1) * P // 64 * 64))
