@@ -512,7 +512,8 @@ def plan_inclusive(args, wl, steps, warmup):
     appended slot lies inside the workload's block table and pool.  Reported:
     the wall time per step of the whole loop (host checks, planning and
     launches overlap the GPU work of the steps before) and the host time of
-    the checks and the planning alone, per new batch."""
+    the checks and the planning alone, per new batch: as served (warm-started
+    from the last full plan) and with every batch planned in full."""
     import torch
 
     import paper_2607_02043_amd as mla
@@ -527,18 +528,28 @@ def plan_inclusive(args, wl, steps, warmup):
         p[dec] = np.maximum(0, p[dec] - (n - 1) + k)
         batches.append(mla.DeviceBatch(b.q_lens, p.astype(np.int32), b.block_table, b.page_size, b.num_pages,
                                        device=dev))
-    reps = []
-    for _ in range(5):  # every call meets a new batch: the plan cache never hits
-        t = time.perf_counter()
-        for db in batches:
-            mla.mixed_step_workspace_bytes(db)
-        reps.append((time.perf_counter() - t) / n * 1e6)
+    def plan_time(warm):
+        mla.debug_set(mla.MLA_DEBUG_WARM_PLAN, 1 if warm else 0)
+        try:
+            reps = []
+            for _ in range(5):  # every call meets a new batch: the exact-lengths cache never hits
+                t = time.perf_counter()
+                for db in batches:
+                    mla.mixed_step_workspace_bytes(db)
+                reps.append((time.perf_counter() - t) / n * 1e6)
+        finally:
+            mla.debug_set(mla.MLA_DEBUG_WARM_PLAN, -1)
+        return {"median": round(float(np.median(reps)), 2), "min": round(float(np.min(reps)), 2)}
+
+    cold = plan_time(False)
+    warm = plan_time(True)
     m = measure(args, wl, steps, warmup, batches=batches)
     s = summary(wl, m)
     s["workload"] = wl.name + "; decode lengths +1 per step"
-    s["host_plan_us"] = {"median": round(float(np.median(reps)), 2), "min": round(float(np.min(reps)), 2)}
+    s["host_plan_us"] = warm
+    s["host_plan_full_us"] = cold
     log(f"[bench] plan-inclusive {wl.name[:40]}: {s['us_per_step']:.1f} us/step, host plan "
-        f"{s['host_plan_us']['median']:.1f} us")
+        f"{warm['median']:.1f} us warm, {cold['median']:.1f} us in full")
     return s
 
 

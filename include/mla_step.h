@@ -124,13 +124,23 @@ int mla_device_flags(int32_t clear, int32_t *flags, void *stream);
  *                         8 query tokens is cut into ceil((p + c) / value) key
  *                         ranges; a multiple of 64, capped by what one work
  *                         item may hold); 0 or -1: the planner's choice.  For
- *                         tuning and tests: results stay within rounding.
+ *                         tuning and tests: results stay within rounding;
+ *   MLA_DEBUG_WARM_PLAN   1 (the default; -1 restores it): a batch with as
+ *                         many chunk requests as the last fully planned one
+ *                         (same page size, table width and device), and
+ *                         within 1/16 of its decode requests, decode tiles,
+ *                         chunk query-key pairs and longest chunk, keeps
+ *                         that plan's key split and decode unit size when
+ *                         the unit still fits the kernel's limits (counts and
+ *                         offsets are recomputed, O(requests)); 0: every new
+ *                         batch is planned in full.
  * Errors: MLA_ERR_INVALID_ARG (unknown knob, bad value). */
 typedef enum {
     MLA_DEBUG_CHECK = 0,
     MLA_DEBUG_SPIN_LIMIT = 1,
     MLA_DEBUG_CHUNK_KEYS = 2,
-    MLA_DEBUG_COUNT = 3
+    MLA_DEBUG_WARM_PLAN = 3,
+    MLA_DEBUG_COUNT = 4
 } mla_debug_knob;
 int mla_debug_set(int32_t knob, int32_t value);
 

@@ -68,6 +68,7 @@ std::atomic<int> &debug_value(int knob) {
         v[MLA_DEBUG_CHECK].store(e && std::atoi(e) != 0 ? 1 : 0);
         v[MLA_DEBUG_SPIN_LIMIT].store(mla::kSpinLimit);
         v[MLA_DEBUG_CHUNK_KEYS].store(0);
+        v[MLA_DEBUG_WARM_PLAN].store(1);
     });
     return v[knob];
 }
@@ -127,6 +128,11 @@ struct Plan {
     int n_dec_units = 0, dec_unit_tiles = 0, dec_total_tiles = 0, grid = 0, merge_hsplit = 1;
     bool chunk_split = false, dec_split = false, chunk_rev = false;
     size_t off_chunk_o = 0, off_chunk_ml = 0, off_dec_o = 0, off_dec_ml = 0, bytes = 0;
+    // what a warm start compares: the work of the batch the plan was made for
+    double chunk_pairs = 0.0;  // query-key pairs of the chunk requests
+    long long chunk_keys_max = 0;  // keys of the longest chunk request
+    int n_chunk_reqs = 0, n_dec_reqs = 0;
+    bool warm = false;  // key split and unit size taken from an earlier plan
 };
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
@@ -250,7 +256,8 @@ double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
 // The device recomputes the same mapping from the device copies of the
 // lengths.  Cost: a closed form per request and candidate key split, then a
 // queue simulation of the best one or two.
-int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkRoute route, Plan *pl) {
+int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkRoute route, Plan *pl,
+                       const Plan *warm = nullptr) {
     const long long P = b->page_size;
     long long cap = ((long long)(mla::kPageWindow - 1) * P) / 64 * 64;  // keys per chunk item
     if (cap < 64) cap = 64;
@@ -275,6 +282,33 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     for (const DecReq &d : dec) min_tiles = std::min(min_tiles, d.tiles);
     const int G = std::max(1, ncu);
     const double row_bytes = (double)mla::kPartialFloats * 4.0;
+    double chunk_pairs = 0.0;
+    long long chunk_keys_max = 0;
+    for (const auto &pc : chunks) {
+        chunk_pairs += (double)pc.second * ((double)pc.first + 0.5 * (double)(pc.second + 1));
+        chunk_keys_max = std::max(chunk_keys_max, pc.first + pc.second);
+    }
+    // large items first: number the chunk requests from the last one when
+    // its items are the larger ones
+    const bool rev = chunks.size() > 1 && chunks.back().first + chunks.back().second >
+                                              chunks.front().first + chunks.front().second;
+
+    // Warm start: a batch with as many chunk requests as an earlier plan's,
+    // and within 1/16 of its decode requests, decode tiles, chunk pairs and
+    // longest chunk (a serving step whose decode lengths grew by a token, or
+    // that gained or lost a few requests), keeps that plan's key split and
+    // unit size when the unit still fits the kernel's limits; only the
+    // derived counts below are recomputed.
+    if (warm != nullptr) {
+        const auto near = [](double x, double y) { return std::fabs(x - y) <= y / 16.0; };
+        const long long U = warm->dec_unit_tiles;
+        const bool ok = (int)chunks.size() == warm->n_chunk_reqs && near((double)dec.size(), warm->n_dec_reqs) &&
+                        near((double)dec_total, (double)warm->dec_total_tiles) && near(chunk_pairs, warm->chunk_pairs) &&
+                        near((double)chunk_keys_max, (double)warm->chunk_keys_max) &&
+                        warm->ks_chunk >= 64 && warm->ks_chunk <= cap &&
+                        (dec_total == 0 || (U >= 1 && U <= dec_total && dec_share_fits(dec, dec_total, U, (int)P, min_tiles)));
+        if (!ok) warm = nullptr;
+    }
 
     // Chunk work for a key split ks: total cost, largest item, items, and
     // the partial rows (written, read back, the merged row written).  Per
@@ -326,15 +360,10 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             }
         }
     };
-    // large items first: number the chunk requests from the last one when
-    // its items are the larger ones
-    const bool rev = chunks.size() > 1 && chunks.back().first + chunks.back().second >
-                                              chunks.front().first + chunks.front().second;
-
     // Decode units: the candidate sizes (tiles) that respect the kernel's
     // per-unit segment and page-window limits.
     std::vector<long long> units;
-    if (dec_total > 0) {
+    if (dec_total > 0 && warm == nullptr) {
         const long long cands[] = {8, 16, 32, 64, ceil_div_ll(dec_total, 3LL * G), ceil_div_ll(dec_total, 2LL * G),
                                    ceil_div_ll(dec_total, G)};
         for (long long U : cands) {
@@ -368,7 +397,10 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     // decode units after it).
     long long ks_best = cap, U_best = units.empty() ? 1 : units.back();
     const long long ks_forced = debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed);
-    {
+    if (warm != nullptr) {
+        ks_best = warm->ks_chunk;
+        U_best = std::max(1, warm->dec_unit_tiles);
+    } else {
         struct Cand {
             long long ks;
             double est, merge_us;
@@ -432,6 +464,11 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     }
     if (nci > (1LL << 27)) return fail(MLA_ERR_INVALID_ARG, "step needs too many work items");
     pl->chunk_rev = rev;
+    pl->chunk_pairs = chunk_pairs;
+    pl->chunk_keys_max = chunk_keys_max;
+    pl->n_chunk_reqs = (int)chunks.size();
+    pl->n_dec_reqs = (int)dec.size();
+    pl->warm = warm != nullptr;
     pl->ks_chunk = (int)ks_best;
     pl->n_chunk_items = (int)nci;
     pl->n_dec_units = (int)ceil_div_ll(n_units, 2);  // a work item is a pair of units, one per wave group
@@ -464,52 +501,54 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     if (log_plan)
         std::fprintf(stderr,
                      "[mla plan] R=%d CUs=%d chunk items=%d (ks=%d keys, split=%d, rev=%d) decode units=%d x %d "
-                     "tiles (total %lld, split=%d, merge x%d) grid=%d workspace=%zu B\n",
+                     "tiles (total %lld, split=%d, merge x%d) grid=%d workspace=%zu B%s\n",
                      sh.R, ncu, pl->n_chunk_items, pl->ks_chunk, (int)pl->chunk_split, (int)pl->chunk_rev,
                      pl->n_dec_units, pl->dec_unit_tiles, dec_total, (int)pl->dec_split, pl->merge_hsplit, pl->grid,
-                     pl->bytes);
+                     pl->bytes, pl->warm ? " (warm)" : "");
     return MLA_OK;
 }
 
 // The plan depends only on the host lengths, the page size and the CU count;
 // the last one is kept per thread so a steady stream of identical steps
-// plans once.
+// plans once.  The last full plan is kept too, as the warm start of batches
+// with nearly the same work (MLA_DEBUG_WARM_PLAN = 0 turns that off).
 int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute route = mla::kAbsorbAll) {
     *pl = Plan{};
     if (sh.R == 0) return MLA_OK;
     int st = MLA_OK;
     const int ncu = cu_count(&st);
     if (st != MLA_OK) return st;
+    constexpr size_t kHdr = 7;
+    const int32_t hdr[kHdr] = {b->page_size, ncu, sh.R, b->max_pages_per_req, route.min_rows, route.pair_keys,
+                               debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed)};
+    const size_t qbytes = (size_t)sh.R * sizeof(int32_t);
+    // key: header, query lengths, prefix lengths
     thread_local std::vector<int32_t> key;
-    thread_local Plan cached;
-    thread_local bool have = false;
-    const size_t n = 7 + 2 * (size_t)sh.R;
-    const int forced = debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed);
-    bool same = have && key.size() == n && key[0] == b->page_size && key[1] == ncu && key[2] == sh.R &&
-                key[3] == b->max_pages_per_req && key[4] == route.min_rows && key[5] == route.pair_keys &&
-                key[6] == forced;
-    if (same) {
-        same = std::memcmp(key.data() + 7, b->q_lens, sh.R * sizeof(int32_t)) == 0 &&
-               std::memcmp(key.data() + 7 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t)) == 0;
-    }
-    if (same) {
+    thread_local int32_t anchor_hdr[kHdr] = {};
+    thread_local bool have_anchor = false;
+    thread_local Plan cached, anchor;
+    if (key.size() == kHdr + 2 * (size_t)sh.R && std::memcmp(key.data(), hdr, sizeof hdr) == 0 &&
+        std::memcmp(key.data() + kHdr, b->q_lens, qbytes) == 0 &&
+        std::memcmp(key.data() + kHdr + sh.R, b->prefix_lens, qbytes) == 0) {
         *pl = cached;
         return MLA_OK;
     }
-    st = make_plan_uncached(b, sh, ncu, route, pl);
+    // the anchor's header must match except for the request count
+    const bool warm = debug_value(MLA_DEBUG_WARM_PLAN).load(std::memory_order_relaxed) != 0 && have_anchor &&
+                      std::memcmp(anchor_hdr, hdr, 2 * sizeof(int32_t)) == 0 &&
+                      std::memcmp(anchor_hdr + 3, hdr + 3, (kHdr - 3) * sizeof(int32_t)) == 0;
+    st = make_plan_uncached(b, sh, ncu, route, pl, warm ? &anchor : nullptr);
     if (st != MLA_OK) return st;
-    key.resize(n);
-    key[0] = b->page_size;
-    key[1] = ncu;
-    key[2] = sh.R;
-    key[3] = b->max_pages_per_req;
-    key[4] = route.min_rows;
-    key[5] = route.pair_keys;
-    key[6] = forced;
-    std::memcpy(key.data() + 7, b->q_lens, sh.R * sizeof(int32_t));
-    std::memcpy(key.data() + 7 + sh.R, b->prefix_lens, sh.R * sizeof(int32_t));
+    key.resize(kHdr + 2 * (size_t)sh.R);
+    std::memcpy(key.data(), hdr, sizeof hdr);
+    std::memcpy(key.data() + kHdr, b->q_lens, qbytes);
+    std::memcpy(key.data() + kHdr + sh.R, b->prefix_lens, qbytes);
     cached = *pl;
-    have = true;
+    if (!pl->warm) {
+        anchor = *pl;
+        std::memcpy(anchor_hdr, hdr, sizeof hdr);
+        have_anchor = true;
+    }
     return MLA_OK;
 }
 
@@ -679,7 +718,10 @@ int mla_debug_set(int32_t knob, int32_t value) {
     if (knob == MLA_DEBUG_SPIN_LIMIT && value < -1) return fail(MLA_ERR_INVALID_ARG, "spin limit %d < -1", value);
     if (knob == MLA_DEBUG_CHUNK_KEYS && (value < -1 || value % 64 != 0) && value != -1)
         return fail(MLA_ERR_INVALID_ARG, "chunk key split %d is not a non-negative multiple of 64", value);
-    debug_value(knob).store(value != -1 ? value : knob == MLA_DEBUG_SPIN_LIMIT ? mla::kSpinLimit : 0);
+    if (knob == MLA_DEBUG_WARM_PLAN && value != 0 && value != 1 && value != -1)
+        return fail(MLA_ERR_INVALID_ARG, "warm planning must be 0 or 1, not %d", value);
+    const int dflt = knob == MLA_DEBUG_SPIN_LIMIT ? mla::kSpinLimit : knob == MLA_DEBUG_WARM_PLAN ? 1 : 0;
+    debug_value(knob).store(value != -1 ? value : dflt);
     return MLA_OK;
 }
 

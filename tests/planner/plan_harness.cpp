@@ -3,10 +3,10 @@
 // launched here, and the device queries answer for a 256-CU device).  Input on
 // stdin, one batch per line:
 //   ncu page_size R q_0 p_0 q_1 p_1 ...
-// (PLAN_ROUTE and PLAN_CHUNK_KEYS in the environment: see main)
+// (PLAN_ROUTE, PLAN_CHUNK_KEYS and PLAN_SERVING in the environment: see main)
 // Output, one line per batch:
 //   ok ks n_chunk_items n_dec_items unit_tiles dec_total grid merge_hsplit chunk_split dec_split bytes
-//      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us
+//      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us warm
 // or "err <status> <message>".
 // A line "ws <bytes> page_size R q_0 p_0 ..." instead calls the real
 // mixed_step_attn entry point with fake device pointers and a workspace of
@@ -56,6 +56,9 @@ int main() {
         std::istringstream r(e);
         r >> route.min_rows >> route.pair_keys;
     }
+    // PLAN_SERVING=1: plan through the library's cached, warm-started
+    // planner (the device's CU count, 256 here), as consecutive calls do
+    const bool serving = std::getenv("PLAN_SERVING") != nullptr;
     // PLAN_CHUNK_KEYS=k: the forced chunk key split of the debug knob
     if (const char *e = std::getenv("PLAN_CHUNK_KEYS")) mla_debug_set(MLA_DEBUG_CHUNK_KEYS, std::atoi(e));
     std::string line;
@@ -119,7 +122,7 @@ int main() {
         double us = 0.0;
         if (st == MLA_OK && sh.R > 0) {
             const auto t0 = std::chrono::steady_clock::now();
-            st = make_plan_uncached(&b, sh, ncu, route, &pl);
+            st = serving ? make_plan(&b, sh, &pl, route) : make_plan_uncached(&b, sh, ncu, route, &pl);
             us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
         }
         if (st != MLA_OK) {
@@ -129,7 +132,8 @@ int main() {
         std::cout << "ok " << pl.ks_chunk << " " << pl.n_chunk_items << " " << pl.n_dec_units << " "
                   << pl.dec_unit_tiles << " " << pl.dec_total_tiles << " " << pl.grid << " " << pl.merge_hsplit << " "
                   << (int)pl.chunk_split << " " << (int)pl.dec_split << " " << pl.bytes << " " << pl.off_chunk_o << " "
-                  << pl.off_chunk_ml << " " << pl.off_dec_o << " " << pl.off_dec_ml << " " << us << "\n";
+                  << pl.off_chunk_ml << " " << pl.off_dec_o << " " << pl.off_dec_ml << " " << us << " "
+                  << (int)pl.warm << "\n";
     }
     return 0;
 }

@@ -150,4 +150,7 @@ def test_debug_settings_are_checked_on_the_host():
     assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, -64) == mla.MLA_ERR_INVALID_ARG
     assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 128) == mla.MLA_OK
     assert L.mla_debug_set(mla.MLA_DEBUG_CHUNK_KEYS, -1) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_WARM_PLAN, 2) == mla.MLA_ERR_INVALID_ARG
+    assert L.mla_debug_set(mla.MLA_DEBUG_WARM_PLAN, 0) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_WARM_PLAN, -1) == mla.MLA_OK
     assert L.mla_device_flags(1, None, None) == mla.MLA_ERR_INVALID_ARG

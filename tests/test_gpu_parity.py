@@ -251,3 +251,20 @@ def test_forced_chunk_key_splits(keys):
         _compare_all_rows(wl, wl.layer(0))
     finally:
         mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)
+
+
+def test_serving_steps_with_warm_plans():
+    """Consecutive steps whose decode lengths grow by one token, as a decode
+    node serves them: every step is a new batch, planned warm from the first
+    one's plan (same key split and unit size, counts recomputed)."""
+    import dataclasses
+    wl = W.config(2)
+    b0, li = wl.batch, wl.layer(0)
+    dec = b0.q_lens == 1
+    for k in range(3):
+        p = b0.prefix_lens.astype(np.int64).copy()
+        p[dec] = np.maximum(0, p[dec] - 2 + k)
+        b = dataclasses.replace(b0, prefix_lens=p.astype(np.int32))
+        log(f"[gpu] serving step {k}: decode prefixes {int(p[dec].min())}..{int(p[dec].max())}")
+        g = run_layer(b, li, fused=True)
+        _compare_sampled(b, li, g, f"serving step {k}", seed=k)

@@ -232,3 +232,50 @@ def test_forced_chunk_key_split(harness, keys):
         ncu, P, q, p = batch
         if any(qi > 1 for qi in q):
             assert d["ks"] == min(keys, max(64, (PAGE_WINDOW - 1) * P // 64 * 64))
+
+
+def _serving_plans(harness, batches):
+    env = dict(os.environ, PLAN_SERVING="1")
+    text = "".join(f"256 {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n" for _, P, q, p in batches)
+    out = subprocess.run([harness], input=text, capture_output=True, text=True, check=True, env=env).stdout
+    res = []
+    for line in out.splitlines():
+        f = line.split()
+        assert f[0] == "ok", line
+        keys = ["ks", "n_chunk_items", "n_dec_items", "U", "dec_total", "grid", "hsplit", "chunk_split",
+                "dec_split", "bytes", "off_co", "off_cml", "off_do", "off_dml"]
+        d = {k: int(v) for k, v in zip(keys, f[1:15])}
+        d["us"], d["warm"] = float(f[15]), int(f[16])
+        res.append(d)
+    assert len(res) == len(batches)
+    return res
+
+
+def test_serving_sequence_plans_warm_and_stays_valid(harness):
+    """A decode node's consecutive steps: decode lengths grow by one token,
+    a request leaves and one joins now and then, the chunk moves on.  Steps
+    close to the last full plan reuse its key split and unit size; every plan
+    still respects the kernel limits, and a warm plan costs a few
+    microseconds."""
+    rng = np.random.default_rng(11)
+    dec = list(rng.integers(2000, 12000, 64))
+    chunk_p, chunk_c = 8192, 2048
+    batches = []
+    for step in range(60):
+        dec = [d + 1 for d in dec]
+        if step % 7 == 6:  # one request finishes, another joins
+            dec = dec[1:] + [int(rng.integers(2000, 12000))]
+        if step == 40:  # the chunk request moves to its next chunk: more keys
+            chunk_p += chunk_c
+        q = [1] * len(dec) + [chunk_c]
+        p = dec + [chunk_p]
+        batches.append((256, 64, q, p))
+    batches.append((256, 64, [1] * 8, list(rng.integers(100, 200, 8))))  # a different batch: planned in full
+    plans = _serving_plans(harness, batches)
+    for batch, d in zip(batches, plans):
+        check_plan(batch, d)
+    assert plans[0]["warm"] == 0 and plans[-1]["warm"] == 0
+    warm = [d for d in plans[1:40] if d["warm"]]
+    assert len(warm) >= 30
+    assert all(d["ks"] == plans[0]["ks"] and d["U"] == plans[0]["U"] for d in warm)
+    assert float(np.median([d["us"] for d in warm])) < 50.0
