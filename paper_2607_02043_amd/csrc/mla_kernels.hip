@@ -6,18 +6,23 @@
 // the paper); the head shapes are those of the served model's absorbed latent
 // attention (DeepSeek-V2-Lite, section 6).
 //
-// Work decomposition (one launch for all rows of a step):
-//   * decode rows (c = 1): persistent workgroups own equal shares of the list
-//     of all decode tiles (32 keys each); see the decode section below.
-//   * chunk rows (c > 1): one workgroup (4 wavefronts) per block of 4 query
-//     tokens (one per wave, 16 head rows each) times a key range of ks_chunk
-//     keys.  32-key tiles go through a 3-deep global -> LDS DMA ring; each
-//     tile's value part is converted once to fp16 and transposed in LDS so
-//     that P*V runs on fp16 MFMA.
-// Rows whose keys are split across workgroups leave fp32 partials (the
-// unnormalised sum, the running max and sum in log2 units); a second, small
-// merge kernel combines them in a fixed order.  Results are therefore
-// run-to-run deterministic and do not depend on the physical page order.
+// Work decomposition (one persistent launch for all rows of a step: one
+// 8-wavefront workgroup per CU takes work items from an atomic counter,
+// chunk items first, then decode items):
+//   * chunk rows (c > 1): an item is a block of 8 query tokens (one per
+//     wave, 16 head rows each) times a range of its causal keys.  32-key
+//     tiles stream through a 3-slot global -> LDS DMA ring; scores on bf16
+//     MFMA against a fixed reference max, probabilities to LDS as fp16, and
+//     each wave accumulates P*V for its 64 value dims of all 8 tokens on fp16
+//     MFMA, V read with transposing LDS reads and converted in registers.
+//   * decode rows (c = 1): the decode tiles (32 keys each) of all decode
+//     requests form one list cut into equal units; an item is a pair of
+//     units, one per 4-wave group of the workgroup, each streaming its tiles
+//     through its own 2-slot ring.
+// Rows whose keys are split across items leave fp32 partials (the
+// unnormalised sum, the max and sum in log2 units); a second, small merge
+// kernel combines them in a fixed order.  Results are therefore run-to-run
+// deterministic and do not depend on the physical page order.
 #include "mla_kernels.h"
 
 #include <limits.h>
@@ -176,18 +181,13 @@ __device__ __forceinline__ float wave_sum16(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// LDS byte offset of 16-byte chunk c of key k inside a tile.  Chunk
-// positions are xor-swizzled inside aligned groups of 8 chunks with a 3-bit
-// function of the key.  Decode tiles use the key's low 3 bits (8 lanes that
-// read the same chunk of 8 consecutive keys hit 8 different bank groups);
-// chunk tiles use bits 1..3 of the key, which keeps the 32x32 MFMA operand
-// reads (32 consecutive keys at one chunk) and the transposing value reads
-// free of bank conflicts.
-template <bool CHUNK>
-__device__ __forceinline__ int tile_swz(int k) {
-    return CHUNK ? (((k & 2) << 1) | ((k >> 2) & 3)) : (k & 7);
-}
-__device__ __forceinline__ int tile_off(int k, int c) { return (k * kChunksPerRow + (c ^ tile_swz<false>(k))) * 16; }
+// LDS byte offset of 16-byte chunk c of key k inside a decode tile (keys
+// row-major, 72 chunks each).  Chunk positions are xor-swizzled inside
+// aligned groups of 8 chunks with the key's low 3 bits, so 8 lanes that read
+// the same chunk of 8 consecutive keys hit 8 different bank groups.  Chunk
+// tiles use their own octet layout (see the chunk section).
+__device__ __forceinline__ int tile_swz(int k) { return k & 7; }
+__device__ __forceinline__ int tile_off(int k, int c) { return (k * kChunksPerRow + (c ^ tile_swz(k))) * 16; }
 
 // Transposing LDS read (gfx950): inside each 16-lane group, lane i receives
 // element (i & 3) of the 8 bytes read by lane 4 j + (i >> 2), j = 0..3.
@@ -313,43 +313,12 @@ __device__ __forceinline__ void load_page_window(const AttnArgs &a, int r, int l
     }
 }
 
-// Issue the DMA of one tile of KEYS keys (kbase .. kbase + KEYS - 1, clamped
-// to the last valid key k1 - 1 so every byte read is a finite cached latent).
-// Instruction i of wave wv fills 1 KB segment i * 4 + wv of the tile.
-// With a fused append, keys p_new .. are the step's new latents: key k comes
-// from row new_row0 + k - p_new of a.new_kv instead of its cache slot.
-template <int KEYS, bool CHUNK>
-__device__ __forceinline__ void issue_tile(const AttnArgs &a, const int *s_pages, int lp0, int kbase, int k1,
-                                           uint32_t lds_tile, int wv, int lane, int p_new, int new_row0) {
-    constexpr int kDma = KEYS * kRowBytes / (kThreads * 16);
-    const char *kv = reinterpret_cast<const char *>(a.kv);
-    const char *nkv = reinterpret_cast<const char *>(a.new_kv);
-    const char *src[kDma];
-#pragma unroll
-    for (int i = 0; i < kDma; ++i) {  // all page-id reads first, then the DMA burst
-        const int seg = i * 4 + wv;
-        const int u = seg * 64 + lane;
-        const int kk = u / kChunksPerRow;
-        const int c = (u - kk * kChunksPerRow) ^ tile_swz<CHUNK>(kk);
-        int key = kbase + kk;
-        key = key < k1 ? key : k1 - 1;
-        const int page = s_pages[min((key >> a.log2_page) - lp0, kPageWindow - 1)];
-        const size_t slot = (size_t)page * a.page_size + (key & (a.page_size - 1));
-        src[i] = (nkv != nullptr && key >= p_new) ? nkv + (size_t)(new_row0 + key - p_new) * kRowBytes + c * 16
-                                                  : kv + slot * kRowBytes + c * 16;
-    }
-#pragma unroll
-    for (int i = 0; i < kDma; ++i)
-        lds_dma16(src[i], __builtin_amdgcn_readfirstlane(lds_tile + (i * 4 + wv) * 1024));
-}
-
 // DMA of a 32-key tile that lies inside one page: a uniform source base (the
 // tile's first key) in SGPRs plus per-lane offsets fixed for all tiles.
 // Round i of wave wv fills LDS chunk u = 256 i + 64 wv + lane of the tile,
 // which holds source chunk (u % 72) ^ swz(key) of key u / 72.
 constexpr int kTileDma = kKeysPerTile * kRowBytes / (kThreads * 16);  // 9 rounds per tile
 // Offsets (< 2^16) packed two per register: round i in the half i & 1 of word i / 2.
-template <bool CHUNK>
 __device__ __forceinline__ void tile_dma_offsets(int wv, int lane, uint32_t (&off)[(kTileDma + 1) / 2]) {
 #pragma unroll
     for (int w = 0; w < (kTileDma + 1) / 2; ++w) off[w] = 0;
@@ -357,7 +326,7 @@ __device__ __forceinline__ void tile_dma_offsets(int wv, int lane, uint32_t (&of
     for (int i = 0; i < kTileDma; ++i) {
         const int u = (i * 4 + wv) * 64 + lane;
         const int kk = u / kChunksPerRow;
-        const int c = (u - kk * kChunksPerRow) ^ tile_swz<CHUNK>(kk);
+        const int c = (u - kk * kChunksPerRow) ^ tile_swz(kk);
         off[i / 2] |= (uint32_t)(kk * kRowBytes + c * 16) << (16 * (i & 1));
     }
 }
@@ -515,17 +484,19 @@ __device__ void merge_row(const AttnArgs &a, int row, int nsplit, Slot slot) {
 }
 
 // ------------------------------------------------------------ decode path
-// Decode rows run on persistent workgroups.  The 32-key tiles of all decode
-// requests, request after request, form one list; workgroup w owns tiles
-// [w S, (w + 1) S).  Its share splits into segments, one per request it
-// touches.  A segment streams its query block and then its tiles through a
-// 4-slot global -> LDS DMA ring, so prefetch runs on across request
-// boundaries and the start-up latency is paid once per workgroup.  Per tile,
-// wave w scores 16 keys over half of the 576 latent dims (the four partial
-// 16 x 16 score blocks meet in LDS), then accumulates its 128-wide slice of
-// the value dims over all 32 keys.  A request spread over several workgroups
-// leaves fp32 partials (slot 2 w for a workgroup's first segment, 2 w + 1 for
-// its last) that the merge kernel combines.
+// The 32-key tiles of all decode requests, request after request, form one
+// list cut into units of S tiles; unit v owns tiles [v S, (v + 1) S), and a
+// decode item is a pair of units, one per 4-wave group of the workgroup
+// (the groups run independently, synchronised by LDS arrival counters).  A
+// unit's share splits into segments, one per request it touches.  A segment
+// streams its query block and then its tiles through the group's 2-slot
+// global -> LDS DMA ring, so prefetch runs on across request boundaries and
+// the start-up latency is paid once per unit.  Per tile, wave w scores 16
+// keys over half of the 576 latent dims (the four partial 16 x 16 score
+// blocks meet in LDS), then accumulates its 128-wide slice of the value dims
+// over all 32 keys.  A request spread over several units leaves fp32
+// partials (slot 2 v for unit v's first segment, 2 v + 1 for its last) that
+// the merge kernel combines.
 constexpr int kMaxSeg = kMaxDecSegments;
 constexpr int kXStride = 20;  // floats per head row of a partial score block (16 + pad)
 
@@ -749,7 +720,7 @@ __device__ void decode_wg(const AttnArgs &a, int w, char *smem, int *s_tmp, int 
     TRACE_VAL(8, 1000000ull * 2 + n_units);
 
     uint32_t dma_off[(kTileDma + 1) / 2];
-    tile_dma_offsets<false>(gw, lane, dma_off);
+    tile_dma_offsets(gw, lane, dma_off);
     const uint32_t ring = lds_addr(smem) + grp * kDecGroupBytes;
     float *s_X = reinterpret_cast<float *>(smem + 2 * kDecGroupBytes + grp * kDecXBytes);
     Cursor prod{0, -1}, cons{0, -1};

@@ -496,11 +496,11 @@ __global__ __launch_bounds__(256) void gemm_f32a_kernel(const GemmArgs g) {
 
 // ------------------------------------------------------------------------
 // Multi-head causal attention of one chunk request (see MhaArgs).  Grid
-// (ceil(c / 64), 16 heads), four waves; wave w owns tokens i0 + 16 w .. + 15.
-// Keys stream in tiles of 64 through two LDS stages, register staged one tile
-// ahead.  Four waves rather than eight: with a quarter of the chunk's blocks
-// per head the causal triangle leaves the chip unevenly loaded, and two
-// workgroups a CU hide each other's barriers.  The K tile holds 64 keys x
+// (ceil(c / 128), 16 heads), eight waves; wave w owns tokens i0 + 16 w .. +
+// 15.  Keys stream in tiles of 64 through three LDS stages (120 KB, one
+// workgroup a CU), register staged one tile ahead; the second half of the
+// waves runs its P V one tile behind its scores, so on each SIMD one wave's
+// softmax overlaps the other wave's MFMAs.  The K tile holds 64 keys x
 // 192 fp16 dims (384 bytes a key, 16-byte chunk c at position
 // c ^ ((key >> 1) & 7) inside its group of 8), the V tile 64 keys x 128 fp16
 // dims (chunk c at c ^ (2 (key & 7))); both keep the operand reads below free
