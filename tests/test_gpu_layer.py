@@ -424,3 +424,36 @@ def test_layer_four_chunks_full_size_sampled_rows(route, weights, mha_route):
                   mean_rel=2e-3)
     else:
         _check_mha(got, ref, ex, "layer out (sampled)")
+
+
+def test_layer_multihead_bad_page_id_writes_nothing(weights, mha_route):
+    """A block-table entry outside the pool in a multi-head chunk request
+    (keys 128..191, all new): those new latents are written nowhere (page 0
+    and every other slot keep their bits, no fault), and every other new
+    latent of the step lands in its own slot.  Outputs are not checked."""
+    import torch
+    mha_route(2)
+    wb, wo, dw = weights
+    wl = W.custom([70, 100], [150, 1], page_size=64, seed=53, name="mha_bad_page")
+    b = wl.batch
+    li = wl.layer(0)
+    b.block_table = b.block_table.copy()
+    assert b.block_table.shape[1] >= 4
+    b.block_table[0, 2] = b.num_pages + 3
+    log(f"[gpu] attention layer, multi-head chunk with block-table entry {b.num_pages + 3} of {b.num_pages} pages")
+    hidden = W.random_hidden(b.num_rows, seed=53)
+    db = mla.DeviceBatch.from_batch(b)
+    pool = to_dev(li.pool)
+    out = torch.empty((b.num_rows, 2048), dtype=torch.float32, device="cuda")
+    mla.mla_attention_layer(db, to_dev(hidden), dw, pool, SCALE, out, mla.layer_workspace_for(db))
+    torch.cuda.synchronize()
+    _, lat = _run_pre(b, hidden, dw)
+    expect = li.pool.copy()
+    cu = b.cu_q
+    for r in range(b.num_reqs):
+        for i in range(int(b.q_lens[r])):
+            t = int(b.prefix_lens[r]) + i
+            pg = int(b.block_table[r, t // b.page_size])
+            if 0 <= pg < b.num_pages:
+                expect[pg, t % b.page_size] = lat[cu[r] + i]
+    assert np.array_equal(from_dev_u16(pool), expect)
