@@ -20,25 +20,32 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
+TRACE_LIB = os.path.join(PKG, "libmlastep_trace.so")
+
+
+def build(verbose: bool = False, trace: bool = False) -> str:
+    """Compile the library; trace=True builds the profiling variant
+    (libmlastep_trace.so: the attention kernel also records a per-item
+    timeline, read by timeline.py) instead."""
     objs = []
+    lib = TRACE_LIB if trace else LIB
     for src in SOURCES:
-        obj = os.path.join(CSRC, src + ".o")
-        cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        obj = os.path.join(CSRC, src + (".trace.o" if trace else ".o"))
+        cmd = [HIPCC, *FLAGS, *(["-DMLA_TRACE"] if trace else []), "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)
         objs.append(obj)
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     for o in objs:
         os.remove(o)
-    return LIB
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, trace="--trace" in sys.argv))
