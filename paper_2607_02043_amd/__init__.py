@@ -85,6 +85,11 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_02043_amd/build.py "
                               "(or __graft_entry__.build())")
+        # torch first: the library's HIP runtime dependency then resolves to
+        # the runtime torch has loaded, so the process holds one HIP runtime
+        # (loading ours first would leave torch a second one, and the first
+        # runtime to open the device keeps it)
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         L.mla_abi_version.restype = ctypes.c_int
         L.mla_last_error.restype = ctypes.c_char_p

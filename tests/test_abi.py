@@ -154,3 +154,15 @@ def test_debug_settings_are_checked_on_the_host():
     assert L.mla_debug_set(mla.MLA_DEBUG_WARM_PLAN, 0) == mla.MLA_OK
     assert L.mla_debug_set(mla.MLA_DEBUG_WARM_PLAN, -1) == mla.MLA_OK
     assert L.mla_device_flags(1, None, None) == mla.MLA_ERR_INVALID_ARG
+
+
+def test_library_shares_torch_hip_runtime():
+    """Loading the library first (a fresh process) still leaves one HIP
+    runtime in the process: the one torch loads."""
+    import subprocess
+    import sys
+    code = ("import paper_2607_02043_amd as m; m.lib(); "
+            "print('\\n'.join(sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l})))")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, check=True,
+                         cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__)))).stdout.split()
+    assert len(out) == 1, out
