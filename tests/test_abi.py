@@ -166,3 +166,29 @@ def test_library_shares_torch_hip_runtime():
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, check=True,
                          cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__)))).stdout.split()
     assert len(out) == 1, out
+
+
+def test_binding_constants_match_the_headers():
+    """Every error code, flag, output mode, debug and tuning knob and size the
+    headers define has the same value in the Python binding."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    text = "".join(open(os.path.join(root, "include", h)).read() for h in ("mla_step.h", "mla_layer.h"))
+    values = {name: int(v) for name, v in re.findall(r"\b(MLA_[A-Z0-9_]+)\s*=\s*(-?\d+)", text)}
+    for name, base, shift in re.findall(r"#define\s+(MLA_[A-Z0-9_]+)\s+\(?(\d+)u?(?:\s*<<\s*(\d+))?", text):
+        values[name] = int(base) << int(shift or 0)
+
+    def py_name(name):
+        if name == "MLA_NOALLOC_SCRATCH_BYTES":
+            return "NOALLOC_SCRATCH_BYTES"
+        return name[len("MLA_"):] if name.startswith("MLA_TUNE_") else name
+
+    for must in ("MLA_OK", "MLA_ERR_INVALID_ARG", "MLA_ERR_UNSUPPORTED", "MLA_ERR_WORKSPACE", "MLA_ERR_HIP",
+                 "MLA_OUT_F32", "MLA_OUT_BF16", "MLA_FLAG_BAD_PAGE", "MLA_FLAG_WAIT_EXPIRED", "MLA_DEBUG_CHECK",
+                 "MLA_DEBUG_SPIN_LIMIT", "MLA_DEBUG_CHUNK_KEYS", "MLA_DEBUG_WARM_PLAN", "MLA_TUNE_GEMM_BM",
+                 "MLA_TUNE_GEMM_BN", "MLA_TUNE_GEMM_DEPTH", "MLA_TUNE_MHA_MIN_ROWS", "MLA_TUNE_MHA_PAIRS",
+                 "MLA_NOALLOC_SCRATCH_BYTES"):
+        assert must in values, must
+        assert getattr(mla, py_name(must)) == values[must], (must, getattr(mla, py_name(must)), values[must])
+    for name, v in values.items():  # anything else the binding also names
+        if hasattr(mla, py_name(name)):
+            assert getattr(mla, py_name(name)) == v, name
