@@ -79,3 +79,27 @@ def test_two_streams_at_once():
         assert np.array_equal(par.pool_np(), pool_ref), f"{wl.name}: pool differs from the oracle"
         assert_close(par.out_np(), out_ref, par.lse_np(), lse_ref, what=wl.name)
         assert np.array_equal(par.out_np(), seq.out_np()) and np.array_equal(par.lse_np(), seq.lse_np())
+
+
+def test_serving_sequence_warm_plans_all_rows():
+    """Five consecutive steps of one decode node: decode lengths grow by a
+    token, a request leaves and another joins, the chunk moves to its next
+    chunk.  Each step's batch is close enough to the first one's for the
+    planner's warm start (same split and unit size, counts recomputed); every
+    step matches the oracle on every row."""
+    rng = np.random.default_rng(77)
+    dec = [int(x) for x in rng.integers(200, 3000, 24)]
+    chunk_p, chunk_c = 512, 96
+    for step in range(5):
+        dec = [d + 1 for d in dec]
+        if step == 2:  # one request finishes, another joins
+            dec = dec[1:] + [int(rng.integers(200, 3000))]
+        if step == 3:  # the chunk request moves on
+            chunk_p += chunk_c
+        prefix, qlen = dec + [chunk_p], [1] * len(dec) + [chunk_c]
+        wl = W.custom(prefix, qlen, page_size=16, seed=300 + step, name=f"serving step {step}")
+        log(f"[gpu] serving step {step}: {len(dec)} decodes, chunk {chunk_c} at {chunk_p}")
+        g = run_layer(wl.batch, wl.layer(0), fused=True)
+        pool_ref, out_ref, lse_ref = oracle.step(wl.batch, wl.layer(0), W.SOFTMAX_SCALE)
+        assert np.array_equal(g.pool_np(), pool_ref), f"step {step}: pool differs from the oracle"
+        assert_close(g.out_np(), out_ref, g.lse_np(), lse_ref, what=wl.name)
