@@ -53,11 +53,20 @@ def log(msg):
 
 
 def kernel_source_hash():
+    """Hash of the attention kernels' sources (kernels, host planner, shared
+    header) with comments and blank lines left out, so that a profile taken
+    from them stays valid across comment edits and no longer after any code
+    change."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for f in ("mla_kernels.hip", "mla_api.cpp", "mla_kernels.h"):
-        with open(os.path.join(ROOT, "paper_2607_02043_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2607_02043_amd", "csrc", f)) as fh:
+            text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
+        for line in text.splitlines():
+            code = line.split("//", 1)[0].rstrip()
+            if code:
+                h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 

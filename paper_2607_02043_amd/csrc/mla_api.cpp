@@ -245,8 +245,10 @@ double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
 
 // Work layout of one call.
 //  * chunk requests -> items of (8 tokens) x (a range of keys): every block
-//    of 8 query tokens is cut into nks = ceil((p + c) / ks_chunk) equal key
-//    ranges (multiples of 64 keys), longest rows first; ks_chunk is picked
+//    of 8 query tokens (longest rows first) takes nks = ceil((p + c) /
+//    ks_chunk) queue slots and cuts its causal keys klim into
+//    ceil(klim / ks_chunk) equal ranges (multiples of 64 keys; the other
+//    slots are empty items); ks_chunk is picked
 //    from a closed-form estimate of the finishing time (work spread over the
 //    CUs plus half the largest item) plus the merge of the partials a split
 //    leaves.  Chunk requests are numbered from the last to the first when the
