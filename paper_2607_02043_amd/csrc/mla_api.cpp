@@ -181,12 +181,24 @@ bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long 
 // Loads of the G workgroups after the chunk items, each item taken in queue
 // order by the first free workgroup.
 std::vector<double> simulate_chunks(const std::vector<double> &items, int G) {
-    std::vector<double> heap(G, 0.0);  // min-heap of workgroup finish times
-    auto cmp = [](double x, double y) { return x > y; };
-    for (double c : items) {
-        std::pop_heap(heap.begin(), heap.end(), cmp);
-        heap.back() += c;
-        std::push_heap(heap.begin(), heap.end(), cmp);
+    // the first G items start on idle workgroups; each later one goes to the
+    // workgroup that finishes first (the root of a min-heap, sifted down)
+    const size_t g = (size_t)G, n0 = std::min(g, items.size());
+    std::vector<double> heap(g, 0.0);
+    for (size_t i = 0; i < n0; ++i) heap[i] = items[i];
+    std::make_heap(heap.begin(), heap.end(), [](double x, double y) { return x > y; });
+    for (size_t i = n0; i < items.size(); ++i) {
+        const double v = heap[0] + items[i];
+        size_t k = 0;
+        for (;;) {
+            size_t c = 2 * k + 1;
+            if (c >= g) break;
+            if (c + 1 < g && heap[c + 1] < heap[c]) ++c;
+            if (heap[c] >= v) break;
+            heap[k] = heap[c];
+            k = c;
+        }
+        heap[k] = v;
     }
     return heap;
 }
@@ -208,14 +220,10 @@ std::vector<LoadRun> load_runs(std::vector<double> loads) {
     return runs;
 }
 
-// Finishing time when n equal units of cost u follow, each taken by the first
-// free workgroup, on top of the workgroup loads.  The last unit starts at the
-// smallest t with sum over loads L < t of ceil((t - L) / u) >= n; the water
-// level of the n units over the least-loaded workgroups bounds that t to
-// [level - u, level].
-double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
-    const double mx = runs.empty() ? 0.0 : runs.back().load;
-    if (n <= 0 || runs.empty()) return mx;
+// Water level of n units of cost u poured onto the workgroup loads: the t
+// with sum over loads L < t of (t - L) = n u.  No schedule of the units
+// finishes before it.
+double water_level(const std::vector<LoadRun> &runs, long long n, double u) {
     double sum = 0.0, level = 0.0;
     long long cnt = 0;
     for (size_t k = 0; k < runs.size(); ++k) {
@@ -224,21 +232,40 @@ double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
         level = (sum + (double)n * u) / (double)cnt;
         if (k + 1 == runs.size() || level <= runs[k + 1].load) break;
     }
-    auto started = [&](double t) {
-        long long c = 0;
-        for (const LoadRun &r : runs) {
-            if (r.load >= t) break;
-            c += r.count * (long long)std::ceil((t - r.load) / u - 1e-9);
-        }
-        return c;
+    return level;
+}
+
+// Finishing time when n equal units of cost u follow, each taken by the first
+// free workgroup, on top of the workgroup loads.  The last unit starts at the
+// smallest t with sum over loads L < t of ceil((t - L) / u) >= n, which lies
+// in [level - u, level].  That sum is a step function of t: a run of loads L
+// has started ceil((lo - L) / u) units by lo and one more just after each
+// L + j u inside the interval (at most two such steps, the interval being
+// one unit long), so t is found exactly from the sorted steps.
+double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
+    const double mx = runs.empty() ? 0.0 : runs.back().load;
+    if (n <= 0 || runs.empty()) return mx;
+    const double level = water_level(runs, n, u);
+    const double lo = std::max(0.0, level - u), hi = level;
+    struct Step {
+        double t;
+        long long count;
     };
-    double lo = std::max(0.0, level - u), hi = level;
-    for (int it = 0; it < 10; ++it) {
-        const double mid = 0.5 * (lo + hi);
-        if (started(mid) >= n)
-            hi = mid;
-        else
-            lo = mid;
+    thread_local std::vector<Step> steps;
+    steps.clear();
+    long long base = 0;  // units started by lo
+    for (const LoadRun &r : runs) {
+        if (r.load >= hi) break;
+        const long long j = r.load < lo ? (long long)std::ceil((lo - r.load) / u - 1e-9) : 0;
+        base += r.count * j;
+        for (double t = r.load + (double)j * u; t < hi; t += u) steps.push_back(Step{t, r.count});
+    }
+    if (base >= n) return std::max(mx, lo + u);
+    std::sort(steps.begin(), steps.end(), [](const Step &x, const Step &y) { return x.t < y.t; });
+    long long c = base;
+    for (const Step &st : steps) {
+        c += st.count;
+        if (c >= n) return std::max(mx, st.t + u);
     }
     return std::max(mx, hi + u);
 }
@@ -349,15 +376,16 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         items.clear();
         for (size_t i = 0; i < chunks.size(); ++i) {
             const auto &pc = chunks[rev ? chunks.size() - 1 - i : i];
-            const long long p = pc.first, c = pc.second;
-            const long long nrb = ceil_div_ll(c, BM), nks = ceil_div_ll(p + c, ks);
-            for (long long rb = nrb - 1; rb >= 0; --rb) {
-                const long long klim = p + std::min(c, (rb + 1) * BM);
-                const long long kp = ceil_div_ll(ceil_div_ll(klim, ceil_div_ll(klim, ks)), 64) * 64;
-                for (long long j = 0; j < nks; ++j) {
-                    const long long keys = std::min(kp, klim - j * kp);
-                    items.push_back(keys > 0 ? kChunkItemUs + kChunkTileUs * (double)ceil_div_ll(keys, KT)
-                                             : kEmptyItemUs);
+            // 32-bit arithmetic: keys per request stay below 2^30
+            const uint32_t p = (uint32_t)pc.first, c = (uint32_t)pc.second, k32 = (uint32_t)ks;
+            const uint32_t nrb = (c + BM - 1) / BM, nks = (p + c + k32 - 1) / k32;
+            for (uint32_t rb = nrb; rb-- > 0;) {
+                const uint32_t klim = p + std::min(c, (rb + 1) * (uint32_t)BM);
+                const uint32_t nr = (klim + k32 - 1) / k32, kp = ((klim + nr - 1) / nr + 63) / 64 * 64;
+                for (uint32_t j = 0; j < nks; ++j) {
+                    const uint32_t k0 = j * kp;
+                    items.push_back(k0 < klim ? kChunkItemUs + kChunkTileUs * (double)((std::min(kp, klim - k0) + KT - 1) / KT)
+                                              : kEmptyItemUs);
                 }
             }
         }
@@ -381,9 +409,13 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     // Finishing time of the decode units (equal cost u) poured onto the
     // workgroup loads left by the chunk items, plus the merge of the requests
     // they split.
-    auto with_decode = [&](const std::vector<LoadRun> &loads, long long U) {
-        const long long n = ceil_div_ll(ceil_div_ll(dec_total, U), 2);  // work items: pairs of units
-        const double u = kDecUnitUs + kDecTileUs * (double)U;
+    // Per unit size U: the work items (pairs of units), a unit's cost and the
+    // merge of the rows it splits.
+    struct DecFill {
+        long long n;
+        double u, merge_us;
+    };
+    auto dec_fill = [&](long long U) {
         long long split_parts = 0;
         const uint32_t u32 = (uint32_t)U;  // tile indices stay below 2^30
         for (const DecReq &d : dec) {
@@ -391,7 +423,8 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             const uint32_t parts = l / u32 - f / u32 + 1;
             if (parts > 1) split_parts += parts + 1;
         }
-        return fill_units(loads, n, u) + (double)split_parts * row_bytes / (kMergeGBs * 1e3);
+        return DecFill{ceil_div_ll(ceil_div_ll(dec_total, U), 2), kDecUnitUs + kDecTileUs * (double)U,
+                       (double)split_parts * row_bytes / (kMergeGBs * 1e3)};
     };
 
     // Key split: the closed-form estimate keeps the best candidate (and the
@@ -447,7 +480,12 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                 continue;
             }
             for (long long U : units) {
-                const double t = with_decode(loads, U) + cd.merge_us;
+                const DecFill df = dec_fill(U);
+                // the water level bounds the finish from below: skip a size
+                // that cannot beat the best one
+                const double lower = std::max(loads.back().load, water_level(loads, df.n, df.u));
+                if (lower + df.merge_us + cd.merge_us >= best) continue;
+                const double t = fill_units(loads, df.n, df.u) + df.merge_us + cd.merge_us;
                 if (t < best) {
                     best = t;
                     ks_best = cd.ks;
