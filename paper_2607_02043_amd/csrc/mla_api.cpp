@@ -235,37 +235,74 @@ double water_level(const std::vector<LoadRun> &runs, long long n, double u) {
     return level;
 }
 
+// A lower bound on the finishing time below.  A workgroup with load L has
+// started at most (t - L) / u + 1 units by t >= L, so the last of the n units
+// cannot start before the t at which that bound, summed over the loads, first
+// reaches n (found segment by segment between the sorted loads).
+double fill_bound(const std::vector<LoadRun> &runs, long long n, double u) {
+    if (n <= 0 || runs.empty()) return runs.empty() ? 0.0 : runs.back().load;
+    double sum = 0.0;
+    long long cnt = 0;
+    for (size_t k = 0;; ++k) {
+        sum += runs[k].load * (double)runs[k].count;
+        cnt += runs[k].count;
+        const double t = std::max(runs[k].load, (sum + (double)(n - cnt) * u) / (double)cnt);
+        if (k + 1 == runs.size() || t <= runs[k + 1].load) return std::max(runs.back().load, t + u);
+    }
+}
+
 // Finishing time when n equal units of cost u follow, each taken by the first
 // free workgroup, on top of the workgroup loads.  The last unit starts at the
 // smallest t with sum over loads L < t of ceil((t - L) / u) >= n, which lies
 // in [level - u, level].  That sum is a step function of t: a run of loads L
 // has started ceil((lo - L) / u) units by lo and one more just after each
 // L + j u inside the interval (at most two such steps, the interval being
-// one unit long), so t is found exactly from the sorted steps.
+// one unit long), so t is the step at which the count reaches n.
 double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
     const double mx = runs.empty() ? 0.0 : runs.back().load;
     if (n <= 0 || runs.empty()) return mx;
     const double level = water_level(runs, n, u);
-    const double lo = std::max(0.0, level - u), hi = level;
+    const double lo = std::max(0.0, level - u), hi = level, inv_u = 1.0 / u;
     struct Step {
         double t;
         long long count;
+        int bucket;
     };
+    // the steps are counted in equal buckets of [lo, hi) (bucket order is t
+    // order); only the bucket where the count reaches n is sorted
+    constexpr int kBuckets = 64;
+    const double scale = hi > lo ? kBuckets / (hi - lo) : 0.0;
+    long long hist[kBuckets] = {};
     thread_local std::vector<Step> steps;
     steps.clear();
     long long base = 0;  // units started by lo
     for (const LoadRun &r : runs) {
         if (r.load >= hi) break;
-        const long long j = r.load < lo ? (long long)std::ceil((lo - r.load) / u - 1e-9) : 0;
+        long long j = 0;  // ceil((lo - L) / u), less a rounding margin
+        if (r.load < lo) {
+            const double x = (lo - r.load) * inv_u - 1e-9;
+            j = (long long)x;
+            j += (double)j < x;
+        }
         base += r.count * j;
-        for (double t = r.load + (double)j * u; t < hi; t += u) steps.push_back(Step{t, r.count});
+        for (double t = r.load + (double)j * u; t < hi; t += u) {
+            const int k = std::min(kBuckets - 1, std::max(0, (int)((t - lo) * scale)));
+            hist[k] += r.count;
+            steps.push_back(Step{t, r.count, k});
+        }
     }
     if (base >= n) return std::max(mx, lo + u);
-    std::sort(steps.begin(), steps.end(), [](const Step &x, const Step &y) { return x.t < y.t; });
-    long long c = base;
-    for (const Step &st : steps) {
-        c += st.count;
-        if (c >= n) return std::max(mx, st.t + u);
+    // the smallest step t with base + (units of the steps <= t) >= n
+    long long need = n - base;
+    int kb = 0;
+    while (kb < kBuckets && need > hist[kb]) need -= hist[kb++];
+    if (kb < kBuckets) {
+        size_t m = 0;
+        for (const Step &st : steps)
+            if (st.bucket == kb) steps[m++] = st;
+        std::sort(steps.begin(), steps.begin() + (std::ptrdiff_t)m, [](const Step &x, const Step &y) { return x.t < y.t; });
+        for (size_t i = 0; i < m; ++i)
+            if ((need -= steps[i].count) <= 0) return std::max(mx, steps[i].t + u);
     }
     return std::max(mx, hi + u);
 }
@@ -382,11 +419,11 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             for (uint32_t rb = nrb; rb-- > 0;) {
                 const uint32_t klim = p + std::min(c, (rb + 1) * (uint32_t)BM);
                 const uint32_t nr = (klim + k32 - 1) / k32, kp = ((klim + nr - 1) / nr + 63) / 64 * 64;
-                for (uint32_t j = 0; j < nks; ++j) {
-                    const uint32_t k0 = j * kp;
-                    items.push_back(k0 < klim ? kChunkItemUs + kChunkTileUs * (double)((std::min(kp, klim - k0) + KT - 1) / KT)
-                                              : kEmptyItemUs);
-                }
+                // ranges of kp keys, the last one shorter, then empty slots
+                const uint32_t full = klim / kp, rest = klim - full * kp;
+                items.insert(items.end(), full, kChunkItemUs + kChunkTileUs * (double)((kp + KT - 1) / KT));
+                if (rest > 0) items.push_back(kChunkItemUs + kChunkTileUs * (double)((rest + KT - 1) / KT));
+                items.insert(items.end(), nks - full - (rest > 0), kEmptyItemUs);
             }
         }
     };
@@ -406,11 +443,8 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         if (units.empty())
             return fail(MLA_ERR_UNSUPPORTED, "decode work does not fit the per-unit segment / page limits");
     }
-    // Finishing time of the decode units (equal cost u) poured onto the
-    // workgroup loads left by the chunk items, plus the merge of the requests
-    // they split.
     // Per unit size U: the work items (pairs of units), a unit's cost and the
-    // merge of the rows it splits.
+    // merge of the request rows it splits.
     struct DecFill {
         long long n;
         double u, merge_us;
@@ -418,10 +452,20 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     auto dec_fill = [&](long long U) {
         long long split_parts = 0;
         const uint32_t u32 = (uint32_t)U;  // tile indices stay below 2^30
+        const double inv = 1.0 / (double)U;
+        auto unit_of = [&](uint32_t x) {  // x / U: the rounded product, corrected
+            uint32_t q = (uint32_t)((double)x * inv);
+            q -= q * u32 > x;
+            q += (q + 1) * u32 <= x;
+            return q;
+        };
+        // the requests' tiles are contiguous: each one starts in the unit of
+        // its predecessor's last tile or in the next one
+        uint32_t first = 0;  // unit of the request's first tile
         for (const DecReq &d : dec) {
-            const uint32_t f = (uint32_t)d.first_tile, l = (uint32_t)(d.first_tile + d.tiles - 1);
-            const uint32_t parts = l / u32 - f / u32 + 1;
-            if (parts > 1) split_parts += parts + 1;
+            const uint32_t l = (uint32_t)(d.first_tile + d.tiles - 1), last = unit_of(l);
+            if (last > first) split_parts += last - first + 2;  // rows moved: the parts, the merged row
+            first = last + ((last + 1) * u32 == l + 1);
         }
         return DecFill{ceil_div_ll(ceil_div_ll(dec_total, U), 2), kDecUnitUs + kDecTileUs * (double)U,
                        (double)split_parts * row_bytes / (kMergeGBs * 1e3)};
@@ -463,9 +507,14 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         } else {
             cands.push_back(Cand{cap, 0.0, 0.0});
         }
+        std::vector<DecFill> fills;
+        for (long long U : units) fills.push_back(dec_fill(U));
         double best = 1e300;
+        size_t best_key = 0;
         std::vector<double> items;
-        for (const Cand &cd : cands) {
+        std::vector<std::pair<double, size_t>> order;
+        for (size_t ci = 0; ci < cands.size(); ++ci) {
+            const Cand &cd = cands[ci];
             std::vector<LoadRun> loads{LoadRun{0.0, (long long)G}};
             if (!chunks.empty()) {
                 chunk_items(cd.ks, rev, items);
@@ -479,17 +528,25 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                 }
                 continue;
             }
-            for (long long U : units) {
-                const DecFill df = dec_fill(U);
-                // the water level bounds the finish from below: skip a size
-                // that cannot beat the best one
-                const double lower = std::max(loads.back().load, water_level(loads, df.n, df.u));
-                if (lower + df.merge_us + cd.merge_us >= best) continue;
+            // sizes are tried by a lower bound on their finish, up to the
+            // first that cannot beat the best one; among equal finishes the
+            // earlier candidate and size win
+            order.clear();
+            for (size_t ui = 0; ui < units.size(); ++ui) {
+                const DecFill &df = fills[ui];
+                order.emplace_back(fill_bound(loads, df.n, df.u) + df.merge_us + cd.merge_us, ui);
+            }
+            std::sort(order.begin(), order.end());
+            for (const auto &o : order) {
+                if (o.first > best) break;
+                const DecFill &df = fills[o.second];
                 const double t = fill_units(loads, df.n, df.u) + df.merge_us + cd.merge_us;
-                if (t < best) {
+                const size_t key = ci * units.size() + o.second;
+                if (t < best || (t == best && key < best_key)) {
                     best = t;
+                    best_key = key;
                     ks_best = cd.ks;
-                    U_best = U;
+                    U_best = units[o.second];
                 }
             }
         }

@@ -12,6 +12,9 @@
 // mixed_step_attn entry point with fake device pointers and a workspace of
 // <bytes> bytes and prints "rc <status> <needed bytes> <message>"; "na 0 ..."
 // calls mixed_step_noalloc the same way (its scratch stubbed by a fake address).
+// A line "cm <seed> <cases>" checks the planner's cost model on random
+// workgroup loads against brute force and prints "cm ok <cases>" or the first
+// case that fails.
 #include <hip/hip_runtime.h>
 
 static hipError_t harness_get_device(int *d) {
@@ -30,6 +33,8 @@ static hipError_t harness_get_attribute(int *v, hipDeviceAttribute_t, int) {
 
 #include <chrono>
 #include <iostream>
+#include <queue>
+#include <random>
 #include <sstream>
 #include <string>
 
@@ -48,6 +53,40 @@ hipError_t noalloc_scratch(void **ptr) {
 }
 }  // namespace mla
 
+// Each item or unit to the workgroup that is free first, one at a time; the
+// finishing time of the last one (or the largest load).
+static std::vector<double> brute_schedule(std::vector<double> loads, const std::vector<double> &items) {
+    for (double c : items) *std::min_element(loads.begin(), loads.end()) += c;
+    return loads;
+}
+
+static std::string cost_model_check(unsigned seed, int cases) {
+    std::mt19937 g(seed);
+    for (int k = 0; k < cases; ++k) {
+        const int G = 1 + (int)(g() % 300);
+        std::vector<double> items(g() % 1500);
+        for (double &c : items) c = g() % 4 == 0 ? 1.5 : 14.0 + 2.2 * (double)(1 + g() % 40);
+        // the chunk queue: same loads as one at a time to the least loaded
+        std::vector<double> sim = simulate_chunks(items, G), ref = brute_schedule(std::vector<double>(G, 0.0), items);
+        std::sort(sim.begin(), sim.end());
+        std::sort(ref.begin(), ref.end());
+        if (sim != ref) return "simulate_chunks differs, case " + std::to_string(k);
+        // decode units after it: exact fill, its bounds
+        const long long n = 1 + (long long)(g() % 3000);
+        const double u = 5.5 + 3.5 * (double)(1 + g() % 64);
+        const std::vector<LoadRun> runs = load_runs(sim);
+        std::vector<double> ld = brute_schedule(sim, std::vector<double>((size_t)n, u));
+        const double want = *std::max_element(ld.begin(), ld.end());
+        const double got = fill_units(runs, n, u), lower = fill_bound(runs, n, u);
+        const double level = std::max(runs.back().load, water_level(runs, n, u));
+        if (std::abs(got - want) > 1e-9 * want)
+            return "fill_units " + std::to_string(got) + " vs " + std::to_string(want) + ", case " + std::to_string(k);
+        if (lower > got * (1 + 1e-12) || level > got * (1 + 1e-12))
+            return "a lower bound exceeds the fill, case " + std::to_string(k);
+    }
+    return "ok " + std::to_string(cases);
+}
+
 int main() {
     // PLAN_ROUTE="min_rows pair_keys": leave the chunk requests that this
     // route sends to the multi-head path out of the plan
@@ -63,6 +102,14 @@ int main() {
     if (const char *e = std::getenv("PLAN_CHUNK_KEYS")) mla_debug_set(MLA_DEBUG_CHUNK_KEYS, std::atoi(e));
     std::string line;
     while (std::getline(std::cin, line)) {
+        if (line.rfind("cm ", 0) == 0) {
+            std::istringstream in(line.substr(3));
+            unsigned seed = 0;
+            int cases = 0;
+            in >> seed >> cases;
+            std::cout << "cm " << cost_model_check(seed, cases) << "\n";
+            continue;
+        }
         const bool noalloc = line.rfind("na ", 0) == 0;
         if (line.rfind("ws ", 0) == 0 || noalloc) {
             std::istringstream in(line.substr(3));

@@ -279,3 +279,15 @@ def test_serving_sequence_plans_warm_and_stays_valid(harness):
     assert len(warm) >= 30
     assert all(d["ks"] == plans[0]["ks"] and d["U"] == plans[0]["U"] for d in warm)
     assert float(np.median([d["us"] for d in warm])) < 50.0
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_cost_model_matches_brute_force(harness, seed):
+    """The planner's queue model against one-at-a-time scheduling on random
+    workgroup loads: the chunk-queue simulation gives the same loads, the
+    decode fill the same finishing time, and both of its lower bounds (the
+    water level, the per-workgroup bound) stay at or below it."""
+    out = subprocess.run([harness], input=f"cm {seed} 1500\n", capture_output=True, text=True,
+                         check=True).stdout.split()
+    assert out == ["cm", "ok", "1500"], out
+
