@@ -154,10 +154,19 @@ def test_plans_of_the_benchmark_workloads(harness):
     wls = [W.config(1), W.config(2), W.config(3), W.config(4, chunk=0), W.config(4, chunk=2048), W.config(5)]
     batches = [(256, w.batch.page_size, [int(x) for x in w.batch.q_lens], [int(x) for x in w.batch.prefix_lens])
                for w in wls]
-    res = plan(harness, batches)
-    for b, d in zip(batches, res):
-        check_plan(b, d)
-        assert d["us"] < 5000, d["us"]  # a plan is recomputed whenever the lengths change
+    reps = 15
+    res = plan(harness, [b for b in batches for _ in range(reps)])
+    for i, b in enumerate(batches):
+        runs = res[i * reps:(i + 1) * reps]
+        check_plan(b, runs[0])
+        assert all({k: v for k, v in d.items() if k != "us"} == {k: v for k, v in runs[0].items() if k != "us"}
+                   for d in runs), "the planner is not deterministic"
+        # a full plan (a batch shape not seen before) takes some 5-25 us on
+        # one core of a current server CPU; the bound leaves room for a busy
+        # or slower host
+        us = float(np.median([d["us"] for d in runs]))
+        assert us < 150.0, (i, us)
+    res = res[::reps]
     # decode-only: one item of two equal units per CU
     assert res[3]["n_chunk_items"] == 0 and res[3]["n_dec_items"] == 256
 
