@@ -410,20 +410,36 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     // from the last, blocks longest first, nks ranges per block; an empty
     // range still takes a queue slot), as costs.
     auto chunk_items = [&](long long ks, bool rev, std::vector<double> &items) {
-        items.clear();
+        // 32-bit arithmetic: keys per request stay below 2^30
+        const uint32_t k32 = (uint32_t)ks;
+        size_t n = 0;
+        for (const auto &pc : chunks)
+            n += (size_t)(((uint32_t)pc.second + BM - 1) / BM) * (((uint32_t)(pc.first + pc.second) + k32 - 1) / k32);
+        items.resize(n);
+        double *out = items.data();
         for (size_t i = 0; i < chunks.size(); ++i) {
             const auto &pc = chunks[rev ? chunks.size() - 1 - i : i];
-            // 32-bit arithmetic: keys per request stay below 2^30
-            const uint32_t p = (uint32_t)pc.first, c = (uint32_t)pc.second, k32 = (uint32_t)ks;
+            const uint32_t p = (uint32_t)pc.first, c = (uint32_t)pc.second;
             const uint32_t nrb = (c + BM - 1) / BM, nks = (p + c + k32 - 1) / k32;
+            // klim falls by at most BM keys a block, so nr = ceil(klim / ks)
+            // and q = ceil(klim / (64 nr)) (kp = 64 q) are stepped down
+            // rather than divided out again
+            uint32_t nr = 0, q = 0;
             for (uint32_t rb = nrb; rb-- > 0;) {
                 const uint32_t klim = p + std::min(c, (rb + 1) * (uint32_t)BM);
-                const uint32_t nr = (klim + k32 - 1) / k32, kp = ((klim + nr - 1) / nr + 63) / 64 * 64;
+                if (nr == 0 || (nr - 1) * k32 >= klim) {
+                    nr = (klim + k32 - 1) / k32;
+                    q = (klim + 64 * nr - 1) / (64 * nr);
+                }
+                while ((q - 1) * 64 * nr >= klim) --q;
+                const uint32_t kp = 64 * q;
                 // ranges of kp keys, the last one shorter, then empty slots
-                const uint32_t full = klim / kp, rest = klim - full * kp;
-                items.insert(items.end(), full, kChunkItemUs + kChunkTileUs * (double)((kp + KT - 1) / KT));
-                if (rest > 0) items.push_back(kChunkItemUs + kChunkTileUs * (double)((rest + KT - 1) / KT));
-                items.insert(items.end(), nks - full - (rest > 0), kEmptyItemUs);
+                uint32_t full = nr;  // floor(klim / kp): nr, or nr - 1 when ks is a multiple of 64
+                while (full * kp > klim) --full;
+                const uint32_t rest = klim - full * kp;
+                out = std::fill_n(out, full, kChunkItemUs + kChunkTileUs * (double)((kp + KT - 1) / KT));
+                if (rest > 0) *out++ = kChunkItemUs + kChunkTileUs * (double)((rest + KT - 1) / KT);
+                out = std::fill_n(out, nks - full - (rest > 0), kEmptyItemUs);
             }
         }
     };
@@ -452,10 +468,9 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     auto dec_fill = [&](long long U) {
         long long split_parts = 0;
         const uint32_t u32 = (uint32_t)U;  // tile indices stay below 2^30
-        const double inv = 1.0 / (double)U;
-        auto unit_of = [&](uint32_t x) {  // x / U: the rounded product, corrected
-            uint32_t q = (uint32_t)((double)x * inv);
-            q -= q * u32 > x;
+        const uint64_t inv = (1ull << 32) / u32;
+        auto unit_of = [&](uint32_t x) {  // x / U: x floor(2^32 / U) / 2^32 is short by at most one
+            uint32_t q = (uint32_t)(((uint64_t)x * inv) >> 32);
             q += (q + 1) * u32 <= x;
             return q;
         };
@@ -508,7 +523,12 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             cands.push_back(Cand{cap, 0.0, 0.0});
         }
         std::vector<DecFill> fills;
-        for (long long U : units) fills.push_back(dec_fill(U));
+        double dec_min = dec_total > 0 ? 1e300 : 0.0, merge_min = dec_total > 0 ? 1e300 : 0.0;
+        for (long long U : units) {
+            fills.push_back(dec_fill(U));
+            dec_min = std::min(dec_min, (double)fills.back().n * fills.back().u);
+            merge_min = std::min(merge_min, fills.back().merge_us);
+        }
         double best = 1e300;
         size_t best_key = 0;
         std::vector<double> items;
@@ -518,6 +538,19 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             std::vector<LoadRun> loads{LoadRun{0.0, (long long)G}};
             if (!chunks.empty()) {
                 chunk_items(cd.ks, rev, items);
+                if (ci > 0) {
+                    // the runner-up finishes no earlier than its largest item
+                    // or its average load per workgroup (the least decode
+                    // work and merge of any unit size added; a shade less,
+                    // for rounding): not simulated if that cannot win
+                    double sum = 0.0, largest = 0.0;
+                    for (double c : items) {
+                        sum += c;
+                        largest = std::max(largest, c);
+                    }
+                    const double lower = std::max(largest, (sum + dec_min) / (double)G) + cd.merge_us + merge_min;
+                    if (lower * (1.0 - 1e-9) >= best) continue;
+                }
                 loads = load_runs(simulate_chunks(items, G));
             }
             if (dec_total == 0) {
