@@ -257,6 +257,14 @@ def main():
                                                "page 64", "points": curve}
         sub["plan_inclusive"] = [plan_inclusive(args, W.config(idx), n_sub, w_sub) for idx in (2, args.config)
                                  if idx in (2, 3, 5)]
+        # host planning alone for the other workloads (new batch every step)
+        plans = {}
+        for name, wi in (("workload_3", W.config(3)), ("workload_4_c2048", W.config(4, chunk=2048)),
+                         ("workload_4_c4096", W.config(4, chunk=4096))):
+            cold, warm = host_plan_times(advancing_batches(wi, 25))
+            plans[name] = {"workload": wi.name, "host_plan_us": warm, "host_plan_full_us": cold}
+            log(f"[bench] host plan {name}: {warm['median']:.1f} us warm, {cold['median']:.1f} us in full")
+        sub["host_plan"] = plans
         result["sub"] = sub
 
     if not args.no_cpu_baseline:
@@ -513,6 +521,49 @@ def measure(args, wl, steps, warmup, calib=0, batches=None):
             "n_rot": n_rot}
 
 
+def advancing_batches(wl, n):
+    """n device batches of the workload whose decode lengths grow by one token
+    per step: step k uses decode prefixes p - (n - 1) + k (clipped at 0), where
+    p are the workload's, so every appended slot lies inside the workload's
+    block table and pool."""
+    import torch
+
+    import paper_2607_02043_amd as mla
+
+    dev = torch.device("cuda:0")
+    b = wl.batch
+    dec = b.q_lens == 1
+    batches = []
+    for k in range(n):
+        p = b.prefix_lens.astype(np.int64).copy()
+        p[dec] = np.maximum(0, p[dec] - (n - 1) + k)
+        batches.append(mla.DeviceBatch(b.q_lens, p.astype(np.int32), b.block_table, b.page_size, b.num_pages,
+                                       device=dev))
+    return batches
+
+
+def host_plan_times(batches):
+    """Host time of the checks and the planning per new batch (the workspace
+    query plans the batch): every batch planned in full, then warm-started from
+    the last full plan as a serving loop does.  Median and min over 5 passes."""
+    import paper_2607_02043_amd as mla
+
+    def plan_time(warm):
+        mla.debug_set(mla.MLA_DEBUG_WARM_PLAN, 1 if warm else 0)
+        try:
+            reps = []
+            for _ in range(5):  # every call meets a new batch: the exact-lengths cache never hits
+                t = time.perf_counter()
+                for db in batches:
+                    mla.mixed_step_workspace_bytes(db)
+                reps.append((time.perf_counter() - t) / len(batches) * 1e6)
+        finally:
+            mla.debug_set(mla.MLA_DEBUG_WARM_PLAN, -1)
+        return {"median": round(float(np.median(reps)), 2), "min": round(float(np.min(reps)), 2)}
+
+    return plan_time(False), plan_time(True)
+
+
 def plan_inclusive(args, wl, steps, warmup):
     """Steps whose decode lengths grow by one token per step, as in serving:
     every step is a new batch, so the host plans every step (a plan is reused
@@ -523,35 +574,8 @@ def plan_inclusive(args, wl, steps, warmup):
     launches overlap the GPU work of the steps before) and the host time of
     the checks and the planning alone, per new batch: as served (warm-started
     from the last full plan) and with every batch planned in full."""
-    import torch
-
-    import paper_2607_02043_amd as mla
-
-    dev = torch.device("cuda:0")
-    b = wl.batch
-    n = steps + warmup
-    dec = b.q_lens == 1
-    batches = []
-    for k in range(n):
-        p = b.prefix_lens.astype(np.int64).copy()
-        p[dec] = np.maximum(0, p[dec] - (n - 1) + k)
-        batches.append(mla.DeviceBatch(b.q_lens, p.astype(np.int32), b.block_table, b.page_size, b.num_pages,
-                                       device=dev))
-    def plan_time(warm):
-        mla.debug_set(mla.MLA_DEBUG_WARM_PLAN, 1 if warm else 0)
-        try:
-            reps = []
-            for _ in range(5):  # every call meets a new batch: the exact-lengths cache never hits
-                t = time.perf_counter()
-                for db in batches:
-                    mla.mixed_step_workspace_bytes(db)
-                reps.append((time.perf_counter() - t) / n * 1e6)
-        finally:
-            mla.debug_set(mla.MLA_DEBUG_WARM_PLAN, -1)
-        return {"median": round(float(np.median(reps)), 2), "min": round(float(np.min(reps)), 2)}
-
-    cold = plan_time(False)
-    warm = plan_time(True)
+    batches = advancing_batches(wl, steps + warmup)
+    cold, warm = host_plan_times(batches)
     m = measure(args, wl, steps, warmup, batches=batches)
     s = summary(wl, m)
     s["workload"] = wl.name + "; decode lengths +1 per step"
