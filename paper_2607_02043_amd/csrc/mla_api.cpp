@@ -203,10 +203,13 @@ std::vector<double> simulate_chunks(const std::vector<double> &items, int G) {
     return heap;
 }
 
-// Workgroup loads as runs of equal values, ascending.
+// Workgroup loads as runs of equal values, ascending, with the sum and the
+// count of the loads up to and including each run.
 struct LoadRun {
     double load;
     long long count;
+    double sum_to;
+    long long count_to;
 };
 std::vector<LoadRun> load_runs(std::vector<double> loads) {
     std::sort(loads.begin(), loads.end());
@@ -215,40 +218,56 @@ std::vector<LoadRun> load_runs(std::vector<double> loads) {
         if (!runs.empty() && runs.back().load == L)
             ++runs.back().count;
         else
-            runs.push_back(LoadRun{L, 1});
+            runs.push_back(LoadRun{L, 1, 0.0, 0});
+    }
+    double sum = 0.0;
+    long long cnt = 0;
+    for (LoadRun &r : runs) {
+        sum += r.load * (double)r.count;
+        cnt += r.count;
+        r.sum_to = sum;
+        r.count_to = cnt;
     }
     return runs;
+}
+
+// The first run k at which pred(k) holds, pred being false up to some run and
+// true from there on (the last run if it never holds): a binary search.
+template <typename Pred>
+size_t first_run(const std::vector<LoadRun> &runs, Pred pred) {
+    size_t lo = 0, hi = runs.size() - 1;
+    while (lo < hi) {
+        const size_t mid = (lo + hi) / 2;
+        if (pred(mid))
+            hi = mid;
+        else
+            lo = mid + 1;
+    }
+    return lo;
 }
 
 // Water level of n units of cost u poured onto the workgroup loads: the t
 // with sum over loads L < t of (t - L) = n u.  No schedule of the units
 // finishes before it.
 double water_level(const std::vector<LoadRun> &runs, long long n, double u) {
-    double sum = 0.0, level = 0.0;
-    long long cnt = 0;
-    for (size_t k = 0; k < runs.size(); ++k) {
-        sum += runs[k].load * (double)runs[k].count;
-        cnt += runs[k].count;
-        level = (sum + (double)n * u) / (double)cnt;
-        if (k + 1 == runs.size() || level <= runs[k + 1].load) break;
-    }
-    return level;
+    if (runs.empty()) return 0.0;
+    // the level over the loads up to run k, which only falls below the next
+    // load once k reaches the answer
+    auto level = [&](size_t k) { return (runs[k].sum_to + (double)n * u) / (double)runs[k].count_to; };
+    return level(first_run(runs, [&](size_t k) { return k + 1 == runs.size() || level(k) <= runs[k + 1].load; }));
 }
 
 // A lower bound on the finishing time below.  A workgroup with load L has
 // started at most (t - L) / u + 1 units by t >= L, so the last of the n units
 // cannot start before the t at which that bound, summed over the loads, first
-// reaches n (found segment by segment between the sorted loads).
+// reaches n (searched for over the segments between the sorted loads).
 double fill_bound(const std::vector<LoadRun> &runs, long long n, double u) {
     if (n <= 0 || runs.empty()) return runs.empty() ? 0.0 : runs.back().load;
-    double sum = 0.0;
-    long long cnt = 0;
-    for (size_t k = 0;; ++k) {
-        sum += runs[k].load * (double)runs[k].count;
-        cnt += runs[k].count;
-        const double t = std::max(runs[k].load, (sum + (double)(n - cnt) * u) / (double)cnt);
-        if (k + 1 == runs.size() || t <= runs[k + 1].load) return std::max(runs.back().load, t + u);
-    }
+    auto start = [&](size_t k) {
+        return std::max(runs[k].load, (runs[k].sum_to + (double)(n - runs[k].count_to) * u) / (double)runs[k].count_to);
+    };
+    const size_t k = first_run(runs, [&](size_t k) { return k + 1 == runs.size() || start(k) <= runs[k + 1].load; });
+    return std::max(runs.back().load, start(k) + u);
 }
 
 // Finishing time when n equal units of cost u follow, each taken by the first
@@ -535,7 +554,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         std::vector<std::pair<double, size_t>> order;
         for (size_t ci = 0; ci < cands.size(); ++ci) {
             const Cand &cd = cands[ci];
-            std::vector<LoadRun> loads{LoadRun{0.0, (long long)G}};
+            std::vector<LoadRun> loads{LoadRun{0.0, (long long)G, 0.0, (long long)G}};
             if (!chunks.empty()) {
                 chunk_items(cd.ks, rev, items);
                 if (ci > 0) {
