@@ -52,7 +52,7 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
+def kernel_source_hash(root=ROOT):
     """Hash of the attention kernels' sources (kernels, host planner, shared
     header) with comments and blank lines left out, so that a profile taken
     from them stays valid across comment edits and no longer after any code
@@ -61,7 +61,7 @@ def kernel_source_hash():
     import re
     h = hashlib.sha256()
     for f in ("mla_kernels.hip", "mla_api.cpp", "mla_kernels.h"):
-        with open(os.path.join(ROOT, "paper_2607_02043_amd", "csrc", f)) as fh:
+        with open(os.path.join(root, "paper_2607_02043_amd", "csrc", f)) as fh:
             text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
         for line in text.splitlines():
             code = line.split("//", 1)[0].rstrip()
@@ -70,11 +70,11 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def profiled_traffic(config_idx):
+def profiled_traffic(config_idx, root=ROOT):
     """HBM bytes per mixed_step call from the committed rocprofv3 counter
     summary, or None if there is none for this workload or the kernels changed
     since it was taken."""
-    path = os.path.join(ROOT, "profiles", "mixed_step_config%d.md" % config_idx)
+    path = os.path.join(root, "profiles", "mixed_step_config%d.md" % config_idx)
     if not os.path.exists(path):
         return None
     fields = {}
@@ -83,7 +83,7 @@ def profiled_traffic(config_idx):
             if ":" in line and line.startswith("    "):
                 k, v = line.strip().split(":", 1)
                 fields[k.strip()] = v.strip()
-    if fields.get("kernel_source_sha256_16") != kernel_source_hash():
+    if fields.get("kernel_source_sha256_16") != kernel_source_hash(root):
         return None
     try:
         return int(fields["traffic_bytes_per_call"])
@@ -166,8 +166,8 @@ def main():
 
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only (--gpus 1): every decode node of the "
-                                   "paper's deployment is an independent one-GPU unit, and this build uses one "
-                                   f"GPU; --gpus {args.gpus} is not supported"}))
+                                   "paper's deployment is an independent one-GPU unit; "
+                                   f"--gpus {args.gpus} is not supported"}))
         sys.exit(2)
 
     import torch
