@@ -340,7 +340,9 @@ double fill_units(const std::vector<LoadRun> &runs, long long n, double u) {
 //    dec_unit_tiles; the units fill the tail after the chunk items.
 // The device recomputes the same mapping from the device copies of the
 // lengths.  Cost: a closed form per request and candidate key split, then a
-// queue simulation of the best one or two.
+// queue simulation of the best one (and of the runner-up while its work
+// bound can still win), with the decode fill of each unit size evaluated
+// exactly until a lower bound rules the rest out.
 int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkRoute route, Plan *pl,
                        const Plan *warm = nullptr) {
     const long long P = b->page_size;
