@@ -73,7 +73,7 @@
 extern "C" {
 #endif
 
-#define MLA_ABI_VERSION 3
+#define MLA_ABI_VERSION 4
 #define MLA_NUM_HEADS 16
 #define MLA_D_QK 576 /* latent width: 512 compressed + 64 rope dims */
 #define MLA_D_V 512  /* value width: the first 512 latent dims */
@@ -133,14 +133,19 @@ int mla_device_flags(int32_t clear, int32_t *flags, void *stream);
  *                         that plan's key split and decode unit size when
  *                         the unit still fits the kernel's limits (counts and
  *                         offsets are recomputed, O(requests)); 0: every new
- *                         batch is planned in full.
+ *                         batch is planned in full;
+ *   MLA_DEBUG_DEC_UNIT    force the decode unit size, in 32-key tiles (made
+ *                         smaller until a unit fits the kernel's segment and
+ *                         page-window limits); 0 or -1: the planner's choice.
+ *                         For tuning and tests: results stay within rounding.
  * Errors: MLA_ERR_INVALID_ARG (unknown knob, bad value). */
 typedef enum {
     MLA_DEBUG_CHECK = 0,
     MLA_DEBUG_SPIN_LIMIT = 1,
     MLA_DEBUG_CHUNK_KEYS = 2,
     MLA_DEBUG_WARM_PLAN = 3,
-    MLA_DEBUG_COUNT = 4
+    MLA_DEBUG_DEC_UNIT = 4,
+    MLA_DEBUG_COUNT = 5
 } mla_debug_knob;
 int mla_debug_set(int32_t knob, int32_t value);
 

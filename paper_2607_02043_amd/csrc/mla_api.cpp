@@ -133,17 +133,22 @@ struct Plan {
     long long chunk_keys_max = 0;  // keys of the longest chunk request
     int n_chunk_reqs = 0, n_dec_reqs = 0;
     bool warm = false;  // key split and unit size taken from an earlier plan
+    double est_us = 0.0;  // the cost model's finishing time of a full plan (0 when warm-started)
 };
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
-// Per-CU costs (us, measured on MI355X) used only to size the work items.
-constexpr double kChunkTileUs = 2.2;   // one chunk tile: 8 tokens x 32 keys
-constexpr double kChunkItemUs = 14.0;  // chunk item: lookup, queries, ring fill; epilogue stores
-constexpr double kEmptyItemUs = 1.5;   // a chunk item past its block's causal limit
-constexpr double kDecTileUs = 3.5;     // one decode tile of a unit (the two units of an item run side by side)
-constexpr double kDecUnitUs = 5.5;     // decode item start-up
-constexpr double kMergeGBs = 4000.0;   // partial rows written and merged, whole chip
+// Per-CU costs (us) used only to size the work items: calibrated so that
+// the planner's choice of key split and decode unit size is close to the
+// fastest measured one over a set of MI355X steps (small and large decode
+// batches, chunks of 124 to 4096 tokens over prefixes up to 8192).
+constexpr double kChunkTileUs = 2.0;    // one chunk tile: 8 tokens x 32 keys
+constexpr double kChunkItemUs = 18.0;   // chunk item: lookup, queries, ring fill; epilogue stores
+constexpr double kEmptyItemUs = 1.5;    // a chunk item past its block's causal limit
+constexpr double kDecTileUs = 3.5;      // one decode tile of a unit (the two units of an item run side by side)
+constexpr double kDecUnitUs = 8.0;      // decode item start-up
+constexpr double kMergeGBs = 3000.0;    // partial rows written and merged, whole chip
+constexpr double kMergeLaunchUs = 7.0;  // the merge launch itself, when any row is split
 constexpr int kCounterBytes = 256;     // work-queue counters at the start of the workspace
 
 struct DecReq {
@@ -398,12 +403,14 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     }
 
     // Chunk work for a key split ks: total cost, largest item, items, and
-    // the partial rows (written, read back, the merged row written).  Per
+    // the partial rows a split adds (each part written, then read back by the
+    // merge, whose merged row replaces the direct store).  Per
     // request in closed form: the blocks' causal limits p + 8 (rb + 1) form
     // an arithmetic sequence (the last block ends at p + c).
     struct ChunkEst {
         double total = 0.0, max_item = 0.0, merge_us = 0.0;
         long long items = 0;
+        bool split = false;
     };
     auto chunk_est = [&](long long ks) {
         ChunkEst e;
@@ -420,11 +427,12 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             if (nks > 1) {
                 // rows of the blocks whose keys span more than one range
                 const double first_split = std::max(0.0, (double)(ks - p) / BM);  // blocks within ks keys
-                split_rows += (double)(nks + 1) * std::max(0.0, (double)c - first_split * BM);
+                split_rows += (double)(2 * nks) * std::max(0.0, (double)c - first_split * BM);
             }
             e.items += nrb * nks;
         }
         e.merge_us = split_rows * row_bytes / (kMergeGBs * 1e3);
+        e.split = split_rows > 0.0;
         return e;
     };
     // Chunk items of key split ks in device queue order (requests forward or
@@ -468,8 +476,10 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     // per-unit segment and page-window limits.
     std::vector<long long> units;
     if (dec_total > 0 && warm == nullptr) {
-        const long long cands[] = {8, 16, 32, 64, ceil_div_ll(dec_total, 3LL * G), ceil_div_ll(dec_total, 2LL * G),
-                                   ceil_div_ll(dec_total, G)};
+        const long long forced_unit = debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed);
+        std::vector<long long> cands{8, 16, 32, 64, ceil_div_ll(dec_total, 3LL * G), ceil_div_ll(dec_total, 2LL * G),
+                                     ceil_div_ll(dec_total, G)};
+        if (forced_unit > 0) cands.assign(1, forced_unit);
         for (long long U : cands) {
             U = std::max(1LL, std::min(U, dec_total));
             bool fits;
@@ -485,6 +495,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     struct DecFill {
         long long n;
         double u, merge_us;
+        bool split;
     };
     auto dec_fill = [&](long long U) {
         long long split_parts = 0;
@@ -500,11 +511,11 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         uint32_t first = 0;  // unit of the request's first tile
         for (const DecReq &d : dec) {
             const uint32_t l = (uint32_t)(d.first_tile + d.tiles - 1), last = unit_of(l);
-            if (last > first) split_parts += last - first + 2;  // rows moved: the parts, the merged row
+            if (last > first) split_parts += 2 * (last - first + 1);  // each part written and read back
             first = last + ((last + 1) * u32 == l + 1);
         }
         return DecFill{ceil_div_ll(ceil_div_ll(dec_total, U), 2), kDecUnitUs + kDecTileUs * (double)U,
-                       (double)split_parts * row_bytes / (kMergeGBs * 1e3)};
+                       (double)split_parts * row_bytes / (kMergeGBs * 1e3), split_parts > 0};
     };
 
     // Key split: the closed-form estimate keeps the best candidate (and the
@@ -519,21 +530,25 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         struct Cand {
             long long ks;
             double est, merge_us;
+            bool split;
         };
         std::vector<Cand> cands;
         // the decode work fills the CUs after the chunk items: about
         // kDecTileUs / 2 per tile (the two units of an item run side by side)
         const double dec_work = 0.5 * kDecTileUs * (double)dec_total;
         if (!chunks.empty() && ks_forced > 0) {
-            cands.push_back(Cand{std::min(ks_forced, cap), 0.0, chunk_est(std::min(ks_forced, cap)).merge_us});
+            const ChunkEst e = chunk_est(std::min(ks_forced, cap));
+            cands.push_back(Cand{std::min(ks_forced, cap), 0.0, e.merge_us, e.split});
         } else if (!chunks.empty()) {
             for (long long ks = 64;; ks *= 2) {
                 const long long k = std::min(ks, cap);
                 const ChunkEst e = chunk_est(k);
                 if (e.items <= 8LL * G || k >= cap) {
                     const double tail = e.items <= G ? 0.0 : 0.5 * e.total / (double)e.items;
-                    cands.push_back(
-                        Cand{k, std::max(e.max_item, (e.total + dec_work) / G + tail) + e.merge_us, e.merge_us});
+                    // (the merge launch is left out here: decode rows may
+                    // need it anyway, which only the simulation below knows)
+                    cands.push_back(Cand{k, std::max(e.max_item, (e.total + dec_work) / G + tail) + e.merge_us,
+                                         e.merge_us, e.split});
                 }
                 if (k >= cap) break;
             }
@@ -541,15 +556,19 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             // the runner-up is simulated too only when the estimates are close
             cands.resize(cands.size() > 1 && cands[1].est <= 1.1 * cands[0].est ? 2 : 1);
         } else {
-            cands.push_back(Cand{cap, 0.0, 0.0});
+            cands.push_back(Cand{cap, 0.0, 0.0, false});
         }
         std::vector<DecFill> fills;
-        double dec_min = dec_total > 0 ? 1e300 : 0.0, merge_min = dec_total > 0 ? 1e300 : 0.0;
+        double dec_min = dec_total > 0 ? 1e300 : 0.0;
         for (long long U : units) {
             fills.push_back(dec_fill(U));
             dec_min = std::min(dec_min, (double)fills.back().n * fills.back().u);
-            merge_min = std::min(merge_min, fills.back().merge_us);
         }
+        // merges of a candidate split and a unit size: their traffic and,
+        // when any row is split, the merge launch
+        auto merges = [](const Cand &cd, const DecFill &df) {
+            return cd.merge_us + df.merge_us + ((cd.split || df.split) ? kMergeLaunchUs : 0.0);
+        };
         double best = 1e300;
         size_t best_key = 0;
         std::vector<double> items;
@@ -569,13 +588,15 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                         sum += c;
                         largest = std::max(largest, c);
                     }
-                    const double lower = std::max(largest, (sum + dec_min) / (double)G) + cd.merge_us + merge_min;
+                    double merge_min = dec_total > 0 ? 1e300 : cd.merge_us + (cd.split ? kMergeLaunchUs : 0.0);
+                    for (const DecFill &df : fills) merge_min = std::min(merge_min, merges(cd, df));
+                    const double lower = std::max(largest, (sum + dec_min) / (double)G) + merge_min;
                     if (lower * (1.0 - 1e-9) >= best) continue;
                 }
                 loads = load_runs(simulate_chunks(items, G));
             }
             if (dec_total == 0) {
-                const double t = loads.back().load + cd.merge_us;
+                const double t = loads.back().load + cd.merge_us + (cd.split ? kMergeLaunchUs : 0.0);
                 if (t < best) {
                     best = t;
                     ks_best = cd.ks;
@@ -588,13 +609,13 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             order.clear();
             for (size_t ui = 0; ui < units.size(); ++ui) {
                 const DecFill &df = fills[ui];
-                order.emplace_back(fill_bound(loads, df.n, df.u) + df.merge_us + cd.merge_us, ui);
+                order.emplace_back(fill_bound(loads, df.n, df.u) + merges(cd, df), ui);
             }
             std::sort(order.begin(), order.end());
             for (const auto &o : order) {
                 if (o.first > best) break;
                 const DecFill &df = fills[o.second];
-                const double t = fill_units(loads, df.n, df.u) + df.merge_us + cd.merge_us;
+                const double t = fill_units(loads, df.n, df.u) + merges(cd, df);
                 const size_t key = ci * units.size() + o.second;
                 if (t < best || (t == best && key < best_key)) {
                     best = t;
@@ -604,6 +625,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                 }
             }
         }
+        pl->est_us = best;
     }
     const long long U = dec_total > 0 ? U_best : 0;
     const long long n_units = dec_total > 0 ? ceil_div_ll(dec_total, U) : 0;
@@ -669,9 +691,10 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute rou
     int st = MLA_OK;
     const int ncu = cu_count(&st);
     if (st != MLA_OK) return st;
-    constexpr size_t kHdr = 7;
+    constexpr size_t kHdr = 8;
     const int32_t hdr[kHdr] = {b->page_size, ncu, sh.R, b->max_pages_per_req, route.min_rows, route.pair_keys,
-                               debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed)};
+                               debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed),
+                               debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed)};
     const size_t qbytes = (size_t)sh.R * sizeof(int32_t);
     // key: header, query lengths, prefix lengths
     thread_local std::vector<int32_t> key;
@@ -871,6 +894,7 @@ int mla_debug_set(int32_t knob, int32_t value) {
         return fail(MLA_ERR_INVALID_ARG, "chunk key split %d is not a non-negative multiple of 64", value);
     if (knob == MLA_DEBUG_WARM_PLAN && value != 0 && value != 1 && value != -1)
         return fail(MLA_ERR_INVALID_ARG, "warm planning must be 0 or 1, not %d", value);
+    if (knob == MLA_DEBUG_DEC_UNIT && value < -1) return fail(MLA_ERR_INVALID_ARG, "decode unit size %d < -1", value);
     const int dflt = knob == MLA_DEBUG_SPIN_LIMIT ? mla::kSpinLimit : knob == MLA_DEBUG_WARM_PLAN ? 1 : 0;
     debug_value(knob).store(value != -1 ? value : dflt);
     return MLA_OK;

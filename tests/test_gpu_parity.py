@@ -253,6 +253,22 @@ def test_forced_chunk_key_splits(keys):
         mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)
 
 
+@pytest.mark.parametrize("unit", [1, 2, 3])
+def test_forced_small_decode_units(unit):
+    """Decode units of 1-3 tiles: every request is cut into many parts (up to
+    ~100 for the longest), each a partial row merged by the split combine,
+    several requests inside one unit where they are short.  Page 16, a chunk
+    beside them."""
+    wl = W.custom([3100, 15, 0, 700, 33, 64, 2000], [1, 1, 40, 1, 1, 1, 1], page_size=16, seed=40 + unit,
+                  name=f"unit{unit}")
+    log(f"[gpu] forced decode unit {unit}")
+    mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, unit)
+    try:
+        _compare_all_rows(wl, wl.layer(0))
+    finally:
+        mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, 0)
+
+
 def test_serving_steps_with_warm_plans():
     """Consecutive steps whose decode lengths grow by one token, as a decode
     node serves them: every step is a new batch, planned warm from the first

@@ -32,7 +32,7 @@ def harness(tmp_path_factory):
     return exe
 
 
-def plan(exe, batches, route=None, chunk_keys=None):
+def plan(exe, batches, route=None, chunk_keys=None, dec_unit=None):
     text = "".join(f"{ncu} {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n"
                    for ncu, P, q, p in batches)
     env = dict(os.environ)
@@ -40,6 +40,8 @@ def plan(exe, batches, route=None, chunk_keys=None):
         env["PLAN_ROUTE"] = f"{route[0]} {route[1]}"
     if chunk_keys is not None:
         env["PLAN_CHUNK_KEYS"] = str(chunk_keys)
+    if dec_unit is not None:
+        env["PLAN_DEC_UNIT"] = str(dec_unit)
     out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True,
                          env=env).stdout.splitlines()
     assert len(out) == len(batches)
@@ -243,6 +245,23 @@ def test_forced_chunk_key_split(harness, keys):
             assert d["ks"] == min(keys, max(64, (PAGE_WINDOW - 1) * P // 64 * 64))
 
 
+@pytest.mark.parametrize("unit", [1, 3, 40, 100000])
+def test_forced_decode_unit(harness, unit):
+    """The debug knob fixes the decode unit size, made smaller only as far as
+    the kernel's segment and page-window limits require; the plan still
+    respects every limit."""
+    rng = np.random.default_rng(unit)
+    batches = [random_batch(rng, 256) for _ in range(40)]
+    reduced = 0
+    for batch, d in zip(batches, plan(harness, batches, dec_unit=unit)):
+        check_plan(batch, d)
+        if d["dec_total"] > 0:
+            assert 1 <= d["U"] <= min(unit, d["dec_total"])
+            reduced += d["U"] < min(unit, d["dec_total"])
+    if unit <= 3:
+        assert reduced == 0  # units this small always fit
+
+
 def _serving_plans(harness, batches):
     env = dict(os.environ, PLAN_SERVING="1")
     text = "".join(f"256 {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n" for _, P, q, p in batches)
@@ -286,7 +305,12 @@ def test_serving_sequence_plans_warm_and_stays_valid(harness):
     assert plans[0]["warm"] == 0 and plans[-1]["warm"] == 0
     warm = [d for d in plans[1:40] if d["warm"]]
     assert len(warm) >= 30
-    assert all(d["ks"] == plans[0]["ks"] and d["U"] == plans[0]["U"] for d in warm)
+    anchor = None  # a warm plan keeps the key split and unit size of the last full plan
+    for d in plans:
+        if d["warm"]:
+            assert (d["ks"], d["U"]) == anchor
+        else:
+            anchor = (d["ks"], d["U"])
     assert float(np.median([d["us"] for d in warm])) < 50.0
 
 
