@@ -29,6 +29,9 @@ EDGE_CASES = {
     "chunk_long_prefix": ([5000], [37], 64),
     "page256": ([600, 0, 1000], [1, 300, 1], 256),
     "chunk_first": ([0, 9, 300], [33, 1, 1], 32),
+    "page512": ([1030, 0, 511], [1, 513, 1], 512),
+    "page1024": ([3000, 0, 1500, 10], [1, 200, 1, 1], 1024),
+    "decode_100k_keys": ([100000, 7], [1, 1], 64),
 }
 
 
