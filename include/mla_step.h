@@ -73,7 +73,7 @@
 extern "C" {
 #endif
 
-#define MLA_ABI_VERSION 4
+#define MLA_ABI_VERSION 5
 #define MLA_NUM_HEADS 16
 #define MLA_D_QK 576 /* latent width: 512 compressed + 64 rope dims */
 #define MLA_D_V 512  /* value width: the first 512 latent dims */
@@ -137,7 +137,15 @@ int mla_device_flags(int32_t clear, int32_t *flags, void *stream);
  *   MLA_DEBUG_DEC_UNIT    force the decode unit size, in 32-key tiles (made
  *                         smaller until a unit fits the kernel's segment and
  *                         page-window limits); 0 or -1: the planner's choice.
- *                         For tuning and tests: results stay within rounding.
+ *                         For tuning and tests: results stay within rounding;
+ *   MLA_DEBUG_DEC_FIRST   force the number of workgroups of the attention
+ *                         launch that take decode work before chunk work
+ *                         (capped by the launch's workgroups; the others
+ *                         start on the chunk work, and every workgroup moves
+ *                         to the other kind once its own is used up): 0 for
+ *                         none (chunk work first everywhere); -1 (the
+ *                         default): the planner's choice.  For tuning and
+ *                         tests: the results do not change.
  * Errors: MLA_ERR_INVALID_ARG (unknown knob, bad value). */
 typedef enum {
     MLA_DEBUG_CHECK = 0,
@@ -145,7 +153,8 @@ typedef enum {
     MLA_DEBUG_CHUNK_KEYS = 2,
     MLA_DEBUG_WARM_PLAN = 3,
     MLA_DEBUG_DEC_UNIT = 4,
-    MLA_DEBUG_COUNT = 5
+    MLA_DEBUG_DEC_FIRST = 5,
+    MLA_DEBUG_COUNT = 6
 } mla_debug_knob;
 int mla_debug_set(int32_t knob, int32_t value);
 

@@ -34,6 +34,7 @@ MLA_DEBUG_SPIN_LIMIT = 1
 MLA_DEBUG_CHUNK_KEYS = 2
 MLA_DEBUG_WARM_PLAN = 3
 MLA_DEBUG_DEC_UNIT = 4
+MLA_DEBUG_DEC_FIRST = 5
 # include/mla_layer.h
 EXPORTED_LAYER = ("mla_proj_workspace_bytes", "mla_pre_attn", "mla_post_attn", "mla_layer_workspace_bytes",
                   "mla_attention_layer", "mla_layer_tune")

@@ -69,6 +69,7 @@ std::atomic<int> &debug_value(int knob) {
         v[MLA_DEBUG_SPIN_LIMIT].store(mla::kSpinLimit);
         v[MLA_DEBUG_CHUNK_KEYS].store(0);
         v[MLA_DEBUG_WARM_PLAN].store(1);
+        v[MLA_DEBUG_DEC_FIRST].store(-1);
     });
     return v[knob];
 }
@@ -126,6 +127,7 @@ int check_batch(const mla_batch *b, Shape *sh) {
 struct Plan {
     int ks_chunk = 0, n_chunk_items = 0;
     int n_dec_units = 0, dec_unit_tiles = 0, dec_total_tiles = 0, grid = 0, merge_hsplit = 1;
+    int dec_first_wgs = 0;  // workgroups that take decode items before chunk items
     bool chunk_split = false, dec_split = false, chunk_rev = false;
     size_t off_chunk_o = 0, off_chunk_ml = 0, off_dec_o = 0, off_dec_ml = 0, bytes = 0;
     // what a warm start compares: the work of the batch the plan was made for
@@ -147,6 +149,8 @@ constexpr double kChunkItemUs = 18.0;   // chunk item: lookup, queries, ring fil
 constexpr double kEmptyItemUs = 1.5;    // a chunk item past its block's causal limit
 constexpr double kDecTileUs = 3.5;      // one decode tile of a unit (the two units of an item run side by side)
 constexpr double kDecUnitUs = 8.0;      // decode item start-up
+constexpr double kDecTileLoUs = 2.65;   // a decode tile when few workgroups stream (per-CU rate bound)
+constexpr double kTwoQueueGain = 0.03;  // decode-first workgroups only for at least this much less time
 constexpr double kMergeGBs = 3000.0;    // partial rows written and merged, whole chip
 constexpr double kMergeLaunchUs = 7.0;  // the merge launch itself, when any row is split
 constexpr int kCounterBytes = 256;     // work-queue counters at the start of the workspace
@@ -184,12 +188,14 @@ bool dec_share_fits(const std::vector<DecReq> &reqs, long long total, long long 
 }
 
 // Loads of the G workgroups after the chunk items, each item taken in queue
-// order by the first free workgroup.
-std::vector<double> simulate_chunks(const std::vector<double> &items, int G) {
-    // the first G items start on idle workgroups; each later one goes to the
-    // workgroup that finishes first (the root of a min-heap, sifted down)
-    const size_t g = (size_t)G, n0 = std::min(g, items.size());
-    std::vector<double> heap(g, 0.0);
+// order by the first free workgroup; `init` (G loads) is where the
+// workgroups start, all at 0 when it is null.
+std::vector<double> simulate_chunks(const std::vector<double> &items, int G, const std::vector<double> *init = nullptr) {
+    // each item goes to the workgroup that finishes first (the root of a
+    // min-heap, sifted down); from idle workgroups the first G items start
+    // directly
+    const size_t g = (size_t)G, n0 = init != nullptr ? 0 : std::min(g, items.size());
+    std::vector<double> heap = init != nullptr ? *init : std::vector<double>(g, 0.0);
     for (size_t i = 0; i < n0; ++i) heap[i] = items[i];
     std::make_heap(heap.begin(), heap.end(), [](double x, double y) { return x > y; });
     for (size_t i = n0; i < items.size(); ++i) {
@@ -472,8 +478,15 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             }
         }
     };
-    // Decode units: the candidate sizes (tiles) that respect the kernel's
-    // per-unit segment and page-window limits.
+    // A decode unit size made smaller until it respects the kernel's
+    // per-unit segment and page-window limits (0 if even one tile does not).
+    auto fit_unit = [&](long long U) {
+        U = std::max(1LL, std::min(U, dec_total));
+        bool fits;
+        while (!(fits = dec_share_fits(dec, dec_total, U, (int)P, min_tiles)) && U > 1) U = std::max(1LL, U * 3 / 4);
+        return fits ? U : 0LL;
+    };
+    // Decode units: the candidate sizes (tiles) that respect those limits.
     std::vector<long long> units;
     if (dec_total > 0 && warm == nullptr) {
         const long long forced_unit = debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed);
@@ -481,11 +494,8 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                                      ceil_div_ll(dec_total, G)};
         if (forced_unit > 0) cands.assign(1, forced_unit);
         for (long long U : cands) {
-            U = std::max(1LL, std::min(U, dec_total));
-            bool fits;
-            while (!(fits = dec_share_fits(dec, dec_total, U, (int)P, min_tiles)) && U > 1) U = std::max(1LL, U * 3 / 4);
-            if (!fits) continue;
-            if (std::find(units.begin(), units.end(), U) == units.end()) units.push_back(U);
+            U = fit_unit(U);
+            if (U > 0 && std::find(units.begin(), units.end(), U) == units.end()) units.push_back(U);
         }
         if (units.empty())
             return fail(MLA_ERR_UNSUPPORTED, "decode work does not fit the per-unit segment / page limits");
@@ -521,7 +531,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     // Key split: the closed-form estimate keeps the best candidate (and the
     // runner-up when within 10%), whose queue is then simulated (with the
     // decode units after it).
-    long long ks_best = cap, U_best = units.empty() ? 1 : units.back();
+    long long ks_best = cap, U_best = units.empty() ? 1 : units.back(), dec_first = 0;
     const long long ks_forced = debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed);
     if (warm != nullptr) {
         ks_best = warm->ks_chunk;
@@ -531,6 +541,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
             long long ks;
             double est, merge_us;
             bool split;
+            ChunkEst e;
         };
         std::vector<Cand> cands;
         // the decode work fills the CUs after the chunk items: about
@@ -538,7 +549,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         const double dec_work = 0.5 * kDecTileUs * (double)dec_total;
         if (!chunks.empty() && ks_forced > 0) {
             const ChunkEst e = chunk_est(std::min(ks_forced, cap));
-            cands.push_back(Cand{std::min(ks_forced, cap), 0.0, e.merge_us, e.split});
+            cands.push_back(Cand{std::min(ks_forced, cap), 0.0, e.merge_us, e.split, e});
         } else if (!chunks.empty()) {
             for (long long ks = 64;; ks *= 2) {
                 const long long k = std::min(ks, cap);
@@ -548,15 +559,13 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                     // (the merge launch is left out here: decode rows may
                     // need it anyway, which only the simulation below knows)
                     cands.push_back(Cand{k, std::max(e.max_item, (e.total + dec_work) / G + tail) + e.merge_us,
-                                         e.merge_us, e.split});
+                                         e.merge_us, e.split, e});
                 }
                 if (k >= cap) break;
             }
             std::sort(cands.begin(), cands.end(), [](const Cand &x, const Cand &y) { return x.est < y.est; });
-            // the runner-up is simulated too only when the estimates are close
-            cands.resize(cands.size() > 1 && cands[1].est <= 1.1 * cands[0].est ? 2 : 1);
         } else {
-            cands.push_back(Cand{cap, 0.0, 0.0, false});
+            cands.push_back(Cand{cap, 0.0, 0.0, false, ChunkEst{}});
         }
         std::vector<DecFill> fills;
         double dec_min = dec_total > 0 ? 1e300 : 0.0;
@@ -572,12 +581,20 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         double best = 1e300;
         size_t best_key = 0;
         std::vector<double> items;
+        long long items_ks = -1;  // the key split `items` holds
+        auto items_for = [&](long long ks) {
+            if (ks != items_ks) chunk_items(ks, rev, items);
+            items_ks = ks;
+        };
         std::vector<std::pair<double, size_t>> order;
-        for (size_t ci = 0; ci < cands.size(); ++ci) {
+        // the best candidate is simulated, and the runner-up too when the
+        // estimates are close
+        const size_t n_sim = cands.size() > 1 && cands[1].est <= 1.1 * cands[0].est ? 2 : 1;
+        for (size_t ci = 0; ci < n_sim; ++ci) {
             const Cand &cd = cands[ci];
             std::vector<LoadRun> loads{LoadRun{0.0, (long long)G, 0.0, (long long)G}};
             if (!chunks.empty()) {
-                chunk_items(cd.ks, rev, items);
+                items_for(cd.ks);
                 if (ci > 0) {
                     // the runner-up finishes no earlier than its largest item
                     // or its average load per workgroup (the least decode
@@ -625,6 +642,85 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                 }
             }
         }
+        // Decode-first workgroups: D of them stream the decode work, one item
+        // each (units of ceil(T / 2D) tiles), while the others run the chunk
+        // items; each moves to the chunk items when its decode item is done.
+        // Fewer workgroups streaming at once get more of the memory
+        // bandwidth each, down to a per-CU floor of kDecTileLoUs a tile, so
+        // the decode work takes fewer workgroup-microseconds than at the
+        // tail of the chunk-first schedule.  Closed form for every key split
+        // and D, then a queue simulation of the best pair (and of the
+        // runner-up when within 5%), taken when it beats the chunk-first
+        // plan by kTwoQueueGain (or D is forced).
+        const long long forced_first = debug_value(MLA_DEBUG_DEC_FIRST).load(std::memory_order_relaxed);
+        if (!chunks.empty() && dec_total > 0 && forced_first != 0) {
+            const long long forced_unit = debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed);
+            std::vector<long long> firsts;
+            if (forced_first > 0)
+                firsts.push_back(std::min<long long>(forced_first, G));
+            else
+                for (int eighths = 2; eighths <= 7; ++eighths) firsts.push_back(std::max(1LL, (long long)G * eighths / 8));
+            struct Two {
+                long long D, U, n, Dp;
+                double c, est;
+                size_t ci;
+                DecFill df;
+            };
+            Two top[2] = {};
+            top[0].est = top[1].est = 1e300;
+            for (long long D : firsts) {
+                const long long U2 = fit_unit(forced_unit > 0 ? forced_unit : ceil_div_ll(dec_total, 2 * D));
+                if (U2 == 0) continue;
+                const DecFill df = dec_fill(U2);
+                const long long Dp = std::min(D, df.n);  // workgroups that stream at once
+                const double tile = std::max(kDecTileLoUs, kDecTileUs * (double)Dp / (double)G);
+                const double c = kDecUnitUs + tile * (double)U2;
+                const double t_first = c * (double)ceil_div_ll(df.n, Dp), dec_wg = c * (double)df.n;
+                Two mine{D, U2, df.n, Dp, c, 1e300, 0, df};  // this D's best key split
+                for (size_t ci = 0; ci < cands.size(); ++ci) {
+                    const ChunkEst &e = cands[ci].e;
+                    // without the tail, about the least any schedule takes:
+                    // a pair that cannot beat the chunk-first plan is dropped
+                    const double floor = std::max({e.max_item, t_first, (e.total + dec_wg) / G}) + merges(cands[ci], df);
+                    if (forced_first <= 0 && floor >= best) continue;
+                    const double tail = e.items <= G ? 0.0 : 0.5 * e.total / (double)e.items;
+                    const double est = std::max(floor, (e.total + dec_wg) / G + tail + merges(cands[ci], df));
+                    if (est < mine.est) {
+                        mine.est = est;
+                        mine.ci = ci;
+                    }
+                }
+                if (mine.est < top[0].est) {
+                    top[1] = top[0];
+                    top[0] = mine;
+                } else if (mine.est < top[1].est) {
+                    top[1] = mine;
+                }
+            }
+            double best_two = 1e300;
+            const Two *pick = nullptr;
+            for (const Two &tw : top) {
+                if (tw.est >= 1e300 || (&tw != top && tw.est > 1.05 * top[0].est)) continue;
+                // decode-first workgroup loads: the items dealt round the Dp
+                // streaming ones
+                std::vector<double> init((size_t)G, 0.0);
+                for (long long j = 0; j < tw.Dp; ++j)
+                    init[(size_t)j] = tw.c * (double)(tw.n / tw.Dp + (j < tw.n % tw.Dp ? 1 : 0));
+                items_for(cands[tw.ci].ks);
+                const std::vector<double> fin = simulate_chunks(items, G, &init);
+                const double t = *std::max_element(fin.begin(), fin.end()) + merges(cands[tw.ci], tw.df);
+                if (t < best_two) {
+                    best_two = t;
+                    pick = &tw;
+                }
+            }
+            if (pick != nullptr && (forced_first > 0 || best_two < best * (1.0 - kTwoQueueGain))) {
+                best = best_two;
+                ks_best = cands[pick->ci].ks;
+                U_best = pick->U;
+                dec_first = pick->D;
+            }
+        }
         pl->est_us = best;
     }
     const long long U = dec_total > 0 ? U_best : 0;
@@ -648,6 +744,11 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     pl->dec_unit_tiles = (int)U;
     pl->dec_total_tiles = (int)dec_total;
     pl->grid = (int)std::min<long long>(G, nci + pl->n_dec_units);
+    {
+        const long long forced_first = debug_value(MLA_DEBUG_DEC_FIRST).load(std::memory_order_relaxed);
+        const long long first = forced_first >= 0 ? forced_first : warm != nullptr ? warm->dec_first_wgs : dec_first;
+        pl->dec_first_wgs = nci > 0 && dec_total > 0 ? (int)std::min<long long>(first, pl->grid) : 0;
+    }
     long long max_parts = 1;
     for (const DecReq &d : dec) {
         const long long parts = (d.first_tile + d.tiles - 1) / U - d.first_tile / U + 1;
@@ -674,10 +775,10 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
     if (log_plan)
         std::fprintf(stderr,
                      "[mla plan] R=%d CUs=%d chunk items=%d (ks=%d keys, split=%d, rev=%d) decode units=%d x %d "
-                     "tiles (total %lld, split=%d, merge x%d) grid=%d workspace=%zu B%s\n",
+                     "tiles (total %lld, split=%d, merge x%d) grid=%d decode-first=%d workspace=%zu B%s\n",
                      sh.R, ncu, pl->n_chunk_items, pl->ks_chunk, (int)pl->chunk_split, (int)pl->chunk_rev,
                      pl->n_dec_units, pl->dec_unit_tiles, dec_total, (int)pl->dec_split, pl->merge_hsplit, pl->grid,
-                     pl->bytes, pl->warm ? " (warm)" : "");
+                     pl->dec_first_wgs, pl->bytes, pl->warm ? " (warm)" : "");
     return MLA_OK;
 }
 
@@ -691,10 +792,11 @@ int make_plan(const mla_batch *b, const Shape &sh, Plan *pl, mla::ChunkRoute rou
     int st = MLA_OK;
     const int ncu = cu_count(&st);
     if (st != MLA_OK) return st;
-    constexpr size_t kHdr = 8;
+    constexpr size_t kHdr = 9;
     const int32_t hdr[kHdr] = {b->page_size, ncu, sh.R, b->max_pages_per_req, route.min_rows, route.pair_keys,
                                debug_value(MLA_DEBUG_CHUNK_KEYS).load(std::memory_order_relaxed),
-                               debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed)};
+                               debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed),
+                               debug_value(MLA_DEBUG_DEC_FIRST).load(std::memory_order_relaxed)};
     const size_t qbytes = (size_t)sh.R * sizeof(int32_t);
     // key: header, query lengths, prefix lengths
     thread_local std::vector<int32_t> key;
@@ -895,7 +997,12 @@ int mla_debug_set(int32_t knob, int32_t value) {
     if (knob == MLA_DEBUG_WARM_PLAN && value != 0 && value != 1 && value != -1)
         return fail(MLA_ERR_INVALID_ARG, "warm planning must be 0 or 1, not %d", value);
     if (knob == MLA_DEBUG_DEC_UNIT && value < -1) return fail(MLA_ERR_INVALID_ARG, "decode unit size %d < -1", value);
-    const int dflt = knob == MLA_DEBUG_SPIN_LIMIT ? mla::kSpinLimit : knob == MLA_DEBUG_WARM_PLAN ? 1 : 0;
+    if (knob == MLA_DEBUG_DEC_FIRST && value < -1)
+        return fail(MLA_ERR_INVALID_ARG, "decode-first workgroups %d < -1", value);
+    const int dflt = knob == MLA_DEBUG_SPIN_LIMIT ? mla::kSpinLimit
+                     : knob == MLA_DEBUG_WARM_PLAN ? 1
+                     : knob == MLA_DEBUG_DEC_FIRST ? -1
+                                                   : 0;
     debug_value(knob).store(value != -1 ? value : dflt);
     return MLA_OK;
 }
@@ -957,6 +1064,7 @@ int attend(const mla_batch *batch, const uint16_t *q, const uint16_t *new_latent
     a.n_dec_units = pl.n_dec_units;
     a.dec_unit_tiles = pl.dec_unit_tiles;
     a.grid = pl.grid;
+    a.dec_first_wgs = pl.dec_first_wgs;
     a.merge_hsplit = pl.merge_hsplit;
     a.dec_total_tiles = pl.dec_total_tiles;
     a.out_bf16 = out_dtype == MLA_OUT_BF16 ? 1 : 0;

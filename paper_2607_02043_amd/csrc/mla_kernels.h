@@ -40,7 +40,7 @@ struct AttnArgs {
     float *ws_chunk_ml;   // [n_chunk_items][block tokens][16][2]
     float *ws_dec_o;      // [2 units][16][512]: first / last segment of each decode unit
     float *ws_dec_ml;     // [2 units][16][2]
-    int32_t *work;        // [2]: next work item, workgroups done; zero between calls
+    int32_t *work;        // [3]: next chunk item, workgroups done, next decode item; zero between calls
     int32_t num_reqs;
     int32_t num_rows;
     int32_t page_size;
@@ -56,6 +56,7 @@ struct AttnArgs {
     int32_t dec_unit_tiles;    // 32-key decode tiles per unit
     int32_t dec_total_tiles;
     int32_t grid;              // persistent workgroups of the attention launch
+    int32_t dec_first_wgs;     // workgroups 0 .. dec_first_wgs - 1 take decode items before chunk items
     int32_t merge_hsplit;      // merge workgroups per split decode row (1, 4 or 8: heads split among them)
     int32_t out_bf16;
     int32_t spin_limit;        // sleeps of a bounded wait before it gives up (kSpinLimit)

@@ -1314,9 +1314,13 @@ __device__ bool chunk_item(const AttnArgs &a, int item, char *smem, int *s_tmp, 
 
 constexpr int kMainLds = kDecLds > kChunkLds ? kDecLds : kChunkLds;
 
-// Persistent workgroups (one per CU) take work items from a counter in the
-// workspace: the chunk items first (largest blocks first), then the decode
-// units, whose small size fills the tail.  An item's results and partial
+// Persistent workgroups (one per CU) take work items from two counters in
+// the workspace, one per queue: the chunk items (largest blocks first) and
+// the decode items.  Workgroups below dec_first_wgs start on the decode
+// queue, the others on the chunk queue, and each moves to the other queue
+// once its own is empty: with no decode-first workgroups the decode units
+// fill the tail after the chunk items; with some, decode streaming runs
+// beside the chunk tiles from the start.  An item's results and partial
 // slots depend only on its index, so the schedule never changes the output
 // bits.  The last workgroup to finish zeroes the counters for the next call.
 __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) {
@@ -1326,12 +1330,26 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) 
     __shared__ DecSeg s_seg[2][kMaxSeg];
     __shared__ int s_gbar[2];
     __shared__ int s_item;
-    const int n_items = a.n_chunk_items + a.n_dec_units;
+    bool on_dec = (int)blockIdx.x < a.dec_first_wgs;  // thread 0's current queue
     for (;;) {
-        if (threadIdx.x == 0) s_item = __hip_atomic_fetch_add(a.work, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (threadIdx.x == 0) {
+            // the current queue, then the other one: -1 once both are empty
+            int it = -1;
+            for (int k = 0; k < 2 && it < 0; ++k) {
+                if (on_dec) {
+                    const int d = __hip_atomic_fetch_add(a.work + 2, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (d < a.n_dec_units) it = a.n_chunk_items + d;
+                } else {
+                    const int c = __hip_atomic_fetch_add(a.work, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (c < a.n_chunk_items) it = c;
+                }
+                if (it < 0) on_dec = !on_dec;
+            }
+            s_item = it;
+        }
         __syncthreads();
         const int item = s_item;
-        if (item >= n_items) break;
+        if (item < 0) break;
         TRACE_ITEM(item);
         if (item < a.n_chunk_items) {
             // a second, exact pass only if the main one was abandoned
@@ -1350,6 +1368,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attention_kernel(AttnArgs a) 
         if (done == (int)gridDim.x - 1) {  // every workgroup has taken its last item
             __hip_atomic_store(a.work, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(a.work + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.work + 2, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }

@@ -8,7 +8,10 @@ the benchmark workloads 2, 3, 5 and 4 at C = 256 .. 4096), every step is
 timed with the planner's own plan and with each forced pair of chunk key
 split (MLA_DEBUG_CHUNK_KEYS: 64 .. 8192 keys below the longest chunk's
 keys, and unsplit) and decode unit size (MLA_DEBUG_DEC_UNIT: 1 .. 128
-tiles and one, two and three units per CU).  Each time is the median of
+tiles and one, two and three units per CU) in the chunk-first schedule
+(MLA_DEBUG_DEC_FIRST = 0), and, for steps with both kinds of work, with
+each key split beside 2/8 .. 7/8 of the CUs starting on the decode work
+(MLA_DEBUG_DEC_FIRST, one decode item each).  Each time is the median of
 five mixed_step calls after two warm-up calls, the last-level cache
 flushed before every call; the planner's own plan is timed before and
 after the forced ones, the faster kept.  The fastest of some fifty noisy
@@ -16,7 +19,7 @@ forced times sits a little below the true fastest, so a regret of 1-2 %
 is within noise.  Printed: per step the planner's time, the
 fastest forced plan and the planner's regret (its time over the fastest,
 minus one), then the mean, 90th percentile and maximum regret; --csv also
-writes every measurement.
+writes every measurement (decode-first workgroups in its last column).
 
 Usage: python -m paper_2607_02043_amd.plan_sweep [--csv FILE] [--quick]
 (--quick: every fourth step only).
@@ -88,10 +91,11 @@ def main(argv=None):
     from paper_2607_02043_amd import workloads as W
     dev = torch.device("cuda:0")
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    ncu = torch.cuda.get_device_properties(dev).multi_processor_count
     all_steps = steps()[::4] if args.quick else steps()
     csv = open(args.csv, "w") if args.csv else None
     if csv:
-        csv.write("step,key_split,unit,us\n")
+        csv.write("step,key_split,unit,us,dec_first\n")
 
     def timed(db, q, new, pool, out, n=5, warm=2):
         ws = mla.workspace_for(db, device=dev)
@@ -118,30 +122,36 @@ def main(argv=None):
         timed(db, qq, new, pool, out, n=20, warm=10)  # page in the new buffers
         own = timed(db, qq, new, pool, out)
         best = (math.inf, None)
-        for ks, u in itertools.product(key_splits(prefix, q), unit_sizes(prefix, q)):
+        forced = [(ks, u, 0) for ks, u in itertools.product(key_splits(prefix, q), unit_sizes(prefix, q))]
+        if any(c == 1 for c in q) and any(c > 1 for c in q):
+            forced += [(ks, 0, ncu * e // 8) for ks in key_splits(prefix, q) for e in range(2, 8)]
+        for ks, u, first in forced:
             mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, ks)
             mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, u)
+            mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, first)
             try:
                 t = timed(db, qq, new, pool, out)
             finally:
                 mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)
                 mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, 0)
+                mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, -1)
             if csv:
-                csv.write(f"{name},{ks},{u},{t:.2f}\n")
-            best = min(best, (t, (ks, u)))
+                csv.write(f"{name},{ks},{u},{t:.2f},{first}\n")
+            best = min(best, (t, (ks, u, first)))
         own = min(own, timed(db, qq, new, pool, out))  # timed again after the forced plans
         regret = own / best[0] - 1
         regrets.append(regret)
         rows.append((name, own, best[0], best[1], regret))
         print(f"[plan_sweep] {si + 1}/{len(all_steps)} {name}: planner {own:.1f} us, fastest {best[0]:.1f} us "
-              f"(key split {best[1][0]}, unit {best[1][1]}), regret {100 * regret:.1f} %", file=sys.stderr, flush=True)
+              f"(key split {best[1][0]}, unit {best[1][1]}, decode-first {best[1][2]}), regret {100 * regret:.1f} %",
+              file=sys.stderr, flush=True)
         del pool, new, qq, out, db, wl, li
         torch.cuda.empty_cache()
     r = np.array(regrets)
-    print("| step | planner µs | fastest forced µs | its key split, unit | regret |")
+    print("| step | planner µs | fastest forced µs | its key split, unit, decode-first | regret |")
     print("|---|---|---|---|---|")
-    for name, own, best, (ks, u), reg in rows:
-        print(f"| {name} | {own:.1f} | {best:.1f} | {ks}, {u} | {100 * reg:.1f} % |")
+    for name, own, best, (ks, u, first), reg in rows:
+        print(f"| {name} | {own:.1f} | {best:.1f} | {ks}, {u or 'planned'}, {first} | {100 * reg:.1f} % |")
     print(f"\nSteps: {len(r)}; regret mean {100 * r.mean():.2f} %, 90th percentile {100 * np.percentile(r, 90):.1f} %, "
           f"max {100 * r.max():.1f} % (negative: the planner's own plan, timed separately, came out faster).")
 

@@ -17,8 +17,12 @@ few times, the last call kept) and prints a markdown summary:
   share of the launch;
 * the longest items (the critical path).
 
-Usage: python -m paper_2607_02043_amd.timeline --config 5 [--chunk C] [--keys KS]
-(--keys forces the chunk key split, as the MLA_DEBUG_CHUNK_KEYS debug knob.)
+Usage: python -m paper_2607_02043_amd.timeline --config 5 [--chunk C] [--keys KS] [--unit U] [--first D]
+[--dump FILE.npy]
+(--keys, --unit and --first force the chunk key split, the decode unit size
+and the decode-first workgroups, as the MLA_DEBUG_CHUNK_KEYS,
+MLA_DEBUG_DEC_UNIT and MLA_DEBUG_DEC_FIRST debug knobs; --dump saves the
+stamps of the last launch, one row per item.)
 """
 import argparse
 import ctypes
@@ -39,7 +43,7 @@ MAX_ITEMS = 1 << 16
 TICK_US = 0.01    # the real-time counter runs at 100 MHz
 
 
-def run(config, chunk=None, keys=0, calls=3):
+def run(config, chunk=None, keys=0, calls=3, unit=0, first=0, dump=None):
     import torch
 
     from paper_2607_02043_amd import workloads as W
@@ -56,7 +60,9 @@ def run(config, chunk=None, keys=0, calls=3):
     def up(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev)
 
-    mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, keys)
+    knobs = ((mla.MLA_DEBUG_CHUNK_KEYS, keys), (mla.MLA_DEBUG_DEC_UNIT, unit), (mla.MLA_DEBUG_DEC_FIRST, first))
+    for k, v in knobs:
+        mla.debug_set(k, v)
     try:
         db = mla.DeviceBatch.from_batch(b, device=dev)
         ws = mla.workspace_for(db, device=dev)
@@ -66,21 +72,29 @@ def run(config, chunk=None, keys=0, calls=3):
             mla.mixed_step(db, q, new, pool, W.SOFTMAX_SCALE, out, None, ws)
         torch.cuda.synchronize()
     finally:
-        mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)
+        for k, _ in knobs:
+            mla.debug_set(k, 0)
     buf = np.zeros((MAX_ITEMS, SLOTS), dtype=np.uint64)
     if L.mla_trace_read(buf.ctypes.data, buf.nbytes) != 0:
         raise SystemExit("reading the trace buffer failed")
+    if dump:
+        np.save(dump, buf[last_launch(buf)])
     return wl, summarize(buf)
 
 
-def summarize(buf):
-    """Figures of the last launch recorded in `buf` (items whose start lies
-    within 3 ms of the latest start; earlier launches of other shapes may
-    have left items with higher indices)."""
+def last_launch(buf):
+    """Indices of the items of the last launch recorded in `buf` (items whose
+    start lies within 3 ms of the latest start; earlier launches of other
+    shapes may have left items with higher indices)."""
     valid = buf[:, 0] > 0
     t_last = buf[valid, 0].astype(np.int64).max()
     valid &= buf[:, 0].astype(np.int64) >= t_last - int(3000 / TICK_US)
-    ix = np.where(valid)[0]
+    return np.where(valid)[0]
+
+
+def summarize(buf):
+    """Figures of the last launch recorded in `buf`."""
+    ix = last_launch(buf)
     stamp = lambda k: buf[ix, k].astype(np.int64)
     kind = (buf[ix, 8] // 1000000).astype(np.int64)   # 1: chunk item, 2: decode item
     units = (buf[ix, 8] % 1000000).astype(np.int64)   # tiles (chunk) or units (decode)
@@ -148,8 +162,11 @@ def main():
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--chunk", type=int, default=None)
     ap.add_argument("--keys", type=int, default=0)
+    ap.add_argument("--unit", type=int, default=0)
+    ap.add_argument("--first", type=int, default=0)
+    ap.add_argument("--dump", default=None)
     args = ap.parse_args()
-    wl, res = run(args.config, args.chunk, args.keys)
+    wl, res = run(args.config, args.chunk, args.keys, unit=args.unit, first=args.first, dump=args.dump)
     cmd = "python -m paper_2607_02043_amd.timeline " + " ".join(sys.argv[1:])
     print(markdown(wl, res, cmd.strip()), flush=True)
 

@@ -3,11 +3,11 @@
 // launched here, and the device queries answer for a 256-CU device).  Input on
 // stdin, one batch per line:
 //   ncu page_size R q_0 p_0 q_1 p_1 ...
-// (PLAN_ROUTE, PLAN_CHUNK_KEYS, PLAN_DEC_UNIT and PLAN_SERVING in the
+// (PLAN_ROUTE, PLAN_CHUNK_KEYS, PLAN_DEC_UNIT, PLAN_DEC_FIRST and PLAN_SERVING in the
 // environment: see main)
 // Output, one line per batch:
 //   ok ks n_chunk_items n_dec_items unit_tiles dec_total grid merge_hsplit chunk_split dec_split bytes
-//      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us warm est_us
+//      off_chunk_o off_chunk_ml off_dec_o off_dec_ml plan_us warm est_us dec_first_wgs
 // or "err <status> <message>".
 // A line "ws <bytes> page_size R q_0 p_0 ..." instead calls the real
 // mixed_step_attn entry point with fake device pointers and a workspace of
@@ -103,6 +103,8 @@ int main() {
     if (const char *e = std::getenv("PLAN_CHUNK_KEYS")) mla_debug_set(MLA_DEBUG_CHUNK_KEYS, std::atoi(e));
     // PLAN_DEC_UNIT=u: the forced decode unit size of the debug knob
     if (const char *e = std::getenv("PLAN_DEC_UNIT")) mla_debug_set(MLA_DEBUG_DEC_UNIT, std::atoi(e));
+    // PLAN_DEC_FIRST=d: the forced decode-first workgroups of the debug knob
+    if (const char *e = std::getenv("PLAN_DEC_FIRST")) mla_debug_set(MLA_DEBUG_DEC_FIRST, std::atoi(e));
     std::string line;
     while (std::getline(std::cin, line)) {
         if (line.rfind("cm ", 0) == 0) {
@@ -183,7 +185,7 @@ int main() {
                   << pl.dec_unit_tiles << " " << pl.dec_total_tiles << " " << pl.grid << " " << pl.merge_hsplit << " "
                   << (int)pl.chunk_split << " " << (int)pl.dec_split << " " << pl.bytes << " " << pl.off_chunk_o << " "
                   << pl.off_chunk_ml << " " << pl.off_dec_o << " " << pl.off_dec_ml << " " << us << " "
-                  << (int)pl.warm << " " << pl.est_us << "\n";
+                  << (int)pl.warm << " " << pl.est_us << " " << pl.dec_first_wgs << "\n";
     }
     return 0;
 }

@@ -156,6 +156,10 @@ def test_debug_settings_are_checked_on_the_host():
     assert L.mla_debug_set(mla.MLA_DEBUG_DEC_UNIT, -2) == mla.MLA_ERR_INVALID_ARG
     assert L.mla_debug_set(mla.MLA_DEBUG_DEC_UNIT, 5) == mla.MLA_OK
     assert L.mla_debug_set(mla.MLA_DEBUG_DEC_UNIT, -1) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_DEC_FIRST, -2) == mla.MLA_ERR_INVALID_ARG
+    assert L.mla_debug_set(mla.MLA_DEBUG_DEC_FIRST, 96) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_DEC_FIRST, 0) == mla.MLA_OK
+    assert L.mla_debug_set(mla.MLA_DEBUG_DEC_FIRST, -1) == mla.MLA_OK
     assert L.mla_device_flags(1, None, None) == mla.MLA_ERR_INVALID_ARG
 
 
@@ -188,7 +192,7 @@ def test_binding_constants_match_the_headers():
     for must in ("MLA_OK", "MLA_ERR_INVALID_ARG", "MLA_ERR_UNSUPPORTED", "MLA_ERR_WORKSPACE", "MLA_ERR_HIP",
                  "MLA_OUT_F32", "MLA_OUT_BF16", "MLA_FLAG_BAD_PAGE", "MLA_FLAG_WAIT_EXPIRED", "MLA_DEBUG_CHECK",
                  "MLA_DEBUG_SPIN_LIMIT", "MLA_DEBUG_CHUNK_KEYS", "MLA_DEBUG_WARM_PLAN", "MLA_DEBUG_DEC_UNIT",
-                 "MLA_TUNE_GEMM_BM",
+                 "MLA_DEBUG_DEC_FIRST", "MLA_TUNE_GEMM_BM",
                  "MLA_TUNE_GEMM_BN", "MLA_TUNE_GEMM_DEPTH", "MLA_TUNE_MHA_MIN_ROWS", "MLA_TUNE_MHA_PAIRS",
                  "MLA_NOALLOC_SCRATCH_BYTES"):
         assert must in values, must

@@ -272,6 +272,36 @@ def test_forced_small_decode_units(unit):
         mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, 0)
 
 
+@pytest.mark.parametrize("first", [1, 5, 64, 100000])
+def test_decode_first_schedule_same_bits(first):
+    """Workgroups that start on the decode queue (1, 5, 64, or every one of
+    the launch) change only which workgroup runs which item: output, LSE and
+    cache are bit-identical to the chunk-first schedule (none forced), which
+    matches the oracle.  Chunks long enough to be split beside decode rows that are
+    split too (small forced units)."""
+    wl = W.custom([4000, 15, 0, 700, 2600, 64, 9000, 300], [1, 1, 300, 1, 1, 1, 1, 129], page_size=16,
+                  seed=50 + first % 97, name=f"first{first}")
+    b, li = wl.batch, wl.layer(0)
+    log(f"[gpu] decode-first workgroups {first}")
+    mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, 7)
+    mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 512)
+    mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, 0)
+    try:
+        base = run_layer(b, li, fused=True)
+        mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, first)
+        g = run_layer(b, li, fused=True)
+    finally:
+        mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, -1)
+        mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, 0)
+        mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)
+    assert np.array_equal(g.out_np().view(np.uint32), base.out_np().view(np.uint32)), "output bits differ"
+    assert np.array_equal(g.lse_np().view(np.uint32), base.lse_np().view(np.uint32)), "LSE bits differ"
+    assert np.array_equal(g.pool_np(), base.pool_np()), "cache differs"
+    pool_ref, out_ref, lse_ref = oracle.step(b, li, W.SOFTMAX_SCALE)
+    assert np.array_equal(g.pool_np(), pool_ref), "append: pool differs from the oracle"
+    assert_close(g.out_np(), out_ref, g.lse_np(), lse_ref, what=wl.name)
+
+
 def test_serving_steps_with_warm_plans():
     """Consecutive steps whose decode lengths grow by one token, as a decode
     node serves them: every step is a new batch, planned warm from the first

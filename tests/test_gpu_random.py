@@ -4,7 +4,8 @@ streams at once (needs an MI355X).
 * Random ragged batches: page sizes 1 .. 256, up to 40 requests, decode rows
   with prefixes up to 3000 keys and chunks of 2 .. 300 rows over prefixes up
   to 2000, some with the chunk key split forced (64 .. 1024 keys) and some
-  with the decode unit size forced (1 .. 64 tiles), the fused and the
+  with the decode unit size forced (1 .. 64 tiles), some with the
+  workgroups that start on the decode work forced (0 .. 256), the fused and the
   two-call entry points; every output row and the whole pool.
 * Concurrency: two different batches, each with its own workspace, launched
   on two streams without a wait between them; each matches the oracle and
@@ -38,23 +39,27 @@ def random_batch(seed):
     keys = int(rng.integers(1, 17)) * 64 if rng.random() < 0.4 else 0
     fused = bool(rng.random() < 0.5)
     unit = int(rng.choice([1, 2, 5, 13, 64])) if rng.random() < 0.4 else 0
-    return prefix, qlen, page, keys, fused, unit
+    first = int(rng.choice([0, 1, 3, 40, 256])) if rng.random() < 0.5 else -1
+    return prefix, qlen, page, keys, fused, unit, first
 
 
 @pytest.mark.parametrize("seed", range(16))
 def test_random_batch_all_rows(seed):
-    prefix, qlen, page, keys, fused, unit = random_batch(seed)
+    prefix, qlen, page, keys, fused, unit, first = random_batch(seed)
     log(f"[gpu] random batch {seed}: R={len(qlen)} page={page} rows={sum(qlen)} "
-        f"chunks={sum(c > 1 for c in qlen)} key split={keys or 'planned'} unit={unit or 'planned'} fused={fused}")
+        f"chunks={sum(c > 1 for c in qlen)} key split={keys or 'planned'} unit={unit or 'planned'} "
+        f"decode-first={first if first >= 0 else 'planned'} fused={fused}")
     wl = W.custom(prefix, qlen, page_size=page, seed=seed, name=f"random{seed}")
     b, li = wl.batch, wl.layer(0)
     mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, keys)
     mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, unit)
+    mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, first)
     try:
         g = run_layer(b, li, fused=fused)
     finally:
         mla.debug_set(mla.MLA_DEBUG_CHUNK_KEYS, 0)
         mla.debug_set(mla.MLA_DEBUG_DEC_UNIT, 0)
+        mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, -1)
     pool_ref, out_ref, lse_ref = oracle.step(b, li, W.SOFTMAX_SCALE)
     assert np.array_equal(g.pool_np(), pool_ref), "append: pool differs from the oracle"
     assert_close(g.out_np(), out_ref, g.lse_np(), lse_ref, what=wl.name)

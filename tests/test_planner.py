@@ -32,7 +32,7 @@ def harness(tmp_path_factory):
     return exe
 
 
-def plan(exe, batches, route=None, chunk_keys=None, dec_unit=None):
+def plan(exe, batches, route=None, chunk_keys=None, dec_unit=None, dec_first=None):
     text = "".join(f"{ncu} {P} {len(q)} " + " ".join(f"{a} {b}" for a, b in zip(q, p)) + "\n"
                    for ncu, P, q, p in batches)
     env = dict(os.environ)
@@ -42,6 +42,8 @@ def plan(exe, batches, route=None, chunk_keys=None, dec_unit=None):
         env["PLAN_CHUNK_KEYS"] = str(chunk_keys)
     if dec_unit is not None:
         env["PLAN_DEC_UNIT"] = str(dec_unit)
+    if dec_first is not None:
+        env["PLAN_DEC_FIRST"] = str(dec_first)
     out = subprocess.run([exe], input=text, capture_output=True, text=True, check=True,
                          env=env).stdout.splitlines()
     assert len(out) == len(batches)
@@ -54,7 +56,7 @@ def plan(exe, batches, route=None, chunk_keys=None, dec_unit=None):
         keys = ["ks", "n_chunk_items", "n_dec_items", "U", "dec_total", "grid", "hsplit", "chunk_split",
                 "dec_split", "bytes", "off_co", "off_cml", "off_do", "off_dml"]
         d = {k: int(v) for k, v in zip(keys, f[1:15])}
-        d["us"] = float(f[15])
+        d["us"], d["est"], d["first"] = float(f[15]), float(f[17]), int(f[18])
         res.append(d)
     return res
 
