@@ -21,8 +21,9 @@ Usage: python -m paper_2607_02043_amd.timeline --config 5 [--chunk C] [--keys KS
 [--dump FILE.npy]
 (--keys, --unit and --first force the chunk key split, the decode unit size
 and the decode-first workgroups, as the MLA_DEBUG_CHUNK_KEYS,
-MLA_DEBUG_DEC_UNIT and MLA_DEBUG_DEC_FIRST debug knobs; --dump saves the
-stamps of the last launch, one row per item.)
+MLA_DEBUG_DEC_UNIT and MLA_DEBUG_DEC_FIRST debug knobs, --first 0 being the
+chunk-first schedule; --dump saves the stamps of the last launch, one row
+per item.)
 """
 import argparse
 import ctypes
@@ -43,7 +44,7 @@ MAX_ITEMS = 1 << 16
 TICK_US = 0.01    # the real-time counter runs at 100 MHz
 
 
-def run(config, chunk=None, keys=0, calls=3, unit=0, first=0, dump=None):
+def run(config, chunk=None, keys=0, calls=3, unit=0, first=-1, dump=None):
     import torch
 
     from paper_2607_02043_amd import workloads as W
@@ -73,7 +74,7 @@ def run(config, chunk=None, keys=0, calls=3, unit=0, first=0, dump=None):
         torch.cuda.synchronize()
     finally:
         for k, _ in knobs:
-            mla.debug_set(k, 0)
+            mla.debug_set(k, -1)  # each knob's default
     buf = np.zeros((MAX_ITEMS, SLOTS), dtype=np.uint64)
     if L.mla_trace_read(buf.ctypes.data, buf.nbytes) != 0:
         raise SystemExit("reading the trace buffer failed")
@@ -163,7 +164,7 @@ def main():
     ap.add_argument("--chunk", type=int, default=None)
     ap.add_argument("--keys", type=int, default=0)
     ap.add_argument("--unit", type=int, default=0)
-    ap.add_argument("--first", type=int, default=0)
+    ap.add_argument("--first", type=int, default=-1)
     ap.add_argument("--dump", default=None)
     args = ap.parse_args()
     wl, res = run(args.config, args.chunk, args.keys, unit=args.unit, first=args.first, dump=args.dump)
