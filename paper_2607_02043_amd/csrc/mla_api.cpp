@@ -151,6 +151,7 @@ constexpr double kDecTileUs = 3.5;      // one decode tile of a unit (the two un
 constexpr double kDecUnitUs = 8.0;      // decode item start-up
 constexpr double kDecTileLoUs = 2.65;   // a decode tile when few workgroups stream (per-CU rate bound)
 constexpr double kTwoQueueGain = 0.03;  // decode-first workgroups only for at least this much less time
+constexpr double kTwoQueueMinUs = 5.0;  // and at least this many microseconds less
 constexpr double kMergeGBs = 3000.0;    // partial rows written and merged, whole chip
 constexpr double kMergeLaunchUs = 7.0;  // the merge launch itself, when any row is split
 constexpr int kCounterBytes = 256;     // work-queue counters at the start of the workspace
@@ -651,7 +652,7 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
         // tail of the chunk-first schedule.  Closed form for every key split
         // and D, then a queue simulation of the best pair (and of the
         // runner-up when within 5%), taken when it beats the chunk-first
-        // plan by kTwoQueueGain (or D is forced).
+        // plan by kTwoQueueGain and kTwoQueueMinUs (or D is forced).
         const long long forced_first = debug_value(MLA_DEBUG_DEC_FIRST).load(std::memory_order_relaxed);
         if (!chunks.empty() && dec_total > 0 && forced_first != 0) {
             const long long forced_unit = debug_value(MLA_DEBUG_DEC_UNIT).load(std::memory_order_relaxed);
@@ -714,7 +715,8 @@ int make_plan_uncached(const mla_batch *b, const Shape &sh, int ncu, mla::ChunkR
                     pick = &tw;
                 }
             }
-            if (pick != nullptr && (forced_first > 0 || best_two < best * (1.0 - kTwoQueueGain))) {
+            if (pick != nullptr && (forced_first > 0 || (best_two < best * (1.0 - kTwoQueueGain) &&
+                                                         best_two < best - kTwoQueueMinUs))) {
                 best = best_two;
                 ks_best = cands[pick->ci].ks;
                 U_best = pick->U;
