@@ -7,8 +7,10 @@
 // attention (DeepSeek-V2-Lite, section 6).
 //
 // Work decomposition (one persistent launch for all rows of a step: one
-// 8-wavefront workgroup per CU takes work items from an atomic counter,
-// chunk items first, then decode items):
+// 8-wavefront workgroup per CU takes work items from two atomic counters,
+// one per kind; the workgroups the host plans as decode-first start on the
+// decode items, the others on the chunk items, and each moves to the other
+// kind when its own runs out):
 //   * chunk rows (c > 1): an item is a block of 8 query tokens (one per
 //     wave, 16 head rows each) times a range of its causal keys.  32-key
 //     tiles stream through a 3-slot global -> LDS DMA ring; scores on bf16
