@@ -129,6 +129,10 @@ def check_plan(batch, d, route=None):
         units = 0
         assert d["n_dec_items"] == 0 and d["dec_split"] == 0
     assert 1 <= d["grid"] <= ncu and d["grid"] <= d["n_chunk_items"] + d["n_dec_items"]
+    # decode-first workgroups: only with both kinds of work, at most the launch
+    assert 0 <= d["first"] <= d["grid"]
+    if d["n_chunk_items"] == 0 or d["n_dec_items"] == 0:
+        assert d["first"] == 0
     # workspace: counters, then 256-byte aligned partial slots
     off = COUNTER_BYTES
     align = lambda v: (v + 255) // 256 * 256
@@ -173,6 +177,25 @@ def test_plans_of_the_benchmark_workloads(harness):
     res = res[::reps]
     # decode-only: one item of two equal units per CU
     assert res[3]["n_chunk_items"] == 0 and res[3]["n_dec_items"] == 256
+    # the 2048-token chunk beside 256 long decode rows streams the decode work
+    # beside the chunk from the start, one decode item per decode-first
+    # workgroup; workload 3 (whose launch its longest chunk item bounds) keeps
+    # the chunk-first schedule
+    assert res[4]["first"] > 0 and res[4]["n_dec_items"] == res[4]["first"]
+    assert res[2]["first"] == 0
+
+
+@pytest.mark.parametrize("first", [0, 1, 96, 100000])
+def test_forced_decode_first_workgroups(harness, first):
+    """The debug knob fixes the decode-first workgroups (0: none), capped by
+    the launch; without both kinds of work there are none.  The plan still
+    respects every limit."""
+    rng = np.random.default_rng(first % 1000 + 7)
+    batches = [random_batch(rng, 256) for _ in range(40)]
+    for batch, d in zip(batches, plan(harness, batches, dec_first=first)):
+        check_plan(batch, d)
+        if d["n_chunk_items"] > 0 and d["n_dec_items"] > 0:
+            assert d["first"] == min(first, d["grid"])
 
 
 def test_single_request_extremes(harness):
@@ -275,7 +298,7 @@ def _serving_plans(harness, batches):
         keys = ["ks", "n_chunk_items", "n_dec_items", "U", "dec_total", "grid", "hsplit", "chunk_split",
                 "dec_split", "bytes", "off_co", "off_cml", "off_do", "off_dml"]
         d = {k: int(v) for k, v in zip(keys, f[1:15])}
-        d["us"], d["warm"] = float(f[15]), int(f[16])
+        d["us"], d["warm"], d["first"] = float(f[15]), int(f[16]), int(f[18])
         res.append(d)
     assert len(res) == len(batches)
     return res
@@ -307,12 +330,14 @@ def test_serving_sequence_plans_warm_and_stays_valid(harness):
     assert plans[0]["warm"] == 0 and plans[-1]["warm"] == 0
     warm = [d for d in plans[1:40] if d["warm"]]
     assert len(warm) >= 30
-    anchor = None  # a warm plan keeps the key split and unit size of the last full plan
+    anchor = None  # a warm plan keeps the key split, unit size and decode-first workgroups of the last full plan
     for d in plans:
         if d["warm"]:
-            assert (d["ks"], d["U"]) == anchor
+            assert (d["ks"], d["U"]) == anchor[:2]
+            if d["n_chunk_items"] > 0 and d["n_dec_items"] > 0:
+                assert d["first"] == min(anchor[2], d["grid"])
         else:
-            anchor = (d["ks"], d["U"])
+            anchor = (d["ks"], d["U"], d["first"])
     assert float(np.median([d["us"] for d in warm])) < 50.0
 
 
