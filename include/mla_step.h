@@ -163,8 +163,11 @@ const char *mla_last_error(void);
 
 /* Device workspace (bytes) that mixed_step_attn / mixed_step need for this
  * batch, or 0 on invalid arguments (then mla_last_error says why; an empty
- * batch also needs 0 bytes).  Depends only on the host arrays and the
- * device's CU count.  The first 256 bytes hold the work-queue counters of the
+ * batch also needs 0 bytes).  Depends only on the host arrays, the
+ * device's CU count and the debug knobs that force the plan (a workspace
+ * sized under one setting of MLA_DEBUG_CHUNK_KEYS, MLA_DEBUG_DEC_UNIT or
+ * MLA_DEBUG_DEC_FIRST may be too small under another: the call then fails
+ * with MLA_ERR_WORKSPACE).  The first 256 bytes hold the work-queue counters of the
  * attention launch: they must be zero when a workspace is first used (e.g.
  * hipMemset once after allocating it), and every completed call leaves them
  * zero again.  The rest holds fp32 partial results of rows whose keys are
