@@ -31,9 +31,16 @@ def _noalloc_vs_workspace(wl):
     assert_close(g.out_np(), out_ref, g.lse_np(), lse_ref, what=wl.name + " (no-alloc)")
 
 
-def test_noalloc_matches_mixed_step_twice():
-    # the larger batch first (key splits: its partials use the scratch), then a smaller one
-    for wl in (W.config(2), W.config(1)):
-        log(f"[gpu] mixed_step_noalloc: {wl.name}")
-        _noalloc_vs_workspace(wl)
+@pytest.mark.parametrize("first", [-1, 64])
+def test_noalloc_matches_mixed_step_twice(first):
+    # the larger batch first (key splits: its partials use the scratch), then a
+    # smaller one; the planner's schedule, then 64 workgroups forced to start on
+    # the decode work (the scratch's decode-queue counter used and left zero)
+    mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, first)
+    try:
+        for wl in (W.config(2), W.config(1)):
+            log(f"[gpu] mixed_step_noalloc: {wl.name} (decode-first {first if first >= 0 else 'planned'})")
+            _noalloc_vs_workspace(wl)
+    finally:
+        mla.debug_set(mla.MLA_DEBUG_DEC_FIRST, -1)
 
